@@ -1,0 +1,115 @@
+"""Planted mistakes in the oracle must fail its pins (no GPU).
+
+Each case below edits a copy of oracle/orc.c in a temporary directory with
+one plausible mistake (a dropped term, a wrong operand, a transposed index,
+a wrong sign or rule), builds it, and runs a battery of the pins from
+test_oracle_pins.py against it.  The battery must fail for every mutant and
+pass for the unmodified source.  Nothing here touches the real oracle build.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import tracegen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "orc.c")
+HAND = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_examples.json")))
+PIN = json.load(open(os.path.join(ROOT, "tests", "golden", "model_shapes.json")))
+
+MUTANTS = [
+    ("p feature reads c", "x[1] = S[1] * (double)p;", "x[1] = S[1] * (double)c;"),
+    ("a3 term dropped", "  acc = acc + th[3] * x[3];\n", ""),
+    ("a2 sign flipped", "acc = acc + th[2] * x[2];", "acc = acc - th[2] * x[2];"),
+    ("a4 batch term n not n^2", "S[3] * (double)Q, (double)n * (double)n};\n    const double tm",
+     "S[3] * (double)Q, (double)n};\n    const double tm"),
+    ("tie goes to COMP", "const int seg = (tc > tm)", "const int seg = (tc >= tm)"),
+    ("share uses other segment", "const double f = dot5(th[ph][seg], x);",
+     "const double f = dot5(th[ph][1 - seg], x);"),
+    ("phase rule and/or", "if (p[i] > 1 || c[i] == 0) prefill = 1;",
+     "if (p[i] > 1 && c[i] == 0) prefill = 1;"),
+    ("beta not split", "x[0] = S[0] / (double)n;", "x[0] = S[0];"),
+    ("KV bytes missing K/V factor", "const int64_t s2 = 2 * L * hkv * d * kb;",
+     "const int64_t s2 = L * hkv * d * kb;"),
+    ("KV uses q heads", "const int64_t s2 = 2 * L * hkv * d * kb;",
+     "const int64_t s2 = 2 * L * hq * d * kb;"),
+    ("layer weights miss o proj", "h * d * (2 * hq + 2 * hkv)", "h * d * (hq + 2 * hkv)"),
+    ("attention constant doubled", "const int64_t s3 = 2 * L * hq * d;",
+     "const int64_t s3 = 4 * L * hq * d;"),
+    ("coefficient index transposed", "th[ph][s][k] = (double)coeffs[(ph * 2 + s) * 5 + k];",
+     "th[ph][s][k] = (double)coeffs[(s * 2 + ph) * 5 + k];"),
+    ("Q sums p not p^2", "sq += (int64_t)p[i] * (int64_t)p[i];", "sq += p[i];"),
+    ("output projection twice", "wb * (L * p_layer + V * h)", "wb * (L * p_layer + 2 * V * h)"),
+    ("empty regime 0", "if (regime) regime[b] = ORC_REGIME_EMPTY;", "if (regime) regime[b] = 0;"),
+    ("tenant sums of other segment", "if (tenant_sums) tenant_sums[tenant[i]] += f;",
+     "if (tenant_sums) tenant_sums[tenant[i]] += dot5(th[ph][1 - seg], x);"),
+    ("per-request p^2 uses p", "x[3] = S[3] * (double)p2;", "x[3] = S[3] * (double)p;"),
+]
+
+
+def coeff_vec(d):
+    return np.array(d["prefill_mem"] + d["prefill_comp"] + d["decode_mem"] + d["decode_comp"],
+                    np.float32)
+
+
+def battery(orc: oracle.Oracle):
+    """A fast subset of the pins; raises AssertionError on the first miss."""
+    th = coeff_vec(HAND["base_coeffs"])
+    by_name = {}
+    for ex in HAND["unit_shape_examples"]:
+        by_name[ex["name"]] = ex
+        t = th.copy()
+        if ex["coeff_override"]:
+            t[ex["coeff_override"]["index"]] = ex["coeff_override"]["value"]
+        off = np.array([0, len(ex["p"])], np.int64)
+        r = orc.attribute(off, ex["p"], ex["c"], [0] * len(ex["p"]), None, t, 1)
+        assert r["T"][0] == ex["T"] and r["regime"][0] == ex["regime"]
+        assert list(r["share"]) == ex["shares"]
+    tt = HAND["tenant_trace"]
+    tr = tracegen.from_batches([(by_name[n]["p"], by_name[n]["c"]) for n in tt["batches"]],
+                               tt["tenants"], tt["n_tenants"])
+    r = orc.attribute(tr.offsets, tr.p, tr.c, tr.tenant, None, th, tr.n_tenants)
+    assert list(r["tenant_sums"]) == tt["tenant_sums"]
+    se = HAND["shaped_examples"]
+    assert list(orc.shape_constants(se["shape"])) == se["S"]
+    ths = coeff_vec(se["coeffs"])
+    for ex in se["examples"]:
+        off = np.array([0, len(ex["p"])], np.int64)
+        r = orc.attribute(off, ex["p"], ex["c"], None, se["shape"], ths, 1)
+        assert r["T"][0] == ex["T"] and list(r["share"]) == ex["shares"]
+    # Llama 3.1 8B published parameter count and KV bytes per token
+    sh = tracegen.SHAPES["llama3.1-8b"]
+    S = orc.shape_constants(sh)
+    streamed = PIN["llama3_1_8b"]["total_parameters"] - sh["vocab"] * sh["hidden"] \
+        - (2 * sh["n_layers"] + 1) * sh["hidden"]
+    assert S[0] == 2 * streamed
+    assert S[2] == PIN["llama3_1_8b"]["kv_cache_bytes_per_token_bf16"]
+    # attention FLOPs: p^2 coefficient of the brute-force pair count
+    pairs2 = 3  # (q0,k0), (q1,k0), (q1,k1)
+    per_pair = sh["n_layers"] * sh["n_q_heads"] * 4 * sh["head_dim"]
+    assert S[3] == (pairs2 * per_pair - 2 * 1 * per_pair) / 2
+
+
+def _build(tmp_path, text, tag):
+    src = tmp_path / f"orc_{tag}.c"
+    src.write_text(text)
+    (tmp_path / "orc.h").write_text(open(os.path.join(ROOT, "oracle", "orc.h")).read())
+    so = tmp_path / f"liborc_{tag}.so"
+    oracle.build(str(so), str(src))
+    return oracle.Oracle(str(so))
+
+
+def test_battery_passes_on_real_source(tmp_path):
+    battery(_build(tmp_path, open(SRC).read(), "orig"))
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    text = open(SRC).read()
+    assert text.count(old) == 1, f"mutation anchor for '{name}' must be unique"
+    orc = _build(tmp_path, text.replace(old, new), "mut")
+    with pytest.raises((AssertionError, oracle.OracleError)):
+        battery(orc)
