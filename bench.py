@@ -1,0 +1,250 @@
+#!/usr/bin/env python3
+"""Benchmark: batched LLMVisor latency attribution on one MI355X.
+
+One step = one llmv_attribute call over the whole trace (per-request
+features, per-batch Eq. 1 evaluation and segment choice, per-request shares,
+per-tenant sums), inputs already resident in HBM.  Prints ONE JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload heavy-tailed]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "k_tiles_heavy-tailed_counters.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_08382_amd", "csrc", f)
+                  for f in ("kernels.hpp", "api.hip")]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(n_requests, n_batches):
+    """Bytes the method must move per step: p, c, tenant (int32) in and the
+    fp32 share out per request; the int64 offset in and the fp32 latency and
+    uint8 regime out per batch (plus the closing offset).  Tenant sums
+    (n_tenants doubles) are negligible and left out."""
+    return 16 * n_requests + 13 * n_batches + 8
+
+
+def traffic_from_profile(workload, n_req, n_b):
+    """HBM bytes per launch of the tile kernel from committed rocprofv3 PMC
+    counters, if they were taken on the current kernel source."""
+    try:
+        prof = json.load(open(PROFILE_COUNTERS))
+    except (OSError, ValueError):
+        return None
+    if prof.get("kernel_source_sha") != kernel_source_sha() or prof.get("workload") != workload:
+        return None
+    return prof.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(tr, coeffs, gpu_out, budget_s=30.0):
+    """The oracle (single thread, fp64) on the same host arrays, with the same
+    outputs as the GPU step, timed.  Its results then check the GPU step's
+    outputs on sampled batches and on the tenant sums."""
+    import numpy as np
+    import oracle
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity
+
+    nB = tr.n_batches
+    # bounded sample: a prefix of the batches sized to the time budget at an
+    # assumed ~20 ns per request, never more than the whole trace
+    max_req = int(budget_s / 20e-9)
+    nb = nB if tr.n_requests <= max_req else int(np.searchsorted(tr.offsets, max_req))
+    nb = max(1, min(nb, nB))
+    off = tr.offsets[:nb + 1]
+    nreq = int(off[-1])
+    log(f"[bench] oracle on {nb} batches / {nreq} requests ...")
+    t0 = time.perf_counter()
+    ref = oracle.attribute(off, tr.p[:nreq], tr.c[:nreq], tr.tenant[:nreq], tr.shape, coeffs,
+                           tr.n_tenants, ("T", "regime", "share", "tenant_sums"))
+    dt = time.perf_counter() - t0
+    rate = nreq / dt
+    # parity on a sample of batches (the oracle re-run on just those batches
+    # also gives both segments' values for the tie rule)
+    rng = np.random.default_rng(5)
+    bids = np.unique(rng.integers(0, nb, min(nb, 2000)))
+    so, sp, sc, st = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
+    sub = oracle.attribute(so, sp, sc, st, tr.shape, coeffs, tr.n_tenants)
+    assert np.array_equal(sub["T"], ref["T"][bids])
+    idx = np.concatenate([np.arange(off[b], off[b + 1]) for b in bids])
+    assert np.array_equal(sub["share"], ref["share"][idx])
+    stats = parity.compare(sub, tr.offsets, gpu_out["latency"], gpu_out["regime"],
+                           gpu_out["share_sample"](idx), None, batch_ids=bids)
+    if nb == nB:
+        e = parity.rel_err(gpu_out["tenant_sums"], ref["tenant_sums"])
+        stats["tenant"] = float(e.max())
+        assert stats["tenant"] <= parity.RTOL
+    sample = (f"full trace ({nreq} requests)" if nb == nB
+              else f"first {nb} of {nB} batches ({nreq} requests)")
+    return {"value": rate, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": sample, "seconds": round(dt, 3)}, stats
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="heavy-tailed")
+    ap.add_argument("--n-batches", type=int, default=None, help="override the batch count")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the attribution path "
+              "is built and measured on a single MI355X", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import tracegen
+    from paper_2608_08382_amd import llmv
+
+    llmv.load()
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    tr = tracegen.config_trace(args.workload, args.n_batches)
+    coeffs = tracegen.config_coeffs(args.workload)
+    log(f"[bench] {args.workload}: {tr.n_batches} batches, {tr.n_requests} requests, "
+        f"generated in {time.perf_counter() - t0:.1f}s")
+    dt = llmv.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    dev = dt.p.device
+    lat = torch.empty(tr.n_batches, dtype=torch.float32, device=dev)
+    reg = torch.empty(tr.n_batches, dtype=torch.uint8, device=dev)
+    share = torch.empty(tr.n_requests, dtype=torch.float32, device=dev)
+    tsum = torch.empty(tr.n_tenants, dtype=torch.float64, device=dev)
+    ws = llmv.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+    torch.cuda.synchronize()
+
+    def step():
+        llmv.llmv_attribute(dt, tr.shape, coeffs, lat, reg, share, tr.n_tenants, tsum, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K steps, HIP events on the stream the kernels run on:
+    # one pair around the whole region, one pair around each step's tile
+    # kernel (recorded by the library right before / after that launch)
+    hip = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    evs = [(hip.create(), hip.create()) for _ in range(args.steps)]
+    start, stop = hip.create(), hip.create()
+    torch.cuda.synchronize()
+    hip.record(start, stream)
+    for i in range(args.steps):
+        llmv.llmv_set_kernel_events(*evs[i])
+        step()
+    llmv.llmv_set_kernel_events(None, None)
+    hip.record(stop, stream)
+    torch.cuda.synchronize()
+    total_ms = hip.elapsed_ms(start, stop)
+    kern_ms = [hip.elapsed_ms(a, b) for a, b in evs]
+    ms_per_step = total_ms / args.steps
+    k_avg_ms = sum(kern_ms) / len(kern_ms)
+    value = tr.n_requests * args.steps / (total_ms / 1e3)
+    nbytes = algorithmic_bytes(tr.n_requests, tr.n_batches)
+    achieved = nbytes / (k_avg_ms / 1e3) / 1e9
+    log(f"[bench] {ms_per_step:.4f} ms/step, tile kernel {k_avg_ms:.4f} ms "
+        f"(min {min(kern_ms):.4f}), {achieved:.0f} GB/s algorithmic")
+
+    reg_host = reg.cpu().numpy()
+    regimes = np.bincount(reg_host[reg_host != 255], minlength=4)[:4]
+    gpu_out = {"latency": lat.cpu().numpy(), "regime": reg_host,
+               "tenant_sums": tsum.cpu().numpy(),
+               "share_sample": lambda idx: _gather(share, idx, tr.n_requests)}
+
+    traffic = traffic_from_profile(args.workload, tr.n_requests, tr.n_batches)
+    result = {
+        "metric": "attributed requests/sec on 1 MI355X; achieved HBM GB/s vs peak",
+        "value": value,
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "n_batches": tr.n_batches,
+                   "n_requests": tr.n_requests, "shape": tracegen.CONFIGS[args.workload][2],
+                   "n_tenants": tr.n_tenants, "outputs": "latency,regime,share,tenant_sums"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
+                     "traffic": traffic, "kernel": "k_tiles",
+                     "kernel_ms": k_avg_ms, "algorithmic_bytes": nbytes},
+        "regime_mix": {"prefill_mem": int(regimes[0]), "prefill_comp": int(regimes[1]),
+                       "decode_mem": int(regimes[2]), "decode_comp": int(regimes[3])},
+    }
+    if not args.no_cpu_baseline:
+        cb, stats = cpu_baseline(tr, coeffs, gpu_out)
+        result["cpu_baseline"] = cb
+        result["parity"] = {k: v for k, v in stats.items()}
+        log(f"[bench] oracle {cb['value']:.3e} req/s on {cb['cores']} core; parity {stats}")
+    print(json.dumps(result), flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime (ctypes)."""
+
+    def __init__(self):
+        import ctypes
+        self.ct = ctypes
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                 ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.events = []
+
+    def _ok(self, rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed with HIP error {rc}")
+
+    def create(self):
+        ev = self.ct.c_void_p()
+        self._ok(self.lib.hipEventCreate(self.ct.byref(ev)), "hipEventCreate")
+        self.events.append(ev)
+        return ev
+
+    def record(self, ev, stream):
+        self._ok(self.lib.hipEventRecord(ev, self.ct.c_void_p(stream)), "hipEventRecord")
+
+    def elapsed_ms(self, a, b):
+        ms = self.ct.c_float()
+        self._ok(self.lib.hipEventElapsedTime(self.ct.byref(ms), a, b), "hipEventElapsedTime")
+        return ms.value
+
+
+def _gather(share, idx, n):
+    import numpy as np
+    import torch
+    out = np.zeros(n, np.float32)
+    out[idx] = share[torch.from_numpy(idx).to(share.device)].cpu().numpy()
+    return out
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,170 @@
+/*
+ * llmv.h -- C ABI of libllmv, batched LLMVisor latency attribution on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The method (LLMVisor, Sec. 2.1, Eq. 1): a batch B of co-scheduled requests
+ * has latency
+ *     T_B = beta + a1*sum_i p_i + a2*sum_i c_i + a3*sum_i p_i^2 + a4*sum_i |B|
+ * with p_i the tokens request i processes in the step and c_i the context
+ * tokens it attends to (Sec. 2.1).  The form has two segments per phase
+ * (memory-bound MEM and compute-bound COMP), so four coefficient sets in all
+ * (Sec. 2.1).  Because T_B is a sum of per-request terms, each request's
+ * share f(i|B) is its own terms, the shares are nonnegative for nonnegative
+ * coefficients and add up to T_B, and a tenant's usage L_u is the sum of its
+ * requests' shares (Sec. 2, Problem formulation).  Features are scaled by
+ * constants proportional to FLOPs and bytes (Sec. 2.1), derived from a model
+ * shape (llmv_shape_constants).
+ *
+ * Readings of points the paper leaves open (the same in every entry point):
+ *   - a4 term: |B| per request, |B|^2 per batch (Eq. 1 sums |B| over i);
+ *   - beta: split equally, beta*S0/|B| per request;
+ *   - segment: COMP when T_COMP > T_MEM (strictly), else MEM; T_B is the
+ *     chosen segment's value, i.e. max(T_MEM, T_COMP);
+ *   - phase: PREFILL when any request has p_i > 1 or c_i == 0, else DECODE;
+ *   - an empty batch has T_B = 0 and regime LLMV_REGIME_EMPTY.
+ *
+ * Conventions for every entry point below:
+ *   - Pointers marked "device" must point to device memory of the current
+ *     HIP device; "host" pointers to host memory.  The caller owns all
+ *     memory; the library allocates nothing on these paths.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *     on it and the call returns without waiting; outputs are valid once the
+ *     stream has reached that point.  llmv_validate is the exception: it
+ *     waits for its own result.
+ *   - `ws` is a device workspace of at least llmv_workspace_size(...) bytes,
+ *     256-byte aligned.  Its contents need no initialisation and are
+ *     clobbered.  Two calls that overlap in time must not share a workspace.
+ *   - Return value: LLMV_OK, or a negative LLMV_E* code.  Host-side argument
+ *     checks run before anything is enqueued.  Device data are NOT checked
+ *     by the attribution calls: data outside the limits below is undefined
+ *     behaviour; check it with llmv_validate.  llmv_last_error() gives a
+ *     message for the calling thread's last failure.
+ */
+#ifndef LLMV_H
+#define LLMV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define LLMV_OK 0
+#define LLMV_EINVAL (-1)     /* bad host-side argument                        */
+#define LLMV_ERANGE (-2)     /* device data outside the limits (llmv_validate) */
+#define LLMV_EDEVICE (-3)    /* HIP runtime or launch error                   */
+#define LLMV_EWORKSPACE (-4) /* workspace too small or misaligned             */
+
+/* Phase / segment / regime numbering: regime = 2*phase + segment. */
+#define LLMV_PREFILL 0
+#define LLMV_DECODE 1
+#define LLMV_MEM 0
+#define LLMV_COMP 1
+#define LLMV_REGIME_EMPTY 255
+
+/* Data limits. */
+#define LLMV_P_MAX (1 << 20)       /* 1 <= p_i <= 2^20                         */
+#define LLMV_BATCH_MAX (1 << 22)   /* 0 <= |B| <= 2^22; c_i is any int32 >= 0  */
+#define LLMV_TENANTS_MAX (1 << 24) /* 1 <= n_tenants <= 2^24                   */
+
+/* Model shape (host struct).  Every field must be > 0.  weight_bytes and
+ * kv_bytes are bytes per element (2 for bf16). */
+typedef struct {
+  int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab,
+      weight_bytes, kv_bytes;
+} llmv_shape;
+
+/* A trace of batches in CSR form (host struct holding device pointers).
+ *   offsets [n_batches+1] int64, device: batch b holds requests
+ *           offsets[b] .. offsets[b+1]-1; offsets[0] == 0, non-decreasing,
+ *           offsets[n_batches] == n_requests.
+ *   p, c    [n_requests] int32, device: tokens processed this step (p_i) and
+ *           context tokens attended (c_i), Sec. 2.1.
+ *   tenant  [n_requests] int32, device, or NULL when no tenant sums are
+ *           requested: 0 <= tenant[i] < n_tenants.                        */
+typedef struct {
+  int64_t n_batches, n_requests;
+  const int64_t *offsets;
+  const int32_t *p, *c, *tenant;
+} llmv_trace;
+
+/* Host only; enqueues nothing.  Shape constants S[0..3] (host array):
+ *   P_layer = hidden*head_dim*(2*Hq + 2*Hkv) + 3*hidden*ffn
+ *   S0 = weight_bytes*(n_layers*P_layer + vocab*hidden)  weight bytes per step
+ *   S1 = 2*n_layers*P_layer                            linear FLOPs per token
+ *   S2 = 2*n_layers*Hkv*head_dim*kv_bytes              KV bytes per context token
+ *   S3 = 2*n_layers*Hq*head_dim                        causal attention FLOPs per p^2
+ * (Sec. 2.1: features proportional to FLOPs and I/O).  shape == NULL gives
+ * (1,1,1,1), i.e. Eq. 1 on the raw sums.  LLMV_EINVAL for a field <= 0 or a
+ * constant >= 2^53. */
+int llmv_shape_constants(const llmv_shape *shape, double S[4]);
+
+/* Bytes of device workspace the calls below need for a trace of this size
+ * on the current device (0 if none).  Depends on the device's compute-unit
+ * count; query it on the device that will run the call. */
+size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
+
+/* Batched attribution (Sec. 2 Problem formulation; Sec. 2.1, Eq. 1).
+ *   trace     host struct, device arrays as above.
+ *   shape     host, or NULL for the unit shape.
+ *   coeffs    host, 20 finite fp32: theta[phase][segment][k] at index
+ *             (phase*2 + segment)*5 + k, k = (beta, a1, a2, a3, a4).
+ *   latency   device [n_batches] fp32 T_B, or NULL.
+ *   regime    device [n_batches] uint8 2*phase+segment / LLMV_REGIME_EMPTY,
+ *             or NULL.
+ *   share     device [n_requests] fp32 f(i|B), or NULL.
+ *   n_tenants number of tenant ids; needed when tenant_sums != NULL.
+ *   tenant_sums device [n_tenants] fp64 L_u, or NULL.  Overwritten (not
+ *             accumulated); needs trace->tenant.
+ * Shares are evaluated in fp64 and rounded once to fp32; tenant sums add the
+ * fp64 shares.  Every output is independent of the others being requested. */
+int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
+                   const float coeffs[20], float *latency, uint8_t *regime,
+                   float *share, int32_t n_tenants, double *tenant_sums,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/* Request and batch features (Sec. 2.1), structure of arrays:
+ *   x_req   device [5][n_requests] fp32, element k of request i at
+ *           x_req[k*n_requests + i]: (S0/|B|, S1*p_i, S2*c_i, S3*p_i^2, |B|),
+ *           or NULL.
+ *   x_batch device [5][n_batches] fp64: the batch sums
+ *           (S0, S1*sum p, S2*sum c, S3*sum p^2, |B|^2), zeros for an empty
+ *           batch, or NULL.
+ * Dotting x with a coefficient set gives Eq. 1's value (batch) or share
+ * (request).  trace->tenant is ignored. */
+int llmv_features(const llmv_trace *trace, const llmv_shape *shape, float *x_req,
+                  double *x_batch, void *ws, size_t ws_bytes, void *stream);
+
+/* Tenant sums of given shares (Sec. 2, Problem formulation: L_u):
+ *   tenant  device [n] int32 in [0, n_tenants);  share device [n] fp32;
+ *   tenant_sums device [n_tenants] fp64, overwritten. */
+int llmv_tenant_sums(const int32_t *tenant, const float *share, int64_t n,
+                     int32_t n_tenants, double *tenant_sums, void *ws,
+                     size_t ws_bytes, void *stream);
+
+/* Checks the device data of a trace against the limits above: offsets
+ * (start at 0, non-decreasing, end at n_requests, batch sizes <= 2^22),
+ * 1 <= p <= 2^20, c >= 0, and 0 <= tenant < n_tenants when trace->tenant is
+ * not NULL.  Waits for the stream.  LLMV_OK when all hold, LLMV_ERANGE when
+ * any does not, or an argument / device error code. */
+int llmv_validate(const llmv_trace *trace, int32_t n_tenants, void *ws,
+                  size_t ws_bytes, void *stream);
+
+/* Message for the calling thread's last non-zero return (static storage,
+ * valid until that thread's next call). */
+const char *llmv_last_error(void);
+
+/* Measurement hook, not part of the method.  For callers that time the main
+ * kernel on its own: while set (per calling thread), llmv_attribute and
+ * llmv_features record `before` (a hipEvent_t) on their stream right before
+ * the tile kernel is enqueued and `after` right after it.  Pass NULL, NULL
+ * to stop.  The events are the caller's; the library does not own them. */
+int llmv_set_kernel_events(void *before, void *after);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LLMV_H */

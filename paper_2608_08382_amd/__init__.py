@@ -1,0 +1,9 @@
+"""MI355X-native batched latency attribution (LLMVisor, Sec. 2.1, Eq. 1).
+
+The computation lives in libllmv.so (HIP kernels for gfx950, C ABI in
+include/llmv.h); ``llmv`` is its ctypes binding.
+"""
+from . import llmv  # noqa: F401
+from .llmv import (DeviceTrace, LlmvError, attribute, features, tenant_sums,  # noqa: F401
+                   llmv_attribute, llmv_features, llmv_last_error, llmv_shape_constants,
+                   llmv_tenant_sums, llmv_validate, llmv_workspace_size, workspace)

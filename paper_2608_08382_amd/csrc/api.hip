@@ -1,0 +1,369 @@
+// api.hip -- host side of the libllmv C ABI (include/llmv.h): argument
+// checks, shape constants, workspace layout and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+
+#include "kernels.hpp"
+#include "llmv.h"
+
+using namespace llmv;
+
+namespace {
+
+thread_local char g_err[512] = "";
+thread_local hipEvent_t g_ev_before = nullptr;  // measurement hook
+thread_local hipEvent_t g_ev_after = nullptr;
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(LLMV_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                       \
+  do {                                            \
+    hipError_t e_ = (expr);                       \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+constexpr int kBlocksPerCu = 4;   // persistent workgroups per compute unit
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Compute units of the current device (cached per device).
+int device_cus(int* out) {
+  static std::mutex m;
+  static int cache[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(LLMV_EDEVICE, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> g(m);
+  if (!cache[dev]) {
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    cache[dev] = cus > 0 ? cus : 1;
+  }
+  *out = cache[dev];
+  return LLMV_OK;
+}
+
+// Persistent grid for n requests: enough workgroups to fill the device, but
+// no more than one per kCap requests.
+int64_t grid_for(int64_t n, int cus) {
+  int64_t g = (int64_t)cus * kBlocksPerCu;
+  if (g > kMaxGrid) g = kMaxGrid;
+  const int64_t by_work = (n + kCap - 1) / kCap;
+  if (by_work < g) g = by_work;
+  return g < 1 ? 1 : g;
+}
+
+bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
+
+struct Layout {
+  size_t wg_first, cnt, partials, part2, flag, total;
+};
+
+// Workspace layout shared by every entry point.
+Layout layout(int64_t grid, int32_t T) {
+  Layout L{};
+  size_t o = 0;
+  L.wg_first = o;
+  o += align_up((size_t)(grid + 1) * sizeof(int64_t));
+  const int64_t chunks = T > 0 ? (T + kTenantChunk - 1) / kTenantChunk : 0;
+  L.cnt = o;
+  o += align_up((size_t)(chunks > 0 ? chunks : 1) * sizeof(uint32_t));
+  L.partials = o;
+  if (lds_hist(T)) o += align_up((size_t)grid * (size_t)T * sizeof(double));
+  L.part2 = o;
+  if (lds_hist(T)) o += align_up((size_t)chunks * kReduceSplit * kTenantChunk * sizeof(double));
+  L.flag = o;
+  o += align_up(sizeof(int));
+  L.total = o;
+  return L;
+}
+
+int shape_constants(const llmv_shape* sh, double S[4]) {
+  if (!sh) {
+    S[0] = S[1] = S[2] = S[3] = 1.0;
+    return LLMV_OK;
+  }
+  const int32_t f[9] = {sh->n_layers, sh->hidden, sh->n_q_heads, sh->n_kv_heads, sh->head_dim,
+                        sh->ffn, sh->vocab, sh->weight_bytes, sh->kv_bytes};
+  for (int i = 0; i < 9; ++i)
+    if (f[i] <= 0) return fail(LLMV_EINVAL, "shape field %d is %d; every field must be > 0", i, f[i]);
+  // All products in int64: at most a few 2^31-bounded fields each; the
+  // results are checked against 2^53 so they convert to fp64 exactly.
+  const long double Ld = sh->n_layers, hd = sh->hidden, hq = sh->n_q_heads, hkv = sh->n_kv_heads,
+                    dd = sh->head_dim, ff = sh->ffn, vv = sh->vocab, wb = sh->weight_bytes,
+                    kb = sh->kv_bytes;
+  const long double layer = hd * dd * (2 * hq + 2 * hkv) + 3 * hd * ff;
+  const long double c0 = wb * (Ld * layer + vv * hd), c1 = 2 * Ld * layer,
+                    c2 = 2 * Ld * hkv * dd * kb, c3 = 2 * Ld * hq * dd;
+  const long double lim = 9007199254740992.0L;  // 2^53
+  if (c0 >= lim || c1 >= lim || c2 >= lim || c3 >= lim)
+    return fail(LLMV_EINVAL, "shape constants exceed 2^53");
+  const int64_t L = sh->n_layers, h = sh->hidden, q = sh->n_q_heads, kv = sh->n_kv_heads,
+                d = sh->head_dim;
+  const int64_t p_layer = h * d * (2 * q + 2 * kv) + 3 * h * (int64_t)sh->ffn;
+  S[0] = (double)((int64_t)sh->weight_bytes * (L * p_layer + (int64_t)sh->vocab * h));
+  S[1] = (double)(2 * L * p_layer);
+  S[2] = (double)(2 * L * kv * d * (int64_t)sh->kv_bytes);
+  S[3] = (double)(2 * L * q * d);
+  return LLMV_OK;
+}
+
+int check_trace(const llmv_trace* tr, bool need_tenant) {
+  if (!tr) return fail(LLMV_EINVAL, "trace is NULL");
+  if (tr->n_batches < 0 || tr->n_requests < 0)
+    return fail(LLMV_EINVAL, "negative sizes (n_batches=%lld, n_requests=%lld)",
+                (long long)tr->n_batches, (long long)tr->n_requests);
+  if (!tr->offsets) return fail(LLMV_EINVAL, "trace offsets is NULL");
+  if (tr->n_requests > 0 && (!tr->p || !tr->c)) return fail(LLMV_EINVAL, "trace p or c is NULL");
+  if (need_tenant && tr->n_requests > 0 && !tr->tenant)
+    return fail(LLMV_EINVAL, "tenant sums requested but trace tenant is NULL");
+  auto aligned = [](const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; };
+  if (!aligned(tr->p) || !aligned(tr->c) || (tr->tenant && !aligned(tr->tenant)))
+    return fail(LLMV_EINVAL, "p, c and tenant must be 16-byte aligned");
+  return LLMV_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return LLMV_OK;
+  if (!ws) return fail(LLMV_EWORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)ws & (kAlign - 1)) != 0) return fail(LLMV_EWORKSPACE, "workspace not 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(LLMV_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+  return LLMV_OK;
+}
+
+template <int MODE, int HIST, bool SHARE>
+hipError_t launch_tiles(const Params& P, int64_t grid, size_t dyn, hipStream_t s) {
+  hipLaunchKernelGGL((k_tiles<MODE, HIST, SHARE>), dim3((unsigned)grid), dim3(kWG), dyn, s, P);
+  return hipGetLastError();
+}
+
+// Partition + tiles (+ tenant reduction) shared by attribute and features.
+int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_tenant,
+              bool want_share, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int cus = 0;
+  int rc = device_cus(&cus);
+  if (rc) return rc;
+  const int64_t grid = grid_for(tr->n_requests, cus);
+  const int32_t Tl = want_tenant ? T : 0;
+  const Layout L = layout(grid, Tl);
+  rc = check_ws(ws, ws_bytes, L.total);
+  if (rc) return rc;
+  char* base = (char*)ws;
+  int64_t* wg_first = (int64_t*)(base + L.wg_first);
+  uint32_t* cnt = (uint32_t*)(base + L.cnt);
+  const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
+  const int n_cnt = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
+
+  P.wg_first = wg_first;
+  P.partials = hist == HIST_LDS ? (double*)(base + L.partials) : nullptr;
+
+  const int64_t step = tr->n_requests > 0 ? (tr->n_requests + grid - 1) / grid : 1;
+  {
+    const int64_t work = tr->n_batches + 1;
+    int64_t blocks = (work + kWG - 1) / kWG;
+    if (blocks > 4096) blocks = 4096;
+    double* zero_buf = hist == HIST_GLOBAL ? P.tenant_sums : nullptr;
+    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, stream, tr->offsets,
+                       tr->n_batches, step, (int)grid, wg_first, cnt, n_cnt, zero_buf,
+                       (int64_t)(hist == HIST_GLOBAL ? T : 0));
+    HIP_TRY(hipGetLastError(), "k_partition launch");
+  }
+
+  const size_t dyn = hist == HIST_LDS ? (size_t)T * sizeof(double) : 0;
+  if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
+  hipError_t e = hipSuccess;
+  if (mode == MODE_FEAT) {
+    e = launch_tiles<MODE_FEAT, HIST_NONE, false>(P, grid, 0, stream);
+  } else if (hist == HIST_NONE) {
+    e = want_share ? launch_tiles<MODE_ATTR, HIST_NONE, true>(P, grid, dyn, stream)
+                   : launch_tiles<MODE_ATTR, HIST_NONE, false>(P, grid, dyn, stream);
+  } else if (hist == HIST_LDS) {
+    e = want_share ? launch_tiles<MODE_ATTR, HIST_LDS, true>(P, grid, dyn, stream)
+                   : launch_tiles<MODE_ATTR, HIST_LDS, false>(P, grid, dyn, stream);
+  } else {
+    e = want_share ? launch_tiles<MODE_ATTR, HIST_GLOBAL, true>(P, grid, dyn, stream)
+                   : launch_tiles<MODE_ATTR, HIST_GLOBAL, false>(P, grid, dyn, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "k_tiles launch");
+  if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
+
+  if (hist == HIST_LDS) {
+    hipLaunchKernelGGL(k_tenant_reduce, dim3(kReduceSplit, (unsigned)n_cnt), dim3(kWG), 0, stream,
+                       (const double*)P.partials, (int)grid, (int)T, (double*)(base + L.part2),
+                       cnt, P.tenant_sums);
+    HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+  }
+  return LLMV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* llmv_last_error(void) { return g_err; }
+
+int llmv_set_kernel_events(void* before, void* after) {
+  if ((before == nullptr) != (after == nullptr))
+    return fail(LLMV_EINVAL, "set both events or neither");
+  g_ev_before = (hipEvent_t)before;
+  g_ev_after = (hipEvent_t)after;
+  return LLMV_OK;
+}
+
+int llmv_shape_constants(const llmv_shape* shape, double S[4]) {
+  if (!S) return fail(LLMV_EINVAL, "S is NULL");
+  return shape_constants(shape, S);
+}
+
+size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
+  (void)n_batches;
+  int cus = 0;
+  if (device_cus(&cus)) return 0;
+  const int64_t n = n_requests > 0 ? n_requests : 0;
+  return layout(grid_for(n, cus), n_tenants > 0 ? n_tenants : 0).total;
+}
+
+int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[20],
+                   float* latency, uint8_t* regime, float* share, int32_t n_tenants,
+                   double* tenant_sums, void* ws, size_t ws_bytes, void* stream) {
+  const bool want_tenant = tenant_sums != nullptr;
+  int rc = check_trace(trace, want_tenant);
+  if (rc) return rc;
+  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
+  for (int i = 0; i < 20; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
+  if (want_tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
+  if (share && ((uintptr_t)share & 15u)) return fail(LLMV_EINVAL, "share must be 16-byte aligned");
+  Params P{};
+  rc = shape_constants(shape, P.S);
+  if (rc) return rc;
+  for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[i];
+  P.off = trace->offsets;
+  P.p = trace->p;
+  P.c = trace->c;
+  P.tenant = want_tenant ? trace->tenant : nullptr;
+  P.nB = trace->n_batches;
+  P.N = trace->n_requests;
+  P.latency = latency;
+  P.regime = regime;
+  P.share = share;
+  P.tenant_sums = tenant_sums;
+  P.n_tenants = want_tenant ? n_tenants : 0;
+  if (!latency && !regime && !share && !want_tenant) return LLMV_OK;  // nothing requested
+  return run_tiles(MODE_ATTR, trace, P, n_tenants, want_tenant, share != nullptr, ws, ws_bytes,
+                   (hipStream_t)stream);
+}
+
+int llmv_features(const llmv_trace* trace, const llmv_shape* shape, float* x_req,
+                  double* x_batch, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_trace(trace, false);
+  if (rc) return rc;
+  Params P{};
+  rc = shape_constants(shape, P.S);
+  if (rc) return rc;
+  P.off = trace->offsets;
+  P.p = trace->p;
+  P.c = trace->c;
+  P.nB = trace->n_batches;
+  P.N = trace->n_requests;
+  P.x_req = x_req;
+  P.x_batch = x_batch;
+  if (!x_req && !x_batch) return LLMV_OK;
+  return run_tiles(MODE_FEAT, trace, P, 0, false, false, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32_t n_tenants,
+                     double* tenant_sums, void* ws, size_t ws_bytes, void* stream) {
+  if (n < 0) return fail(LLMV_EINVAL, "n=%lld is negative", (long long)n);
+  if (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX)
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
+  if (!tenant_sums) return fail(LLMV_EINVAL, "tenant_sums is NULL");
+  if (n > 0 && (!tenant || !share)) return fail(LLMV_EINVAL, "tenant or share is NULL");
+  hipStream_t s = (hipStream_t)stream;
+  int cus = 0;
+  int rc = device_cus(&cus);
+  if (rc) return rc;
+  const int64_t grid = grid_for(n, cus);
+  const Layout L = layout(grid, n_tenants);
+  rc = check_ws(ws, ws_bytes, L.total);
+  if (rc) return rc;
+  char* base = (char*)ws;
+  uint32_t* cnt = (uint32_t*)(base + L.cnt);
+  const int n_cnt = (n_tenants + kTenantChunk - 1) / kTenantChunk;
+  const bool lds = lds_hist(n_tenants);
+  // Clear the counters (and the output for the atomics path) with the
+  // partition kernel on an empty batch list.
+  hipLaunchKernelGGL(k_partition, dim3(16), dim3(kWG), 0, s, (const int64_t*)nullptr, (int64_t)-1,
+                     (int64_t)1, 0, (int64_t*)(base + L.wg_first), cnt, n_cnt,
+                     lds ? (double*)nullptr : tenant_sums, (int64_t)(lds ? 0 : n_tenants));
+  HIP_TRY(hipGetLastError(), "k_partition launch");
+  if (lds) {
+    double* partials = (double*)(base + L.partials);
+    hipLaunchKernelGGL(k_tenant_hist<HIST_LDS>, dim3((unsigned)grid), dim3(kWG),
+                       (size_t)n_tenants * sizeof(double), s, tenant, share, n, n_tenants,
+                       partials, tenant_sums);
+    HIP_TRY(hipGetLastError(), "k_tenant_hist launch");
+    hipLaunchKernelGGL(k_tenant_reduce, dim3(kReduceSplit, (unsigned)n_cnt), dim3(kWG), 0, s,
+                       (const double*)partials, (int)grid, (int)n_tenants,
+                       (double*)(base + L.part2), cnt, tenant_sums);
+    HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+  } else {
+    hipLaunchKernelGGL(k_tenant_hist<HIST_GLOBAL>, dim3((unsigned)grid), dim3(kWG), 0, s, tenant,
+                       share, n, n_tenants, (double*)nullptr, tenant_sums);
+    HIP_TRY(hipGetLastError(), "k_tenant_hist launch");
+  }
+  return LLMV_OK;
+}
+
+int llmv_validate(const llmv_trace* trace, int32_t n_tenants, void* ws, size_t ws_bytes,
+                  void* stream) {
+  int rc = check_trace(trace, false);
+  if (rc) return rc;
+  if (trace->tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
+  hipStream_t s = (hipStream_t)stream;
+  int cus = 0;
+  rc = device_cus(&cus);
+  if (rc) return rc;
+  const Layout L = layout(grid_for(trace->n_requests, cus), 0);
+  rc = check_ws(ws, ws_bytes, L.flag + sizeof(int));
+  if (rc) return rc;
+  int* flag = (int*)((char*)ws + L.flag);
+  hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, flag, 1);
+  HIP_TRY(hipGetLastError(), "k_zero_i32 launch");
+  const int64_t work = trace->n_requests > trace->n_batches ? trace->n_requests : trace->n_batches;
+  int64_t blocks = (work + kWG - 1) / kWG;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_validate, dim3((unsigned)blocks), dim3(kWG), 0, s, trace->offsets,
+                     trace->n_batches, trace->n_requests, trace->p, trace->c, trace->tenant,
+                     n_tenants, (int)LLMV_BATCH_MAX, (int)LLMV_P_MAX, flag);
+  HIP_TRY(hipGetLastError(), "k_validate launch");
+  int h = 0;
+  HIP_TRY(hipMemcpyAsync(&h, flag, sizeof(int), hipMemcpyDeviceToHost, s), "hipMemcpyAsync");
+  HIP_TRY(hipStreamSynchronize(s), "hipStreamSynchronize");
+  if (h) return fail(LLMV_ERANGE, "trace data outside the limits");
+  return LLMV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,237 @@
+"""ctypes binding of libllmv (include/llmv.h).
+
+Argument marshalling only: torch tensors are passed as device pointers, the
+current torch stream as the hipStream_t, and every step of the computation
+runs in the library's HIP kernels.  There is no CPU fallback: if the built
+library is missing, loading fails with an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libllmv.so")
+
+LLMV_OK, LLMV_EINVAL, LLMV_ERANGE, LLMV_EDEVICE, LLMV_EWORKSPACE = 0, -1, -2, -3, -4
+LLMV_PREFILL, LLMV_DECODE = 0, 1
+LLMV_MEM, LLMV_COMP = 0, 1
+LLMV_REGIME_EMPTY = 255
+LLMV_P_MAX = 1 << 20
+LLMV_BATCH_MAX = 1 << 22
+LLMV_TENANTS_MAX = 1 << 24
+
+EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute", "llmv_features",
+           "llmv_tenant_sums", "llmv_validate", "llmv_last_error", "llmv_set_kernel_events")
+
+
+class LlmvError(RuntimeError):
+    def __init__(self, code: int, func: str, msg: str):
+        super().__init__(f"{func} failed ({code}): {msg}")
+        self.code = code
+
+
+class llmv_shape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab",
+        "weight_bytes", "kv_bytes")]
+
+
+class llmv_trace(ctypes.Structure):
+    _fields_ = [("n_batches", ctypes.c_int64), ("n_requests", ctypes.c_int64),
+                ("offsets", ctypes.c_void_p), ("p", ctypes.c_void_p), ("c", ctypes.c_void_p),
+                ("tenant", ctypes.c_void_p)]
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Loads libllmv; raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(path):
+                raise RuntimeError(
+                    f"{path} is missing: build the HIP library first (__graft_entry__.build())")
+            lib = ctypes.CDLL(path)
+            P, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+            lib.llmv_shape_constants.argtypes = [P, P]
+            lib.llmv_workspace_size.argtypes = [i64, i64, i32]
+            lib.llmv_workspace_size.restype = sz
+            lib.llmv_attribute.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
+            lib.llmv_features.argtypes = [P, P, P, P, P, sz, P]
+            lib.llmv_tenant_sums.argtypes = [P, P, i64, i32, P, P, sz, P]
+            lib.llmv_validate.argtypes = [P, i32, P, sz, P]
+            lib.llmv_last_error.argtypes = []
+            lib.llmv_last_error.restype = ctypes.c_char_p
+            lib.llmv_set_kernel_events.argtypes = [P, P]
+            lib.llmv_set_kernel_events.restype = ctypes.c_int
+            for f in ("llmv_shape_constants", "llmv_attribute", "llmv_features",
+                      "llmv_tenant_sums", "llmv_validate"):
+                getattr(lib, f).restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+def _check(rc: int, func: str):
+    if rc != LLMV_OK:
+        raise LlmvError(rc, func, load().llmv_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch tensor")
+    if t.numel() and not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def make_shape(shape) -> llmv_shape | None:
+    """shape: None, a dict with the nine field names, or llmv_shape."""
+    if shape is None or isinstance(shape, llmv_shape):
+        return shape
+    return llmv_shape(*[int(shape[f[0]]) for f in llmv_shape._fields_])
+
+
+def _shape_ref(sh):
+    return None if sh is None else ctypes.byref(sh)
+
+
+class DeviceTrace:
+    """A trace resident in device memory (torch tensors on the current device)."""
+
+    def __init__(self, offsets, p, c, tenant=None):
+        self.offsets = offsets
+        self.p = p
+        self.c = c
+        self.tenant = tenant
+        self.n_batches = offsets.numel() - 1
+        self.n_requests = p.numel()
+
+    @classmethod
+    def from_host(cls, offsets, p, c, tenant=None, device="cuda"):
+        f = lambda a, dt: torch.as_tensor(a).to(device=device, dtype=dt).contiguous()
+        return cls(f(offsets, torch.int64), f(p, torch.int32), f(c, torch.int32),
+                   None if tenant is None else f(tenant, torch.int32))
+
+    def struct(self, with_tenant=True) -> llmv_trace:
+        return llmv_trace(self.n_batches, self.n_requests, _ptr(self.offsets), _ptr(self.p),
+                          _ptr(self.c), _ptr(self.tenant) if with_tenant else None)
+
+
+# ---------------------------------------------------------------- C ABI
+
+def llmv_shape_constants(shape=None):
+    S = (ctypes.c_double * 4)()
+    sh = make_shape(shape)
+    _check(load().llmv_shape_constants(_shape_ref(sh), S), "llmv_shape_constants")
+    return [S[i] for i in range(4)]
+
+
+def llmv_workspace_size(n_batches: int, n_requests: int, n_tenants: int) -> int:
+    return int(load().llmv_workspace_size(n_batches, n_requests, n_tenants))
+
+
+def llmv_attribute(trace: DeviceTrace, shape, coeffs, latency=None, regime=None, share=None,
+                   n_tenants: int = 0, tenant_sums=None, ws=None, stream=None):
+    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    sh = make_shape(shape)
+    tr = trace.struct(with_tenant=tenant_sums is not None)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().llmv_attribute(ctypes.byref(tr), _shape_ref(sh), co, _ptr(latency),
+                                 _ptr(regime), _ptr(share), int(n_tenants), _ptr(tenant_sums),
+                                 _ptr(ws), nbytes, _stream(stream)), "llmv_attribute")
+
+
+def llmv_features(trace: DeviceTrace, shape, x_req=None, x_batch=None, ws=None, stream=None):
+    sh = make_shape(shape)
+    tr = trace.struct(with_tenant=False)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().llmv_features(ctypes.byref(tr), _shape_ref(sh), _ptr(x_req), _ptr(x_batch),
+                                _ptr(ws), nbytes, _stream(stream)), "llmv_features")
+
+
+def llmv_tenant_sums(tenant, share, n_tenants: int, tenant_sums, ws=None, stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().llmv_tenant_sums(_ptr(tenant), _ptr(share), int(share.numel()),
+                                   int(n_tenants), _ptr(tenant_sums), _ptr(ws), nbytes,
+                                   _stream(stream)), "llmv_tenant_sums")
+
+
+def llmv_validate(trace: DeviceTrace, n_tenants: int = 0, ws=None, stream=None) -> int:
+    """Returns LLMV_OK or LLMV_ERANGE; raises on argument / device errors."""
+    tr = trace.struct(with_tenant=trace.tenant is not None)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    rc = load().llmv_validate(ctypes.byref(tr), int(n_tenants), _ptr(ws), nbytes,
+                              _stream(stream))
+    if rc not in (LLMV_OK, LLMV_ERANGE):
+        _check(rc, "llmv_validate")
+    return rc
+
+
+def llmv_last_error() -> str:
+    return load().llmv_last_error().decode()
+
+
+def llmv_set_kernel_events(before=None, after=None):
+    """before/after: hipEvent_t handles (ctypes.c_void_p or int), or None."""
+    _check(load().llmv_set_kernel_events(before, after), "llmv_set_kernel_events")
+
+
+# ---------------------------------------------------------------- helpers
+
+def workspace(n_batches: int, n_requests: int, n_tenants: int, device="cuda"):
+    """A device workspace tensor of llmv_workspace_size bytes (256-aligned)."""
+    n = llmv_workspace_size(n_batches, n_requests, n_tenants)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+
+
+def attribute(trace: DeviceTrace, shape, coeffs, n_tenants: int = 0,
+              outputs=("latency", "regime", "share", "tenant_sums"), ws=None):
+    """Allocates the requested outputs and runs llmv_attribute."""
+    dev = trace.p.device
+    out = {}
+    if "latency" in outputs:
+        out["latency"] = torch.empty(trace.n_batches, dtype=torch.float32, device=dev)
+    if "regime" in outputs:
+        out["regime"] = torch.empty(trace.n_batches, dtype=torch.uint8, device=dev)
+    if "share" in outputs:
+        out["share"] = torch.empty(trace.n_requests, dtype=torch.float32, device=dev)
+    if "tenant_sums" in outputs:
+        out["tenant_sums"] = torch.empty(n_tenants, dtype=torch.float64, device=dev)
+    if ws is None:
+        ws = workspace(trace.n_batches, trace.n_requests, n_tenants, dev)
+    llmv_attribute(trace, shape, coeffs, out.get("latency"), out.get("regime"), out.get("share"),
+                   n_tenants, out.get("tenant_sums"), ws)
+    return out
+
+
+def features(trace: DeviceTrace, shape, ws=None):
+    dev = trace.p.device
+    x_req = torch.empty((5, trace.n_requests), dtype=torch.float32, device=dev)
+    x_batch = torch.empty((5, trace.n_batches), dtype=torch.float64, device=dev)
+    if ws is None:
+        ws = workspace(trace.n_batches, trace.n_requests, 0, dev)
+    llmv_features(trace, shape, x_req, x_batch, ws)
+    return x_req, x_batch
+
+
+def tenant_sums(tenant, share, n_tenants: int, ws=None):
+    out = torch.empty(n_tenants, dtype=torch.float64, device=share.device)
+    if ws is None:
+        ws = workspace(0, share.numel(), n_tenants, share.device)
+    llmv_tenant_sums(tenant, share, n_tenants, out, ws)
+    return out

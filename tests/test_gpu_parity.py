@@ -1,0 +1,389 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Rules and tolerances: tests/parity.py."""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import tracegen
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HAND = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_examples.json")))
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def L():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_08382_amd import llmv
+    llmv.load()
+    torch.cuda.set_device(0)
+    return llmv
+
+
+def run_gpu(L, tr, shape, coeffs, n_tenants, outputs=("latency", "regime", "share", "tenant_sums")):
+    import torch
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant if "tenant_sums" in outputs else None)
+    out = L.attribute(dt, shape, coeffs, n_tenants, outputs)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def check(L, tr, shape, coeffs, n_tenants, name=""):
+    say(f"[parity] {name}: nB={tr.n_batches} N={tr.n_requests} T={n_tenants}")
+    g = run_gpu(L, tr, shape, coeffs, n_tenants)
+    ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shape, coeffs, n_tenants)
+    return parity.compare(ref, tr.offsets, g["latency"], g["regime"], g["share"],
+                          g["tenant_sums"]), g, ref
+
+
+def coeff_vec(d):
+    return np.array(d["prefill_mem"] + d["prefill_comp"] + d["decode_mem"] + d["decode_comp"],
+                    np.float32)
+
+
+# ----------------------------------------------------------- hand examples
+
+
+def test_hand_examples_exact(L):
+    th = coeff_vec(HAND["base_coeffs"])
+    for ex in HAND["unit_shape_examples"]:
+        t = th.copy()
+        if ex["coeff_override"]:
+            t[ex["coeff_override"]["index"]] = ex["coeff_override"]["value"]
+        tr = tracegen.from_batches([(ex["p"], ex["c"])], [[0] * len(ex["p"])], 1)
+        g = run_gpu(L, tr, None, t, 1)
+        say(f"[hand] {ex['name']}")
+        assert g["latency"][0] == ex["T"], ex["name"]
+        assert g["regime"][0] == ex["regime"], ex["name"]
+        assert list(g["share"]) == ex["shares"], ex["name"]
+        assert g["tenant_sums"][0] == sum(ex["shares"]), ex["name"]
+    se = HAND["shaped_examples"]
+    for ex in se["examples"]:
+        tr = tracegen.from_batches([(ex["p"], ex["c"])], [[0] * len(ex["p"])], 1)
+        g = run_gpu(L, tr, se["shape"], coeff_vec(se["coeffs"]), 1)
+        assert g["latency"][0] == ex["T"] and g["regime"][0] == ex["regime"], ex["name"]
+        assert list(g["share"]) == ex["shares"], ex["name"]
+
+
+def test_hand_tenant_trace_exact(L):
+    tt = HAND["tenant_trace"]
+    by = {e["name"]: e for e in HAND["unit_shape_examples"]}
+    tr = tracegen.from_batches([(by[n]["p"], by[n]["c"]) for n in tt["batches"]], tt["tenants"],
+                               tt["n_tenants"])
+    g = run_gpu(L, tr, None, coeff_vec(HAND["base_coeffs"]), tt["n_tenants"])
+    assert list(g["tenant_sums"]) == tt["tenant_sums"]
+    assert list(g["latency"]) == [by[n]["T"] for n in tt["batches"]]
+
+
+# ------------------------------------------------------- workload recipes
+
+
+@pytest.mark.parametrize("name,nb", [("tiny-mixed", None), ("decode-only", 3000),
+                                     ("chunked-prefill", 2000), ("heavy-tailed", 3000),
+                                     ("whatif-sweep", 2000)])
+def test_config_recipes(L, name, nb):
+    tr = tracegen.config_trace(name, nb)
+    st, g, ref = check(L, tr, tr.shape, tracegen.config_coeffs(name), tr.n_tenants, name)
+    say(f"[parity] {name}: {st}")
+    # every regime the recipe produces is exercised
+    assert len(set(g["regime"].tolist())) >= 2
+
+
+def test_all_four_regimes(L):
+    """A trace built to land in every (phase, segment) pair."""
+    rng = np.random.default_rng(7)
+    batches = []
+    for _ in range(50):
+        batches.append(([1] * int(rng.integers(1, 8)), list(rng.integers(1, 100, 1))))
+    batches = [(b[0], [int(rng.integers(1, 50)) for _ in b[0]]) for b in batches]  # decode, small
+    batches += [([1] * 300, [int(x) for x in rng.integers(1, 50, 300)]) for _ in range(20)]
+    batches += [([int(x) for x in rng.integers(2, 6, 3)], [0, 0, 0]) for _ in range(20)]
+    batches += [([int(x) for x in rng.integers(1000, 4000, 3)], [0, 0, 0]) for _ in range(20)]
+    tr = tracegen.from_batches(batches, [[i % 3 for i in range(len(b[0]))] for b in batches], 3)
+    th = coeff_vec(HAND["base_coeffs"])
+    st, g, ref = check(L, tr, None, th, 3, "four regimes")
+    assert set(ref["regime"].tolist()) == {0, 1, 2, 3}
+
+
+# ------------------------------------------------------------- edge cases
+
+
+def random_fill(rng, sizes, n_tenants=5, p_hi=5000, c_hi=200000):
+    off = np.zeros(len(sizes) + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    N = int(off[-1])
+    pre = rng.random(len(sizes)) < 0.3
+    p = np.ones(N, np.int32)
+    c = rng.integers(1, c_hi, N).astype(np.int32)
+    for b in np.nonzero(pre)[0]:
+        p[off[b]:off[b + 1]] = rng.integers(1, p_hi, off[b + 1] - off[b])
+        c[off[b]:off[b + 1]] = 0
+    t = rng.integers(0, n_tenants, N).astype(np.int32)
+    return tracegen.Trace(off, p, c, t, n_tenants, None)
+
+
+SIZE_SETS = {
+    "wave-edges": [1, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513],
+    "tile-edges": [767, 768, 769, 1023, 1024, 1025, 3068, 3069, 3070, 3071, 3072, 3073],
+    "big": [5000, 1, 2, 3, 100000, 7, 3075],
+    "tiny": [1] * 700 + [2] * 300 + [3] * 100,
+    "unaligned": [3, 5, 7, 1, 9, 11, 13, 2, 6, 10] * 50,
+}
+
+
+@pytest.mark.parametrize("key", sorted(SIZE_SETS))
+def test_batch_size_edges(L, key):
+    rng = np.random.default_rng(hash(key) % 1000)
+    tr = random_fill(rng, SIZE_SETS[key])
+    for shape in (None, tracegen.SHAPES["qwen2.5-14b"]):
+        co = tracegen.base_coeffs(31)
+        st, _, _ = check(L, tr, shape, co, tr.n_tenants, key)
+        say(f"[edge] {key}: {st}")
+
+
+@pytest.mark.parametrize("pattern", ["leading", "trailing", "long-run", "all-empty", "no-batches",
+                                     "interleaved"])
+def test_empty_batches(L, pattern):
+    rng = np.random.default_rng(11)
+    if pattern == "leading":
+        sizes = [0] * 5 + list(rng.integers(1, 200, 50))
+    elif pattern == "trailing":
+        sizes = list(rng.integers(1, 200, 50)) + [0] * 7
+    elif pattern == "long-run":
+        sizes = list(rng.integers(1, 200, 20)) + [0] * 700 + list(rng.integers(1, 200, 20)) + \
+            [0] * 300
+    elif pattern == "all-empty":
+        sizes = [0] * 1000
+    elif pattern == "no-batches":
+        sizes = []
+    else:
+        sizes = [int(x) if i % 2 else 0 for i, x in enumerate(rng.integers(1, 50, 600))]
+    tr = random_fill(rng, np.array(sizes, np.int64))
+    check(L, tr, tracegen.SHAPES["llama3.1-8b"], tracegen.base_coeffs(32), tr.n_tenants, pattern)
+
+
+@pytest.mark.parametrize("N", [1, 2, 3, 4, 5, 6, 7, 8, 9, 4097, 4098, 4099])
+def test_request_count_tails(L, N):
+    """N not a multiple of 4: the last 16-byte group runs past the array."""
+    rng = np.random.default_rng(N)
+    sizes = []
+    left = N
+    while left > 0:
+        s = int(min(left, rng.integers(1, 40)))
+        sizes.append(s)
+        left -= s
+    tr = random_fill(rng, sizes)
+    check(L, tr, None, tracegen.base_coeffs(33), tr.n_tenants, f"N={N}")
+
+
+@pytest.mark.parametrize("n_tenants", [1, 2, 4096, 4097, 100000])
+def test_tenant_counts(L, n_tenants):
+    rng = np.random.default_rng(n_tenants)
+    tr = random_fill(rng, rng.integers(1, 300, 400), n_tenants=n_tenants)
+    check(L, tr, tracegen.SHAPES["qwen2.5-32b"], tracegen.base_coeffs(34), n_tenants,
+          f"T={n_tenants}")
+
+
+def test_single_tenant_all_requests(L):
+    """Every request on one tenant: maximal LDS atomic contention."""
+    rng = np.random.default_rng(5)
+    tr = random_fill(rng, rng.integers(1, 1024, 300), n_tenants=64)
+    tr.tenant[:] = 17
+    st, g, ref = check(L, tr, None, tracegen.base_coeffs(35), 64, "one tenant")
+    assert np.count_nonzero(g["tenant_sums"]) == 1
+
+
+def test_extreme_values(L):
+    """Largest p (2^20) over a full tile and c near 2^31: the packed 32-bit
+    prompt sums and 64-bit context sums stay exact."""
+    sizes = [3072, 3069, 1, 5000, 2]
+    off = np.zeros(len(sizes) + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    N = int(off[-1])
+    p = np.full(N, 1 << 20, np.int32)
+    c = np.full(N, (1 << 31) - 1, np.int32)
+    c[off[1]:off[2]] = 0
+    t = (np.arange(N) % 3).astype(np.int32)
+    tr = tracegen.Trace(off, p, c, t, 3, None)
+    th = np.ones(20, np.float32)
+    check(L, tr, None, th, 3, "extreme")
+    check(L, tr, tracegen.SHAPES["70b-like"], tracegen.base_coeffs(36), 3, "extreme shaped")
+
+
+def test_exact_ties_choose_mem(L):
+    """Constructed exact ties (example A with decode-COMP a1 raised to 16)."""
+    ex = [e for e in HAND["unit_shape_examples"] if e["name"] == "A_tie"][0]
+    th = coeff_vec(HAND["base_coeffs"])
+    th[16] = 16
+    tr = tracegen.from_batches([(ex["p"], ex["c"])] * 500, [[0] * 4] * 500, 1)
+    g = run_gpu(L, tr, None, th, 1)
+    assert np.all(g["regime"] == 2)
+    assert np.all(g["latency"] == 352)
+
+
+def test_output_subsets_agree(L):
+    tr = tracegen.config_trace("heavy-tailed", 800)
+    co = tracegen.config_coeffs("heavy-tailed")
+    full = run_gpu(L, tr, tr.shape, co, tr.n_tenants)
+    for outs in (("latency",), ("regime",), ("share",), ("tenant_sums",), ("latency", "share"),
+                 ("regime", "tenant_sums")):
+        part = run_gpu(L, tr, tr.shape, co, tr.n_tenants, outs)
+        for k in outs:
+            if k == "tenant_sums":
+                np.testing.assert_allclose(part[k], full[k], rtol=1e-12)
+            else:
+                assert np.array_equal(part[k], full[k]), (outs, k)
+
+
+def test_deterministic(L):
+    tr = tracegen.config_trace("decode-only", 4000)
+    co = tracegen.config_coeffs("decode-only")
+    a = run_gpu(L, tr, tr.shape, co, tr.n_tenants)
+    b = run_gpu(L, tr, tr.shape, co, tr.n_tenants)
+    for k in ("latency", "regime", "share"):
+        assert np.array_equal(a[k], b[k]), k
+    np.testing.assert_allclose(a["tenant_sums"], b["tenant_sums"], rtol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_traces(L, seed):
+    rng = np.random.default_rng(1000 + seed)
+    kind = seed % 3
+    nb = int(rng.integers(1, 3000))
+    if kind == 0:
+        sizes = rng.integers(0, 50, nb)
+    elif kind == 1:
+        sizes = np.minimum(rng.pareto(1.2, nb) * 30 + 1, 4000).astype(np.int64)
+    else:
+        sizes = rng.choice([0, 1, 2, 255, 256, 1000, 3071, 3072, 3500], nb)
+    tr = random_fill(rng, sizes, n_tenants=int(rng.integers(1, 2000)))
+    sh = tracegen.SHAPES[sorted(tracegen.SHAPES)[seed % 4]]
+    check(L, tr, sh, tracegen.base_coeffs(40 + seed), tr.n_tenants, f"random {seed}")
+
+
+# ---------------------------------------------------------------- features
+
+
+@pytest.mark.parametrize("name,nb", [("tiny-mixed", None), ("heavy-tailed", 1500)])
+def test_features(L, name, nb):
+    import torch
+    tr = tracegen.config_trace(name, nb)
+    rng = np.random.default_rng(3)
+    sizes = tr.sizes().copy()
+    sizes[rng.integers(0, len(sizes), 20)] = 0  # some empty batches
+    off = np.zeros(len(sizes) + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    N = int(off[-1])
+    p, c = tr.p[:N], tr.c[:N]
+    for shape in (None, tr.shape):
+        dt = L.DeviceTrace.from_host(off, p, c)
+        xr, xb = L.features(dt, shape)
+        torch.cuda.synchronize()
+        rr, rb = oracle.features(off, p, c, shape)
+        e_r = parity.rel_err(xr.cpu().numpy(), rr)
+        e_b = parity.rel_err(xb.cpu().numpy(), rb)
+        say(f"[features] {name} shape={shape is not None}: req {e_r.max():.2e} batch {e_b.max():.2e}")
+        assert e_r.max() <= parity.RTOL
+        assert e_b.max() <= 1e-12
+
+
+# --------------------------------------------------------- tenant sums API
+
+
+@pytest.mark.parametrize("n,T", [(0, 3), (1, 1), (12345, 16), (1_000_003, 1024), (200_000, 5000)])
+def test_tenant_sums_standalone(L, n, T):
+    import torch
+    rng = np.random.default_rng(n + T)
+    t = rng.integers(0, T, n).astype(np.int32)
+    s = (rng.random(n) * 100).astype(np.float32)
+    out = L.tenant_sums(torch.from_numpy(t).cuda(), torch.from_numpy(s).cuda(), T)
+    torch.cuda.synchronize()
+    want = oracle.tenant_sums(t, s.astype(np.float64), T)
+    e = parity.rel_err(out.cpu().numpy(), want)
+    assert e.max() <= 1e-12 if e.size else True
+
+
+# ---------------------------------------------------------------- validate
+
+
+def test_validate(L):
+    tr = tracegen.config_trace("tiny-mixed")
+    ws = L.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+
+    def v(off, p, c, t, T=tr.n_tenants):
+        return L.llmv_validate(L.DeviceTrace.from_host(off, p, c, t), T, ws)
+
+    assert v(tr.offsets, tr.p, tr.c, tr.tenant) == L.LLMV_OK
+    bad = [
+        (np.concatenate([[1], tr.offsets[1:]]), tr.p, tr.c, tr.tenant),
+        (tr.offsets, np.where(np.arange(len(tr.p)) == 7, 0, tr.p), tr.c, tr.tenant),
+        (tr.offsets, np.where(np.arange(len(tr.p)) == 9, L.LLMV_P_MAX + 1, tr.p), tr.c, tr.tenant),
+        (tr.offsets, tr.p, np.where(np.arange(len(tr.c)) == 3, -1, tr.c), tr.tenant),
+        (tr.offsets, tr.p, tr.c, np.where(np.arange(len(tr.c)) == 5, tr.n_tenants, tr.tenant)),
+    ]
+    off2 = tr.offsets.copy()
+    off2[10], off2[11] = off2[11], off2[10]  # decreasing
+    bad.append((off2, tr.p, tr.c, tr.tenant))
+    for i, args in enumerate(bad):
+        assert v(*args) == L.LLMV_ERANGE, i
+    # n_requests disagreeing with offsets[nB]
+    assert v(tr.offsets[:-1], tr.p, tr.c, tr.tenant) == L.LLMV_ERANGE
+
+
+# ----------------------------------------- full-size workloads, sampled
+
+
+def full_size_sampled(L, name, n_sample=1500):
+    import torch
+    tr = tracegen.config_trace(name)
+    co = tracegen.config_coeffs(name)
+    say(f"[full] {name}: nB={tr.n_batches} N={tr.n_requests}")
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    out = L.attribute(dt, tr.shape, co, tr.n_tenants)
+    torch.cuda.synchronize()
+    lat = out["latency"].cpu().numpy()
+    reg = out["regime"].cpu().numpy()
+    ts = out["tenant_sums"].cpu().numpy()
+    rng = np.random.default_rng(99)
+    sizes = tr.sizes()
+    bids = np.unique(np.concatenate([
+        rng.integers(0, tr.n_batches, n_sample), np.arange(5), tr.n_batches - 1 - np.arange(5),
+        np.argsort(sizes)[-20:]]))
+    # shares of the sampled batches only
+    share = out["share"]
+    idx = np.concatenate([np.arange(tr.offsets[b], tr.offsets[b + 1]) for b in bids])
+    g_share = np.zeros(tr.n_requests, np.float32)
+    g_share[idx] = share[torch.from_numpy(idx).cuda()].cpu().numpy()
+    del out, share, dt
+    torch.cuda.empty_cache()
+    off, p, c, t = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
+    ref = oracle.attribute(off, p, c, t, tr.shape, co, tr.n_tenants,
+                           ("T", "TM", "TC", "phase", "regime", "share", "share_alt"))
+    st = parity.compare(ref, tr.offsets, lat, reg, g_share, None, batch_ids=bids)
+    # tenant sums over the whole trace
+    ref_ts = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co, tr.n_tenants,
+                              ("tenant_sums",))["tenant_sums"]
+    e = parity.rel_err(ts, ref_ts)
+    st["tenant"] = float(e.max())
+    assert st["tenant"] <= parity.RTOL
+    # properties at full size: tenant sums add up to the total latency
+    tot = lat.astype(np.float64).sum()
+    assert abs(ts.sum() - tot) / tot <= parity.RTOL
+    say(f"[full] {name}: {st}")
+
+
+@pytest.mark.parametrize("name", ["decode-only", "chunked-prefill", "heavy-tailed"])
+def test_full_size_sampled(L, name):
+    full_size_sampled(L, name)

@@ -1,0 +1,136 @@
+"""The C-ABI library on the CPU host (no GPU): it loads, exports every
+function include/llmv.h declares, computes the same shape constants as the
+oracle, and rejects bad host arguments before touching the device."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle
+import tracegen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "llmv.h")
+
+
+@pytest.fixture(scope="module")
+def llmv():
+    from paper_2608_08382_amd import build, llmv as mod
+    if build.is_stale():
+        build.build()
+    mod.load()
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(llmv_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function(llmv):
+    names = declared_functions()
+    assert set(names) == set(llmv.EXPORTS)
+    lib = llmv.load()
+    for n in names:
+        assert hasattr(lib, n)
+    out = subprocess.run(["nm", "-D", "--defined-only", llmv.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (llmv_\w+)", out))
+    assert set(names) <= exported
+    # nothing else with the llmv_ prefix leaks out
+    assert exported == set(names)
+
+
+def test_library_is_gfx950_code_object(llmv):
+    # the offload bundle inside the library names its target
+    data = open(llmv.LIB_PATH, "rb").read()
+    assert b"amdgcn-amd-amdhsa--gfx950" in data
+
+
+@pytest.mark.parametrize("name", sorted(tracegen.SHAPES))
+def test_shape_constants_match_oracle(llmv, name):
+    sh = tracegen.SHAPES[name]
+    assert llmv.llmv_shape_constants(sh) == list(oracle.shape_constants(sh))
+
+
+@settings(max_examples=50, deadline=None)
+@given(st.lists(st.integers(1, 1 << 12), min_size=9, max_size=9))
+def test_shape_constants_random(llmv, v):
+    sh = dict(zip(tracegen.SHAPE_FIELDS, v))
+    try:
+        want = list(oracle.shape_constants(sh))
+    except oracle.OracleError:
+        with pytest.raises(llmv.LlmvError):
+            llmv.llmv_shape_constants(sh)
+        return
+    assert llmv.llmv_shape_constants(sh) == want
+
+
+def test_shape_constants_unit_and_errors(llmv):
+    assert llmv.llmv_shape_constants(None) == [1.0, 1.0, 1.0, 1.0]
+    bad = dict(tracegen.SHAPES["llama3.1-8b"], head_dim=0)
+    with pytest.raises(llmv.LlmvError) as ei:
+        llmv.llmv_shape_constants(bad)
+    assert ei.value.code == llmv.LLMV_EINVAL
+    assert "field" in llmv.llmv_last_error()
+    huge = dict(tracegen.SHAPES["llama3.1-8b"], n_layers=1 << 30, hidden=1 << 30)
+    with pytest.raises(llmv.LlmvError):
+        llmv.llmv_shape_constants(huge)
+
+
+FAKE = 0x100000  # never dereferenced: every call below fails its host checks first
+
+
+def _trace(llmv, nB=4, N=8, off=FAKE, p=FAKE, c=FAKE, t=FAKE):
+    return llmv.llmv_trace(nB, N, off, p, c, t)
+
+
+def _attr(llmv, tr, coeffs=None, share=None, T=1, tsum=None, ws=None, wsb=0):
+    lib = llmv.load()
+    co = (ctypes.c_float * 20)(*(coeffs if coeffs is not None else [1.0] * 20))
+    return lib.llmv_attribute(None if tr is None else ctypes.byref(tr), None, co, None, None,
+                              share, T, tsum, ws, wsb, None)
+
+
+def test_host_argument_errors(llmv):
+    lib = llmv.load()
+    E = llmv.LLMV_EINVAL
+    assert _attr(llmv, None) == E
+    assert _attr(llmv, _trace(llmv, nB=-1)) == E
+    assert _attr(llmv, _trace(llmv, N=-5)) == E
+    assert _attr(llmv, _trace(llmv, off=0)) == E
+    assert _attr(llmv, _trace(llmv, p=0)) == E
+    assert _attr(llmv, _trace(llmv, p=FAKE + 4)) == E  # misaligned
+    assert _attr(llmv, _trace(llmv), coeffs=[float("nan")] + [1.0] * 19) == E
+    assert _attr(llmv, _trace(llmv), coeffs=[1.0] * 19 + [float("inf")]) == E
+    assert _attr(llmv, _trace(llmv), share=FAKE + 8) == E
+    # tenant sums need tenant ids and a tenant count
+    assert _attr(llmv, _trace(llmv, t=0), tsum=FAKE) == E
+    assert _attr(llmv, _trace(llmv), T=0, tsum=FAKE) == E
+    assert _attr(llmv, _trace(llmv), T=(1 << 24) + 1, tsum=FAKE) == E
+    assert "n_tenants" in llmv.llmv_last_error()
+    # features / tenant sums / validate
+    assert lib.llmv_features(None, None, None, None, None, 0, None) == E
+    assert lib.llmv_tenant_sums(FAKE, FAKE, -1, 4, FAKE, None, 0, None) == E
+    assert lib.llmv_tenant_sums(FAKE, FAKE, 10, 0, FAKE, None, 0, None) == E
+    assert lib.llmv_tenant_sums(FAKE, FAKE, 10, 4, None, None, 0, None) == E
+    assert lib.llmv_tenant_sums(None, FAKE, 10, 4, FAKE, None, 0, None) == E
+    assert lib.llmv_validate(None, 0, None, 0, None) == E
+    tr = _trace(llmv)
+    assert lib.llmv_validate(ctypes.byref(tr), 0, None, 0, None) == E  # tenant without count
+
+
+def test_python_binding_refuses_without_library(tmp_path):
+    from paper_2608_08382_amd import llmv as mod
+    saved = mod._lib
+    try:
+        mod._lib = None
+        with pytest.raises(RuntimeError, match="build the HIP library"):
+            mod.load(str(tmp_path / "missing.so"))
+    finally:
+        mod._lib = saved
