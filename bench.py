@@ -106,6 +106,10 @@ def main():
     ap.add_argument("--workload", default="heavy-tailed")
     ap.add_argument("--n-batches", type=int, default=None, help="override the batch count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true",
+                    help="also time the step with subsets of the outputs (stderr)")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="also run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -166,6 +170,33 @@ def main():
     achieved = nbytes / (k_avg_ms / 1e3) / 1e9
     log(f"[bench] {ms_per_step:.4f} ms/step, tile kernel {k_avg_ms:.4f} ms "
         f"(min {min(kern_ms):.4f}), {achieved:.0f} GB/s algorithmic")
+
+    if args.breakdown:
+        variants = {"latency+regime": (lat, reg, None, None), "share": (None, None, share, None),
+                    "tenant_sums": (None, None, None, tsum),
+                    "latency+regime+share": (lat, reg, share, None)}
+        for name, (a, b, c, d) in variants.items():
+            ev = [(hip.create(), hip.create()) for _ in range(5)]
+            for i in range(5):
+                llmv.llmv_set_kernel_events(*ev[i])
+                llmv.llmv_attribute(dt, tr.shape, coeffs, a, b, c, tr.n_tenants, d, ws)
+            llmv.llmv_set_kernel_events(None, None)
+            torch.cuda.synchronize()
+            ms = min(hip.elapsed_ms(x, y) for x, y in ev)
+            log(f"[bench] breakdown {name}: tile kernel {ms:.4f} ms")
+    if args.copy_bytes:
+        src = torch.empty(args.copy_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        ev = [(hip.create(), hip.create()) for _ in range(3)]
+        for x, y in ev:
+            hip.record(x, stream)
+            dst.copy_(src)
+            hip.record(y, stream)
+        torch.cuda.synchronize()
+        ms = min(hip.elapsed_ms(x, y) for x, y in ev)
+        log(f"[bench] copy of {args.copy_bytes} bytes: {ms:.4f} ms, "
+            f"{2 * args.copy_bytes / ms / 1e6:.0f} GB/s read+write")
+        del src, dst
 
     reg_host = reg.cpu().numpy()
     regimes = np.bincount(reg_host[reg_host != 255], minlength=4)[:4]

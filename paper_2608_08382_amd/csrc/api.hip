@@ -37,7 +37,6 @@ int hip_fail(hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail(e_, what); \
   } while (0)
 
-constexpr int kBlocksPerCu = 4;   // persistent workgroups per compute unit
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -61,14 +60,28 @@ int device_cus(int* out) {
   return LLMV_OK;
 }
 
-// Persistent grid for n requests: enough workgroups to fill the device, but
-// no more than one per kCap requests.
-int64_t grid_for(int64_t n, int cus) {
-  int64_t g = (int64_t)cus * kBlocksPerCu;
-  if (g > kMaxGrid) g = kMaxGrid;
+// Upper bound of the persistent grid for n requests (sizes the workspace):
+// no more than one workgroup per kCap requests, at most kMaxGrid.
+int64_t grid_max_for(int64_t n) {
   const int64_t by_work = (n + kCap - 1) / kCap;
-  if (by_work < g) g = by_work;
-  return g < 1 ? 1 : g;
+  return by_work < 1 ? 1 : (by_work > kMaxGrid ? kMaxGrid : by_work);
+}
+
+// Resident workgroups per compute unit for a kernel and its dynamic LDS.
+template <typename K>
+int blocks_per_cu(K kernel, size_t dyn) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, kWG, dyn) != hipSuccess || nb < 1)
+    nb = 1;
+  return nb;
+}
+
+// Persistent grid: exactly the workgroups that are resident at once (one
+// wave of workgroups, no tail), capped by grid_max_for.
+int64_t grid_for(int64_t n, int cus, int per_cu) {
+  const int64_t g = (int64_t)cus * per_cu;
+  const int64_t m = grid_max_for(n);
+  return g < m ? g : m;
 }
 
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
@@ -150,10 +163,15 @@ int check_ws(void* ws, size_t ws_bytes, size_t need) {
   return LLMV_OK;
 }
 
-template <int MODE, int HIST, bool SHARE>
-hipError_t launch_tiles(const Params& P, int64_t grid, size_t dyn, hipStream_t s) {
-  hipLaunchKernelGGL((k_tiles<MODE, HIST, SHARE>), dim3((unsigned)grid), dim3(kWG), dyn, s, P);
-  return hipGetLastError();
+typedef void (*TileKernel)(const Params);
+
+TileKernel pick_tiles(int mode, int hist, bool share) {
+  if (mode == MODE_FEAT) return k_tiles<MODE_FEAT, HIST_NONE, false>;
+  if (hist == HIST_NONE)
+    return share ? k_tiles<MODE_ATTR, HIST_NONE, true> : k_tiles<MODE_ATTR, HIST_NONE, false>;
+  if (hist == HIST_LDS)
+    return share ? k_tiles<MODE_ATTR, HIST_LDS, true> : k_tiles<MODE_ATTR, HIST_LDS, false>;
+  return share ? k_tiles<MODE_ATTR, HIST_GLOBAL, true> : k_tiles<MODE_ATTR, HIST_GLOBAL, false>;
 }
 
 // Partition + tiles (+ tenant reduction) shared by attribute and features.
@@ -162,15 +180,17 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   int cus = 0;
   int rc = device_cus(&cus);
   if (rc) return rc;
-  const int64_t grid = grid_for(tr->n_requests, cus);
   const int32_t Tl = want_tenant ? T : 0;
-  const Layout L = layout(grid, Tl);
+  const Layout L = layout(grid_max_for(tr->n_requests), Tl);
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
+  const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
+  const size_t dyn = hist == HIST_LDS ? (size_t)T * sizeof(double) : 0;
+  const TileKernel kern = pick_tiles(mode, hist, want_share);
+  const int64_t grid = grid_for(tr->n_requests, cus, blocks_per_cu(kern, dyn));
   char* base = (char*)ws;
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   uint32_t* cnt = (uint32_t*)(base + L.cnt);
-  const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
   const int n_cnt = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
   P.wg_first = wg_first;
@@ -188,22 +208,9 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
     HIP_TRY(hipGetLastError(), "k_partition launch");
   }
 
-  const size_t dyn = hist == HIST_LDS ? (size_t)T * sizeof(double) : 0;
   if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
-  hipError_t e = hipSuccess;
-  if (mode == MODE_FEAT) {
-    e = launch_tiles<MODE_FEAT, HIST_NONE, false>(P, grid, 0, stream);
-  } else if (hist == HIST_NONE) {
-    e = want_share ? launch_tiles<MODE_ATTR, HIST_NONE, true>(P, grid, dyn, stream)
-                   : launch_tiles<MODE_ATTR, HIST_NONE, false>(P, grid, dyn, stream);
-  } else if (hist == HIST_LDS) {
-    e = want_share ? launch_tiles<MODE_ATTR, HIST_LDS, true>(P, grid, dyn, stream)
-                   : launch_tiles<MODE_ATTR, HIST_LDS, false>(P, grid, dyn, stream);
-  } else {
-    e = want_share ? launch_tiles<MODE_ATTR, HIST_GLOBAL, true>(P, grid, dyn, stream)
-                   : launch_tiles<MODE_ATTR, HIST_GLOBAL, false>(P, grid, dyn, stream);
-  }
-  if (e != hipSuccess) return hip_fail(e, "k_tiles launch");
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, stream, P);
+  HIP_TRY(hipGetLastError(), "k_tiles launch");
   if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
 
   if (hist == HIST_LDS) {
@@ -236,10 +243,8 @@ int llmv_shape_constants(const llmv_shape* shape, double S[4]) {
 
 size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
   (void)n_batches;
-  int cus = 0;
-  if (device_cus(&cus)) return 0;
   const int64_t n = n_requests > 0 ? n_requests : 0;
-  return layout(grid_for(n, cus), n_tenants > 0 ? n_tenants : 0).total;
+  return layout(grid_max_for(n), n_tenants > 0 ? n_tenants : 0).total;
 }
 
 int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[20],
@@ -303,14 +308,16 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
   int cus = 0;
   int rc = device_cus(&cus);
   if (rc) return rc;
-  const int64_t grid = grid_for(n, cus);
-  const Layout L = layout(grid, n_tenants);
+  const Layout L = layout(grid_max_for(n), n_tenants);
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
   char* base = (char*)ws;
   uint32_t* cnt = (uint32_t*)(base + L.cnt);
   const int n_cnt = (n_tenants + kTenantChunk - 1) / kTenantChunk;
   const bool lds = lds_hist(n_tenants);
+  const int64_t grid =
+      lds ? grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_LDS>, (size_t)n_tenants * sizeof(double)))
+          : grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_GLOBAL>, 0));
   // Clear the counters (and the output for the atomics path) with the
   // partition kernel on an empty batch list.
   hipLaunchKernelGGL(k_partition, dim3(16), dim3(kWG), 0, s, (const int64_t*)nullptr, (int64_t)-1,
@@ -342,10 +349,7 @@ int llmv_validate(const llmv_trace* trace, int32_t n_tenants, void* ws, size_t w
   if (trace->tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
     return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
   hipStream_t s = (hipStream_t)stream;
-  int cus = 0;
-  rc = device_cus(&cus);
-  if (rc) return rc;
-  const Layout L = layout(grid_for(trace->n_requests, cus), 0);
+  const Layout L = layout(grid_max_for(trace->n_requests), 0);
   rc = check_ws(ws, ws_bytes, L.flag + sizeof(int));
   if (rc) return rc;
   int* flag = (int*)((char*)ws + L.flag);

@@ -27,15 +27,14 @@
 
 namespace llmv {
 
-constexpr int kWG = 256;                         // threads per workgroup
-constexpr int kWaves = kWG / 64;                 // wave64
-constexpr int kVec = 4;                          // consecutive requests per lane per round
-constexpr int kRounds = 3;                       // rounds held in registers per wave
-constexpr int kRoundSpan = 64 * kVec;            // 256 requests per wave-round
-constexpr int kWaveSpan = kRoundSpan * kRounds;  // 768
-constexpr int kCap = kWaveSpan * kWaves;         // 3072 request slots per tile
-constexpr int kWindow = 256;                     // offsets examined per tile
-constexpr int kMaxTileBatches = kWindow - 1;     // 255 batches per tile
+constexpr int kWG = 256;                     // threads per workgroup
+constexpr int kWaves = kWG / 64;             // wave64
+constexpr int kVec = 16;                     // consecutive requests held per lane
+constexpr int kWaveSpan = 64 * kVec;         // 1024 requests per wave
+constexpr int kCap = kWaveSpan * kWaves;     // 4096 request slots per tile
+constexpr int kMaskWords = kCap / 32;        // batch-start bitmask of a tile
+constexpr int kWindow = 256;                 // offsets examined per tile
+constexpr int kMaxTileBatches = kWindow - 1; // 255 batches per tile
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 2048;                   // persistent workgroups, upper bound
 constexpr int kReduceSplit = 16;                 // row blocks in k_tenant_reduce
@@ -183,7 +182,7 @@ __device__ __forceinline__ double request_out(const Params& P, const double* k, 
     return 0.0;
   }
   const double s = k[0] + k[1] * pd + k[2] * (double)c + k[3] * (pd * pd);
-  if (SHARE && store_scalar) __builtin_nontemporal_store((float)s, P.share + i);
+  if (SHARE && store_scalar) P.share[i] = (float)s;
   if (HIST == HIST_LDS) atomicAdd(s_hist + t, s);
   if (HIST == HIST_GLOBAL) unsafeAtomicAdd(P.tenant_sums + t, s);
   return s;
@@ -258,28 +257,45 @@ __device__ void big_batch(const Params& P, int64_t bg, int64_t rs, int64_t re,
 
 // ----------------------------------------------------------------- tiles
 
-struct Pref {
-  uint64_t pc;  // sum p (low 32 bits) | count of prefill-like requests (high)
-  uint64_t c;
-  uint64_t q;
-  uint32_t w;   // wave whose running prefix this is relative to
-  uint32_t pad;
+// Running prefix of one request position, relative to the start of its
+// lane's run of kVec requests.  id = lane + 64*wave locates the lane base.
+struct LanePref {
+  uint32_t p;   // sum p
+  uint32_t id;
+  uint64_t cz;  // sum c (bits 0..47) | count of c == 0 (bits 48..63)
+  uint64_t q;   // sum p^2
 };
+
+struct Sums {
+  uint64_t p, cz, q;
+};
+
+constexpr uint64_t kZeroUnit = 1ull << 48;
+constexpr uint64_t kCMask = kZeroUnit - 1;
+
+__device__ __forceinline__ uint32_t lds_popc_below(const uint32_t* mask, int pos) {
+  // set bits of the tile bitmask at positions < pos, pos < 32 of its word
+  return __builtin_popcount(mask[pos >> 5] & ((1u << (pos & 31)) - 1u));
+}
 
 template <int MODE, int HIST, bool SHARE>
 __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
-  extern __shared__ double s_hist[];  // [n_tenants] when HIST_LDS
-  __shared__ int32_t s_lo[kWindow];   // batch starts relative to the tile base
-  __shared__ Pref s_xs[kWindow];      // prefix before each batch's first request
-  __shared__ Pref s_xe[kWindow];      // prefix through each batch's last request
-  __shared__ double s_k[kWindow][4];  // per-batch share / feature constants
-  __shared__ uint64_t s_wt[kWaves][3];
+  extern __shared__ double s_hist[];       // [n_tenants] when HIST_LDS
+  __shared__ int32_t s_lo[kWindow];        // batch starts relative to the tile base
+  __shared__ uint32_t s_mask[kMaskWords + 1];  // bit x: a nonempty batch starts at x
+  __shared__ uint64_t s_ball[kWaves];      // nonempty flags of the window's batches
+  __shared__ LanePref s_xs[kWindow];       // prefix before each batch's first request
+  __shared__ LanePref s_xe[kWindow];       // prefix through each batch's last request
+  __shared__ Sums s_lb[kWG];               // exclusive prefix of each lane within its wave
+  __shared__ Sums s_wt[kWaves];            // wave totals
+  __shared__ double s_k[kWindow][4];       // per nonempty batch: share / feature constants
   __shared__ BigRed s_red[kWaves];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t N = P.N;
+  const int32_t x0 = wave * kWaveSpan + lane * kVec;  // first slot of this lane
 
   if (HIST == HIST_LDS)
     for (int u = tid; u < P.n_tenants; u += kWG) s_hist[u] = 0.0;
@@ -296,15 +312,16 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
   __syncthreads();
 
   while (b < bw1) {
+    // ---- A: window -> s_lo; batches b .. b+count-1 end within kCap slots
     const int64_t lim = min((int64_t)kMaxTileBatches, bw1 - b);
-    const int64_t ra = r0 & ~(int64_t)(kVec - 1);  // 16-byte aligned tile base
+    const int64_t ra = r0 & ~(int64_t)3;  // 16-byte aligned tile base
     int pred = 0;
     if (tid <= lim) {
       const int64_t rel = wv - ra;
       s_lo[tid] = (int32_t)min(rel, (int64_t)kCap + 1);
       pred = (tid >= 1 && rel <= kCap) ? 1 : 0;
     }
-    // Batches b .. b+count-1 end within kCap slots of the tile base.
+    if (tid <= kMaskWords) s_mask[tid] = 0u;
     const int count = __syncthreads_count(pred);
 
     if (count == 0) {
@@ -321,172 +338,169 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
     const int32_t xf = s_lo[0];     // first tile request relative to ra (0..3)
     const int64_t r1 = ra + L;
 
-    // Window of the next tile, in flight while this one is processed.
-    int64_t nwv = 0;
+    // ---- B: batch-start bits, nonempty ballots; loads of this lane's slots
+    bool ne = false;
+    if (tid < count) {
+      const int32_t lo = s_lo[tid];
+      ne = s_lo[tid + 1] > lo;
+      if (ne) atomicOr(&s_mask[lo >> 5], 1u << (lo & 31));
+    }
+    const uint64_t ball = __ballot(ne);
+    if (lane == 0) s_ball[wave] = ball;
+
+    int64_t nwv = 0;  // window of the next tile, in flight meanwhile
     if (e < bw1 && tid <= min((int64_t)kMaxTileBatches, bw1 - e)) nwv = P.off[e + tid];
 
-    // ---- load: lane holds positions x0..x0+3 of each round (x rel. to ra)
-    int32_t pv[kRounds][kVec], cv[kRounds][kVec], tv[kRounds][kVec];
+    int32_t pv[kVec], cv[kVec], tv[kVec];
 #pragma unroll
-    for (int k = 0; k < kRounds; ++k) {
-      const int32_t x0 = wave * kWaveSpan + k * kRoundSpan + lane * kVec;
-      const int64_t pos = ra + x0;
+    for (int q = 0; q < kVec; ++q) pv[q] = cv[q] = tv[q] = 0;
+    if (x0 < L) {
+      const int32_t* pb = P.p + ra;
+      const int32_t* cb = P.c + ra;
+      const int32_t* tb = P.tenant + ra;
+      if (ra + x0 + kVec <= N) {
 #pragma unroll
-      for (int q = 0; q < kVec; ++q) pv[k][q] = cv[k][q] = tv[k][q] = 0;
-      if (x0 < L) {
-        if (pos + kVec <= N) {
-          const v4i a = __builtin_nontemporal_load((const v4i*)(P.p + pos));
-          const v4i d = __builtin_nontemporal_load((const v4i*)(P.c + pos));
-          pv[k][0] = a.x; pv[k][1] = a.y; pv[k][2] = a.z; pv[k][3] = a.w;
-          cv[k][0] = d.x; cv[k][1] = d.y; cv[k][2] = d.z; cv[k][3] = d.w;
+        for (int g = 0; g < kVec / 4; ++g) {
+          const v4i a = *(const v4i*)(pb + x0 + 4 * g);
+          const v4i d = *(const v4i*)(cb + x0 + 4 * g);
+          pv[4 * g] = a.x; pv[4 * g + 1] = a.y; pv[4 * g + 2] = a.z; pv[4 * g + 3] = a.w;
+          cv[4 * g] = d.x; cv[4 * g + 1] = d.y; cv[4 * g + 2] = d.z; cv[4 * g + 3] = d.w;
           if (HIST != HIST_NONE) {
-            const v4i t = __builtin_nontemporal_load((const v4i*)(P.tenant + pos));
-            tv[k][0] = t.x; tv[k][1] = t.y; tv[k][2] = t.z; tv[k][3] = t.w;
+            const v4i t = *(const v4i*)(tb + x0 + 4 * g);
+            tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
           }
-        } else {
+        }
+      } else {
 #pragma unroll
-          for (int q = 0; q < kVec; ++q) {
-            if (pos + q < N) {
-              pv[k][q] = P.p[pos + q];
-              cv[k][q] = P.c[pos + q];
-              if (HIST != HIST_NONE) tv[k][q] = P.tenant[pos + q];
-            }
+        for (int q = 0; q < kVec; ++q) {
+          if (ra + x0 + q < N) {
+            pv[q] = pb[x0 + q];
+            cv[q] = cb[x0 + q];
+            if (HIST != HIST_NONE) tv[q] = tb[x0 + q];
           }
         }
       }
     }
+    __syncthreads();
 
-    // ---- batch id of each held request (binary search in s_lo), while the
-    // loads are in flight.  bits: valid 0-3, first-of-batch 4-7, last 8-11.
-    uint32_t bids[kRounds], flags[kRounds];
-#pragma unroll
-    for (int k = 0; k < kRounds; ++k) {
-      const int32_t x0 = wave * kWaveSpan + k * kRoundSpan + lane * kVec;
-      const int32_t xs = max(x0, xf);
-      int lo_i = 0, hi_i = count;
-      while (hi_i - lo_i > 1) {
-        const int mid = (lo_i + hi_i) >> 1;
-        if (s_lo[mid] <= xs) lo_i = mid;
-        else hi_i = mid;
-      }
-      int j = lo_i;
-      int32_t cur = s_lo[j], nxt = s_lo[j + 1];
-      uint32_t bp = 0, fl = 0;
+    // ---- C: ordinal of each held request's batch among the tile's
+    // nonempty batches, from the batch-start bitmask
+    const uint32_t w0 = s_mask[x0 >> 5];
+    const uint32_t bits = (w0 >> (x0 & 16)) & 0xffffu;  // starts at x0 .. x0+15
+    const uint32_t next_bit = (s_mask[(x0 + kVec) >> 5] >> ((x0 + kVec) & 31)) & 1u;
+    uint32_t wave_base = 0;  // starts in the slots of earlier waves
+    if (wave > 0) {
+      uint32_t cnt = 0;
+      if (lane < 32 * wave) cnt += __builtin_popcount(s_mask[lane]);
+      if (lane + 64 < 32 * wave) cnt += __builtin_popcount(s_mask[lane + 64]);
+      for (int m = 32; m >= 1; m >>= 1) cnt += __shfl_xor(cnt, m, 64);
+      wave_base = cnt;
+    }
+    const uint32_t h = __builtin_popcount(bits);
+    uint32_t hs = h;  // inclusive wave scan of the lanes' start counts
+    hs += dpp_u32<0x111, 0xf>(hs);
+    hs += dpp_u32<0x112, 0xf>(hs);
+    hs += dpp_u32<0x114, 0xf>(hs);
+    hs += dpp_u32<0x118, 0xf>(hs);
+    hs += dpp_u32<0x142, 0xa>(hs);
+    hs += dpp_u32<0x143, 0xc>(hs);
+    const uint32_t ord0 = wave_base + hs - h;  // starts before x0
+
+    // ---- D: one pass over the lane's requests: lane-relative prefixes at
+    // batch starts and ends, lane totals
+    uint32_t ords[kVec / 4];  // 8-bit ordinal per held request
+    uint32_t valid = 0;
+    uint32_t ap = 0;
+    uint64_t acz = 0, aq = 0;
+    {
+      uint32_t ord = ord0;
 #pragma unroll
       for (int q = 0; q < kVec; ++q) {
         const int32_t x = x0 + q;
-        const bool valid = (x >= xf) && (x < L);
-        if (valid) {
-          while (nxt <= x) {
-            ++j;
-            cur = nxt;
-            nxt = s_lo[j + 1];
-          }
-          fl |= 1u << q;
-          if (x == cur) fl |= 1u << (4 + q);
-          if (x + 1 == nxt) fl |= 1u << (8 + q);
+        const bool v = (x >= xf) && (x < L);
+        const uint32_t st = (bits >> q) & 1u;
+        const uint32_t en = ((q + 1 < kVec ? (bits >> (q + 1)) : next_bit) & 1u) | (x + 1 == L);
+        ord += st;
+        const uint32_t k = ord - 1u;
+        if (q % 4 == 0) ords[q / 4] = 0;
+        ords[q / 4] |= (k & 0xffu) << (8 * (q % 4));
+        if (v) {
+          valid |= 1u << q;
+          const uint32_t p = (uint32_t)pv[q];
+          const uint32_t c = (uint32_t)cv[q];
+          if (st) s_xs[k] = LanePref{ap, (uint32_t)tid, acz, aq};
+          ap += p;
+          acz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
+          aq += (uint64_t)p * p;
+          if (en) s_xe[k] = LanePref{ap, (uint32_t)tid, acz, aq};
         }
-        bp |= (uint32_t)j << (8 * q);
       }
-      bids[k] = bp;
-      flags[k] = fl;
     }
-
-    // ---- prefix sums: in-lane, wave (DPP), carried across rounds
-    uint64_t carry_pc = 0, carry_c = 0, carry_q = 0;
-#pragma unroll
-    for (int k = 0; k < kRounds; ++k) {
-      uint64_t ipc[kVec], ic[kVec], iq[kVec];
-      uint64_t apc = 0, ac = 0, aq = 0;
-#pragma unroll
-      for (int q = 0; q < kVec; ++q) {
-        const bool valid = (flags[k] >> q) & 1u;
-        const int32_t p = pv[k][q], c = cv[k][q];
-        const uint64_t xpc = valid ? ((uint64_t)(uint32_t)p |
-                                      ((uint64_t)((p > 1 || c == 0) ? 1 : 0) << 32))
-                                   : 0;
-        const uint64_t xc = valid ? (uint64_t)(uint32_t)c : 0;
-        const uint64_t xq = valid ? (uint64_t)((int64_t)p * p) : 0;
-        apc += xpc;
-        ac += xc;
-        aq += xq;
-        ipc[q] = apc;
-        ic[q] = ac;
-        iq[q] = aq;
-      }
-      const uint64_t spc = wave_incl_scan(apc);
-      const uint64_t sc = wave_incl_scan(ac);
+    {
+      const uint64_t sp = wave_incl_scan((uint64_t)ap);
+      const uint64_t scz = wave_incl_scan(acz);
       const uint64_t sq = wave_incl_scan(aq);
-      const uint64_t bpc = carry_pc + spc - apc;  // prefix before this lane
-      const uint64_t bc = carry_c + sc - ac;
-      const uint64_t bq = carry_q + sq - aq;
-      if (flags[k] & 0xff0u) {
-#pragma unroll
-        for (int q = 0; q < kVec; ++q) {
-          const uint32_t j = (bids[k] >> (8 * q)) & 0xffu;
-          const uint64_t prev_pc = q ? ipc[q - 1] : 0, prev_c = q ? ic[q - 1] : 0,
-                         prev_q = q ? iq[q - 1] : 0;
-          if ((flags[k] >> (4 + q)) & 1u)
-            s_xs[j] = Pref{bpc + prev_pc, bc + prev_c, bq + prev_q, (uint32_t)wave, 0};
-          if ((flags[k] >> (8 + q)) & 1u)
-            s_xe[j] = Pref{bpc + ipc[q], bc + ic[q], bq + iq[q], (uint32_t)wave, 0};
-        }
-      }
-      carry_pc += readlane_u64(spc, 63);
-      carry_c += readlane_u64(sc, 63);
-      carry_q += readlane_u64(sq, 63);
-    }
-    if (lane == 0) {
-      s_wt[wave][0] = carry_pc;
-      s_wt[wave][1] = carry_c;
-      s_wt[wave][2] = carry_q;
+      s_lb[tid] = Sums{sp - ap, scz - acz, sq - aq};
+      if (lane == 63) s_wt[wave] = Sums{sp, scz, sq};
     }
     __syncthreads();
 
-    // ---- per batch: totals from prefix differences, then the model
+    // ---- E: per batch: totals from prefix differences, then the model
     if (tid < count) {
       const int j = tid;
-      const int64_t n = (int64_t)s_lo[j + 1] - s_lo[j];
       const int64_t bg = b + j;
-      if (n == 0) {
+      if (!ne) {
         empty_batch<MODE>(P, bg);
       } else {
-        const Pref xs = s_xs[j], xe = s_xe[j];
-        uint64_t st_pc = xs.pc, st_c = xs.c, st_q = xs.q;
-        uint64_t en_pc = xe.pc, en_c = xe.c, en_q = xe.q;
+        uint32_t k = __builtin_popcountll(s_ball[wave] & ((1ull << lane) - 1ull));
+        for (int w = 0; w < wave; ++w) k += __builtin_popcountll(s_ball[w]);
+        const LanePref xs = s_xs[k], xe = s_xe[k];
+        const Sums ls = s_lb[xs.id], le = s_lb[xe.id];
+        uint64_t p0 = xs.p + ls.p, cz0 = xs.cz + ls.cz, q0 = xs.q + ls.q;
+        uint64_t p1 = xe.p + le.p, cz1 = xe.cz + le.cz, q1 = xe.q + le.q;
         for (uint32_t w = 0; w < (uint32_t)kWaves; ++w) {
-          if (w < xs.w) { st_pc += s_wt[w][0]; st_c += s_wt[w][1]; st_q += s_wt[w][2]; }
-          if (w < xe.w) { en_pc += s_wt[w][0]; en_c += s_wt[w][1]; en_q += s_wt[w][2]; }
+          const Sums t = s_wt[w];
+          if (w < (xs.id >> 6)) { p0 += t.p; cz0 += t.cz; q0 += t.q; }
+          if (w < (xe.id >> 6)) { p1 += t.p; cz1 += t.cz; q1 += t.q; }
         }
-        const uint64_t dpc = en_pc - st_pc;
-        batch_model<MODE>(P, bg, n, dpc & 0xffffffffull, en_c - st_c, en_q - st_q,
-                          (dpc >> 32) != 0, s_k[j]);
+        const int64_t n = (int64_t)s_lo[j + 1] - s_lo[j];
+        const uint64_t Ps = p1 - p0, CZ = cz1 - cz0, Qs = q1 - q0;
+        // decode iff every request processes one token over a nonzero context
+        const bool prefill = (Ps != (uint64_t)n) || ((CZ >> 48) != 0);
+        batch_model<MODE>(P, bg, n, Ps, CZ & kCMask, Qs, prefill, s_k[k]);
       }
     }
     __syncthreads();
 
-    // ---- per request: share (+ tenant) or features
-#pragma unroll
-    for (int k = 0; k < kRounds; ++k) {
-      const uint32_t fl = flags[k];
-      if (!(fl & 0xfu)) continue;
-      const int32_t x0 = wave * kWaveSpan + k * kRoundSpan + lane * kVec;
+    // ---- F: per request: share (+ tenant) or features
+    if (valid) {
       const int64_t pos = ra + x0;
-      const bool full = (fl & 0xfu) == 0xfu;
-      float sv[kVec];
+      uint32_t kcur = 0xffffffffu;
+      double kk[4] = {0.0, 0.0, 0.0, 0.0};
+      const bool full = valid == 0xffffu;
 #pragma unroll
-      for (int q = 0; q < kVec; ++q) {
-        sv[q] = 0.0f;
-        if ((fl >> q) & 1u) {
-          const uint32_t j = (bids[k] >> (8 * q)) & 0xffu;
-          const double kk[4] = {s_k[j][0], s_k[j][1], s_k[j][2], s_k[j][3]};
-          sv[q] = (float)request_out<MODE, HIST, SHARE>(P, kk, pv[k][q], cv[k][q], s_hist,
-                                                        tv[k][q], pos + q, !full);
+      for (int g = 0; g < kVec / 4; ++g) {
+        float sv[4];
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int q = 4 * g + qq;
+          sv[qq] = 0.0f;
+          if ((valid >> q) & 1u) {
+            const uint32_t k = (ords[g] >> (8 * qq)) & 0xffu;
+            if (k != kcur) {
+              kcur = k;
+              kk[0] = s_k[k][0]; kk[1] = s_k[k][1]; kk[2] = s_k[k][2]; kk[3] = s_k[k][3];
+            }
+            sv[qq] = (float)request_out<MODE, HIST, SHARE>(P, kk, pv[q], cv[q], s_hist, tv[q],
+                                                           pos + q, !full);
+          }
         }
-      }
-      if (MODE == MODE_ATTR && SHARE && full) {
-        const v4f v = {sv[0], sv[1], sv[2], sv[3]};
-        __builtin_nontemporal_store(v, (v4f*)(P.share + pos));
+        if (MODE == MODE_ATTR && SHARE && full) {
+          // ordinary (write-back) stores: the four 16-byte stores of a lane
+          // land in the same lines, which L2 merges before writing them out
+          const v4f v = {sv[0], sv[1], sv[2], sv[3]};
+          *(v4f*)(P.share + pos + 4 * g) = v;
+        }
       }
     }
 
