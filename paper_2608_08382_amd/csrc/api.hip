@@ -61,9 +61,11 @@ int device_cus(int* out) {
 }
 
 // Upper bound of the persistent grid for n requests (sizes the workspace):
-// no more than one workgroup per kCap requests, at most kMaxGrid.
+// no more than one workgroup per kWaves wave tiles of requests, at most
+// kMaxGrid.
 int64_t grid_max_for(int64_t n) {
-  const int64_t by_work = (n + kCap - 1) / kCap;
+  const int64_t per = (int64_t)kCap * kWaves;
+  const int64_t by_work = (n + per - 1) / per;
   return by_work < 1 ? 1 : (by_work > kMaxGrid ? kMaxGrid : by_work);
 }
 
@@ -94,8 +96,8 @@ struct Layout {
 Layout layout(int64_t grid, int32_t T) {
   Layout L{};
   size_t o = 0;
-  L.wg_first = o;
-  o += align_up((size_t)(grid + 1) * sizeof(int64_t));
+  L.wg_first = o;  // first batch of each wave worker
+  o += align_up((size_t)(grid * kWaves + 1) * sizeof(int64_t));
   const int64_t chunks = T > 0 ? (T + kTenantChunk - 1) / kTenantChunk : 0;
   L.cnt = o;
   o += align_up((size_t)(chunks > 0 ? chunks : 1) * sizeof(uint32_t));
@@ -196,14 +198,15 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   P.wg_first = wg_first;
   P.partials = hist == HIST_LDS ? (double*)(base + L.partials) : nullptr;
 
-  const int64_t step = tr->n_requests > 0 ? (tr->n_requests + grid - 1) / grid : 1;
+  const int64_t workers = grid * kWaves;
+  const int64_t step = tr->n_requests > 0 ? (tr->n_requests + workers - 1) / workers : 1;
   {
     const int64_t work = tr->n_batches + 1;
     int64_t blocks = (work + kWG - 1) / kWG;
     if (blocks > 4096) blocks = 4096;
     double* zero_buf = hist == HIST_GLOBAL ? P.tenant_sums : nullptr;
     hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, stream, tr->offsets,
-                       tr->n_batches, step, (int)grid, wg_first, cnt, n_cnt, zero_buf,
+                       tr->n_batches, step, (int)workers, wg_first, cnt, n_cnt, zero_buf,
                        (int64_t)(hist == HIST_GLOBAL ? T : 0));
     HIP_TRY(hipGetLastError(), "k_partition launch");
   }

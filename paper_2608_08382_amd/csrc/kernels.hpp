@@ -7,16 +7,16 @@
 // of the chosen set; tenant usage is the sum of its requests' shares.
 //
 // Work decomposition (memory-bound ragged reduction, no dense contraction):
-//  * k_partition: splits the batch list into one contiguous range per
-//    persistent workgroup, balanced by request count.
-//  * k_tiles: each workgroup walks its range in tiles.  A tile is a run of
-//    whole batches whose requests fit in kCap slots (greedy), so every
-//    request is read from HBM once, held in registers while its batch totals
-//    are formed, and its share written once.  Batch totals come from
-//    prefix sums: a wave-level DPP scan per 256-request round, carried across
-//    rounds and waves; the prefix at a batch's first request is subtracted
-//    from the prefix at its last.  Batches that do not fit in a tile go
-//    through a slower two-pass path inside the same workgroup.
+//  * k_partition: splits the batch list into one contiguous range per wave
+//    worker, balanced by request count.
+//  * k_tiles: persistent workgroups of four independent wave workers.  A wave
+//    walks its range in wave tiles: runs of whole batches whose requests fit
+//    in kCap slots (lane l holds 16 consecutive requests), so every request is
+//    read from HBM once, held in registers while its batch totals are formed,
+//    and its share written once.  Batch totals are lane-local run sums added
+//    into per-batch LDS accumulators; batch membership comes from an LDS
+//    bitmask of batch starts and popcounts.  A batch larger than a tile is
+//    handled by the wave in two passes.
 //  * Tenant sums accumulate in an fp64 LDS histogram per workgroup, flushed
 //    once to a [grid][n_tenants] partial array that k_tenant_reduce folds in
 //    a fixed order.
@@ -30,11 +30,7 @@ namespace llmv {
 constexpr int kWG = 256;                     // threads per workgroup
 constexpr int kWaves = kWG / 64;             // wave64
 constexpr int kVec = 16;                     // consecutive requests held per lane
-constexpr int kWaveSpan = 64 * kVec;         // 1024 requests per wave
-constexpr int kCap = kWaveSpan * kWaves;     // 4096 request slots per tile
-constexpr int kMaskWords = kCap / 32;        // batch-start bitmask of a tile
-constexpr int kWindow = 256;                 // offsets examined per tile
-constexpr int kMaxTileBatches = kWindow - 1; // 255 batches per tile
+constexpr int kCap = 2048;                   // request slots per wave tile
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 2048;                   // persistent workgroups, upper bound
 constexpr int kReduceSplit = 16;                 // row blocks in k_tenant_reduce
@@ -164,27 +160,29 @@ __device__ __forceinline__ void empty_batch(const Params& P, int64_t bg) {
   }
 }
 
-// Per-request epilogue: share (+ tenant histogram) or the feature row.
+// Per-request epilogue: the share (+ tenant histogram) or the feature row.
+// Shares: k0 + k1*p + k2*c + k3*p^2 in fp32 from the batch's constants
+// (themselves evaluated in fp64), relative error a few fp32 ulp.
 template <int MODE, int HIST, bool SHARE>
-__device__ __forceinline__ double request_out(const Params& P, const double* k, int32_t p,
-                                              int32_t c, double* s_hist, int32_t t,
-                                              int64_t i, bool store_scalar) {
-  const double pd = (double)p;
+__device__ __forceinline__ float request_out(const Params& P, const float* k, const double* kd,
+                                             int32_t p, int32_t c, double* s_hist, int32_t t,
+                                             int64_t i) {
   if (MODE == MODE_FEAT) {
     if (P.x_req) {
+      const double pd = (double)p;
       const int64_t N = P.N;
-      P.x_req[0 * N + i] = (float)k[0];
+      P.x_req[0 * N + i] = (float)kd[0];
       P.x_req[1 * N + i] = (float)(P.S[1] * pd);
       P.x_req[2 * N + i] = (float)(P.S[2] * (double)c);
       P.x_req[3 * N + i] = (float)(P.S[3] * (pd * pd));
-      P.x_req[4 * N + i] = (float)k[1];
+      P.x_req[4 * N + i] = (float)kd[1];
     }
-    return 0.0;
+    return 0.0f;
   }
-  const double s = k[0] + k[1] * pd + k[2] * (double)c + k[3] * (pd * pd);
-  if (SHARE && store_scalar) P.share[i] = (float)s;
-  if (HIST == HIST_LDS) atomicAdd(s_hist + t, s);
-  if (HIST == HIST_GLOBAL) unsafeAtomicAdd(P.tenant_sums + t, s);
+  const float pf = (float)p;
+  const float s = fmaf(k[3], pf * pf, fmaf(k[2], (float)c, fmaf(k[1], pf, k[0])));
+  if (HIST == HIST_LDS) atomicAdd(s_hist + t, (double)s);
+  if (HIST == HIST_GLOBAL) unsafeAtomicAdd(P.tenant_sums + t, (double)s);
   return s;
 }
 
@@ -210,298 +208,357 @@ __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, int64_t
   for (int64_t i = gid; i < n_zero; i += stride) zero_buf[i] = 0.0;
 }
 
-// ------------------------------------------------------------ big batches
+// ------------------------------------------------------------ wave tiles
+//
+// Every wave is an independent worker over its own contiguous range of
+// batches (no workgroup barriers inside the loop); the four waves of a
+// workgroup share only the LDS tenant histogram.  A wave tile is a run of
+// whole batches whose requests fit in kTile slots from a 16-byte aligned
+// base.  The tile is held in registers as kRounds rounds of 1024 slots: in
+// round r lane l holds slots 1024r + 16l .. 1024r + 16l + 15.
 
-struct BigRed {
-  uint64_t p, c, q, pre;
-};
+constexpr int kRounds = 2;
+constexpr int kRoundSlots = 64 * kVec;          // 1024
+constexpr int kTile = kRounds * kRoundSlots;    // 2048 request slots per wave tile
+constexpr int kTileMaskWords = kTile / 32;      // batch-start bitmask words
+constexpr int kTileBatches = 63;                // batches per wave tile (64 offsets)
+constexpr int kStagePitch = kVec + 4;           // padded lane pitch of the share stage
 
-// One batch too large for a tile, processed by the whole workgroup in two
-// passes over its requests (the second pass mostly hits in L2).
-template <int MODE, int HIST, bool SHARE>
-__device__ void big_batch(const Params& P, int64_t bg, int64_t rs, int64_t re,
-                          double* s_hist, double (*s_k)[4], BigRed* s_red) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  uint64_t sp = 0, sc = 0, sq = 0, pre = 0;
-  for (int64_t i = rs + tid; i < re; i += kWG) {
-    const int32_t p = P.p[i], c = P.c[i];
-    sp += (uint64_t)p;
-    sc += (uint64_t)c;
-    sq += (uint64_t)((int64_t)p * p);
-    pre += (p > 1 || c == 0) ? 1 : 0;
-  }
-  sp = wave_sum_u64(sp);
-  sc = wave_sum_u64(sc);
-  sq = wave_sum_u64(sq);
-  pre = wave_sum_u64(pre);
-  if (lane == 0) s_red[wave] = BigRed{sp, sc, sq, pre};
-  __syncthreads();
-  if (tid == 0) {
-    BigRed t{0, 0, 0, 0};
-    for (int w = 0; w < kWaves; ++w) {
-      t.p += s_red[w].p;
-      t.c += s_red[w].c;
-      t.q += s_red[w].q;
-      t.pre += s_red[w].pre;
-    }
-    batch_model<MODE>(P, bg, re - rs, t.p, t.c, t.q, t.pre > 0, s_k[0]);
-  }
-  __syncthreads();
-  const double k[4] = {s_k[0][0], s_k[0][1], s_k[0][2], s_k[0][3]};
-  for (int64_t i = rs + tid; i < re; i += kWG) {
-    const int32_t t = (HIST != HIST_NONE) ? P.tenant[i] : 0;
-    request_out<MODE, HIST, SHARE>(P, k, P.p[i], P.c[i], s_hist, t, i, true);
-  }
-  __syncthreads();
-}
+constexpr uint64_t kZeroUnit = 1ull << 48;      // count of c == 0, above the c sum
+constexpr uint64_t kCMask = kZeroUnit - 1;
 
-// ----------------------------------------------------------------- tiles
-
-// Running prefix of one request position, relative to the start of its
-// lane's run of kVec requests.  id = lane + 64*wave locates the lane base.
-struct LanePref {
-  uint32_t p;   // sum p
-  uint32_t id;
+struct BatchAcc {
+  uint64_t p;   // sum p
   uint64_t cz;  // sum c (bits 0..47) | count of c == 0 (bits 48..63)
   uint64_t q;   // sum p^2
 };
 
-struct Sums {
-  uint64_t p, cz, q;
+// LDS private to one wave.
+struct WaveLds {
+  uint32_t mask[kTileMaskWords + 2];  // bit x: a nonempty batch starts at slot x
+  BatchAcc acc[kTileBatches];         // per nonempty batch of the tile
+  double k[kTileBatches][4];          // per nonempty batch: share / feature constants
+  float stage[64 * kStagePitch];      // one round of shares, lane-major
 };
 
-constexpr uint64_t kZeroUnit = 1ull << 48;
-constexpr uint64_t kCMask = kZeroUnit - 1;
+// Orders LDS accesses between the lanes of one wave (a wave's LDS accesses
+// complete in order; this keeps the compiler from moving them across).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
-__device__ __forceinline__ uint32_t lds_popc_below(const uint32_t* mask, int pos) {
-  // set bits of the tile bitmask at positions < pos, pos < 32 of its word
-  return __builtin_popcount(mask[pos >> 5] & ((1u << (pos & 31)) - 1u));
+__device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
+  return (int64_t)readlane_u64((uint64_t)v, lane);
+}
+
+// Wave-uniform values held in scalar registers.
+__device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uni(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ uint64_t wave_sum(uint64_t x) {
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
+  x += dpp_u32<0x111, 0xf>(x);
+  x += dpp_u32<0x112, 0xf>(x);
+  x += dpp_u32<0x114, 0xf>(x);
+  x += dpp_u32<0x118, 0xf>(x);
+  x += dpp_u32<0x142, 0xa>(x);
+  x += dpp_u32<0x143, 0xc>(x);
+  return x;
+}
+
+// Loads slots x .. x+15 (x a multiple of 4, x >= 0) of p, c (and tenant);
+// slots at or past N read as 0.
+template <bool TENANT>
+__device__ __forceinline__ void load16(const Params& P, int64_t x, int32_t* pv, int32_t* cv,
+                                       int32_t* tv) {
+  if (x + kVec <= P.N) {
+#pragma unroll
+    for (int g = 0; g < kVec / 4; ++g) {
+      const v4i a = *(const v4i*)(P.p + x + 4 * g);
+      const v4i d = *(const v4i*)(P.c + x + 4 * g);
+      pv[4 * g] = a.x; pv[4 * g + 1] = a.y; pv[4 * g + 2] = a.z; pv[4 * g + 3] = a.w;
+      cv[4 * g] = d.x; cv[4 * g + 1] = d.y; cv[4 * g + 2] = d.z; cv[4 * g + 3] = d.w;
+      if (TENANT) {
+        const v4i t = *(const v4i*)(P.tenant + x + 4 * g);
+        tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < kVec; ++q) {
+      const bool in = x + q < P.N;
+      pv[q] = in ? P.p[x + q] : 0;
+      cv[q] = in ? P.c[x + q] : 0;
+      if (TENANT) tv[q] = in ? P.tenant[x + q] : 0;
+    }
+  }
+}
+
+// Writes one round of shares staged lane-major in the wave's LDS (lane l:
+// slots s0 + 16l .. s0 + 16l + 15, pitch kStagePitch) so that every global
+// store instruction writes 1 KB of consecutive shares.  Only slots in
+// [xf, L) are written.
+__device__ __forceinline__ void store_round(const Params& P, WaveLds& W, int64_t ra, int32_t s0,
+                                            int32_t xf, int32_t L) {
+  const int lane = threadIdx.x & 63;
+  wave_lds_sync();
+#pragma unroll
+  for (int g = 0; g < kVec / 4; ++g) {
+    const int32_t e = 256 * g + 4 * lane;  // slot within the round
+    const int32_t x = s0 + e;              // slot within the tile
+    const float* src = &W.stage[(e >> 4) * kStagePitch + (e & 15)];
+    if (x >= xf && x + 4 <= L) {
+      *(v4f*)(P.share + ra + x) = *(const v4f*)src;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (x + q >= xf && x + q < L) P.share[ra + x + q] = src[q];
+    }
+  }
+  wave_lds_sync();
+}
+
+// One batch too large for a wave tile: two passes over its requests by the
+// whole wave (the second pass mostly hits in L2).
+template <int MODE, int HIST, bool SHARE>
+__device__ void big_batch(const Params& P, WaveLds& W, int64_t bg, int64_t rs, int64_t re,
+                          double* s_hist) {
+  const int lane = threadIdx.x & 63;
+  const int64_t ra = rs & ~(int64_t)3;
+  uint64_t sp = 0, scz = 0, sq = 0;
+  int32_t pv[kVec], cv[kVec], tv[kVec];
+  for (int64_t base = ra; base < re; base += kRoundSlots) {
+    const int64_t x = base + lane * kVec;
+    load16<false>(P, x, pv, cv, tv);
+#pragma unroll
+    for (int q = 0; q < kVec; ++q) {
+      if (x + q >= rs && x + q < re) {
+        const uint32_t p = (uint32_t)pv[q], c = (uint32_t)cv[q];
+        sp += p;
+        scz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
+        sq += (uint64_t)p * p;
+      }
+    }
+  }
+  sp = wave_sum(sp);
+  scz = wave_sum(scz);
+  sq = wave_sum(sq);
+  const int64_t n = re - rs;
+  if (lane == 0) {
+    const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
+    batch_model<MODE>(P, bg, n, sp, scz & kCMask, sq, prefill, W.k[0]);
+  }
+  wave_lds_sync();
+  const double kd[4] = {W.k[0][0], W.k[0][1], W.k[0][2], W.k[0][3]};
+  const float k[4] = {(float)kd[0], (float)kd[1], (float)kd[2], (float)kd[3]};
+  for (int64_t base = ra; base < re; base += kRoundSlots) {
+    const int64_t x = base + lane * kVec;
+    load16<HIST != HIST_NONE>(P, x, pv, cv, tv);
+#pragma unroll
+    for (int g = 0; g < kVec / 4; ++g) {
+      float sv[4];
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        const int q = 4 * g + qq;
+        sv[qq] = 0.0f;
+        if (x + q >= rs && x + q < re)
+          sv[qq] = request_out<MODE, HIST, SHARE>(P, k, kd, pv[q], cv[q], s_hist, tv[q], x + q);
+      }
+      if (MODE == MODE_ATTR && SHARE)
+        *(v4f*)&W.stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
+    }
+    if (MODE == MODE_ATTR && SHARE)
+      store_round(P, W, ra, (int32_t)(base - ra), (int32_t)(rs - ra), (int32_t)(re - ra));
+  }
+  wave_lds_sync();
 }
 
 template <int MODE, int HIST, bool SHARE>
 __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
-  extern __shared__ double s_hist[];       // [n_tenants] when HIST_LDS
-  __shared__ int32_t s_lo[kWindow];        // batch starts relative to the tile base
-  __shared__ uint32_t s_mask[kMaskWords + 1];  // bit x: a nonempty batch starts at x
-  __shared__ uint64_t s_ball[kWaves];      // nonempty flags of the window's batches
-  __shared__ LanePref s_xs[kWindow];       // prefix before each batch's first request
-  __shared__ LanePref s_xe[kWindow];       // prefix through each batch's last request
-  __shared__ Sums s_lb[kWG];               // exclusive prefix of each lane within its wave
-  __shared__ Sums s_wt[kWaves];            // wave totals
-  __shared__ double s_k[kWindow][4];       // per nonempty batch: share / feature constants
-  __shared__ BigRed s_red[kWaves];
+  extern __shared__ double s_hist[];  // [n_tenants] when HIST_LDS
+  __shared__ WaveLds s_wave[kWaves];
+  constexpr bool TEN = HIST != HIST_NONE;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int64_t N = P.N;
-  const int32_t x0 = wave * kWaveSpan + lane * kVec;  // first slot of this lane
+  WaveLds& W = s_wave[tid >> 6];
+  const int32_t x0 = lane * kVec;  // first slot of this lane in a round
 
   if (HIST == HIST_LDS)
     for (int u = tid; u < P.n_tenants; u += kWG) s_hist[u] = 0.0;
-
-  const int64_t bw0 = P.wg_first[blockIdx.x];
-  const int64_t bw1 = P.wg_first[blockIdx.x + 1];
-  int64_t b = bw0;
-  int64_t r0 = 0;  // first request of batch b
-  int64_t wv = 0;  // offsets[b + tid] (window)
-  if (b < bw1) {
-    r0 = P.off[b];
-    if (tid <= min((int64_t)kMaxTileBatches, bw1 - b)) wv = P.off[b + tid];
-  }
   __syncthreads();
 
+  const int64_t worker = (int64_t)blockIdx.x * kWaves + (tid >> 6);
+  const int64_t bw0 = uni(P.wg_first[worker]);
+  const int64_t bw1 = uni(P.wg_first[worker + 1]);
+  int64_t b = bw0;
+  // offsets window: lane j holds offsets[b + j] for j <= min(kTileBatches, bw1 - b)
+  int64_t wv = (b < bw1 && lane <= min((int64_t)kTileBatches, bw1 - b)) ? P.off[b + lane] : 0;
+  int64_t r0 = uni(readlane_i64(wv, 0));  // first request of batch b
+
   while (b < bw1) {
-    // ---- A: window -> s_lo; batches b .. b+count-1 end within kCap slots
-    const int64_t lim = min((int64_t)kMaxTileBatches, bw1 - b);
-    const int64_t ra = r0 & ~(int64_t)3;  // 16-byte aligned tile base
-    int pred = 0;
-    if (tid <= lim) {
-      const int64_t rel = wv - ra;
-      s_lo[tid] = (int32_t)min(rel, (int64_t)kCap + 1);
-      pred = (tid >= 1 && rel <= kCap) ? 1 : 0;
+    // ---- tile: the longest run of whole batches from b within kTile slots
+    const int64_t lim = min((int64_t)kTileBatches, bw1 - b);
+    const int64_t ra = r0 & ~(int64_t)3;
+    const int64_t rel = wv - ra;
+    const uint64_t fits = __ballot(lane >= 1 && lane <= lim && rel <= kTile);
+    const int32_t count = uni((int32_t)__builtin_popcountll(fits));  // a prefix of lanes
+    const int32_t adv = count > 0 ? count : 1;  // batches consumed by this step
+    const int64_t e = b + adv;
+    const int64_t r1 = uni(readlane_i64(wv, adv));
+
+    // next window: lane j takes offsets[e + j] from lane j + adv, or loads it
+    int64_t nwv;
+    {
+      const int64_t sh = __shfl(wv, min(lane + adv, 63), 64);
+      const bool have = lane + adv <= lim;
+      nwv = have ? sh
+                 : ((e < bw1 && lane <= min((int64_t)kTileBatches, bw1 - e)) ? P.off[e + lane] : 0);
     }
-    if (tid <= kMaskWords) s_mask[tid] = 0u;
-    const int count = __syncthreads_count(pred);
 
     if (count == 0) {
-      const int64_t re = P.off[b + 1];
-      big_batch<MODE, HIST, SHARE>(P, b, r0, re, s_hist, s_k, s_red);
-      b += 1;
-      r0 = re;
-      if (b < bw1 && tid <= min((int64_t)kMaxTileBatches, bw1 - b)) wv = P.off[b + tid];
-      continue;
-    }
+      big_batch<MODE, HIST, SHARE>(P, W, b, r0, r1, s_hist);
+    } else {
+      const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
+      const int32_t lo_next = __shfl_down(lo, 1, 64);
+      const int32_t L = (int32_t)(r1 - ra);
+      const int32_t xf = (int32_t)(r0 - ra);
+      const bool ne = lane < count && lo_next > lo;  // batch b+lane is nonempty
+      const uint64_t ne_ball = __ballot(ne);
 
-    const int64_t e = b + count;
-    const int32_t L = s_lo[count];  // tile end relative to ra
-    const int32_t xf = s_lo[0];     // first tile request relative to ra (0..3)
-    const int64_t r1 = ra + L;
-
-    // ---- B: batch-start bits, nonempty ballots; loads of this lane's slots
-    bool ne = false;
-    if (tid < count) {
-      const int32_t lo = s_lo[tid];
-      ne = s_lo[tid + 1] > lo;
-      if (ne) atomicOr(&s_mask[lo >> 5], 1u << (lo & 31));
-    }
-    const uint64_t ball = __ballot(ne);
-    if (lane == 0) s_ball[wave] = ball;
-
-    int64_t nwv = 0;  // window of the next tile, in flight meanwhile
-    if (e < bw1 && tid <= min((int64_t)kMaxTileBatches, bw1 - e)) nwv = P.off[e + tid];
-
-    int32_t pv[kVec], cv[kVec], tv[kVec];
+      // ---- held requests (tenant ids are loaded per round, when needed)
+      int32_t pv[kRounds][kVec], cv[kRounds][kVec];
 #pragma unroll
-    for (int q = 0; q < kVec; ++q) pv[q] = cv[q] = tv[q] = 0;
-    if (x0 < L) {
-      const int32_t* pb = P.p + ra;
-      const int32_t* cb = P.c + ra;
-      const int32_t* tb = P.tenant + ra;
-      if (ra + x0 + kVec <= N) {
+      for (int r = 0; r < kRounds; ++r) {
+        if (r * kRoundSlots + x0 < L) {
+          load16<false>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], nullptr);
+        } else {
 #pragma unroll
-        for (int g = 0; g < kVec / 4; ++g) {
-          const v4i a = *(const v4i*)(pb + x0 + 4 * g);
-          const v4i d = *(const v4i*)(cb + x0 + 4 * g);
-          pv[4 * g] = a.x; pv[4 * g + 1] = a.y; pv[4 * g + 2] = a.z; pv[4 * g + 3] = a.w;
-          cv[4 * g] = d.x; cv[4 * g + 1] = d.y; cv[4 * g + 2] = d.z; cv[4 * g + 3] = d.w;
-          if (HIST != HIST_NONE) {
-            const v4i t = *(const v4i*)(tb + x0 + 4 * g);
-            tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
-          }
+          for (int q = 0; q < kVec; ++q) pv[r][q] = cv[r][q] = 0;
         }
-      } else {
+      }
+
+      // ---- batch-start bitmask, accumulators
+      if (lane < kTileMaskWords + 2) W.mask[lane] = 0u;
+      if (lane < count) W.acc[lane] = BatchAcc{0, 0, 0};
+      wave_lds_sync();
+      if (ne) atomicOr(&W.mask[lo >> 5], 1u << (lo & 31));
+      wave_lds_sync();
+
+      uint32_t bits[kRounds], ord0[kRounds], valid[kRounds];
+      {
+        uint32_t before = 0;  // starts in earlier rounds
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) {
+          const int32_t s = r * kRoundSlots + x0;
+          bits[r] = (W.mask[s >> 5] >> (s & 16)) & 0xffffu;
+          const uint32_t h = __builtin_popcount(bits[r]);
+          const uint32_t hs = wave_incl_scan_u32(h);
+          ord0[r] = before + hs - h;  // nonempty batches starting before slot s
+          before += (uint32_t)__builtin_amdgcn_readlane((int)hs, 63);
+          const int32_t a = max(xf - s, 0), z = min(L - s, kVec);
+          valid[r] = z > a ? (((1u << (z - a)) - 1u) << a) & 0xffffu : 0u;
+        }
+      }
+
+      // ---- batch sums: lane-local runs, added into the batch accumulators
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) {
+        // a run ends where a batch starts at the next slot, at the last valid
+        // slot, or at the end of the lane's slots
+        const uint32_t ends =
+            ((bits[r] >> 1) | (1u << (kVec - 1)) | (valid[r] & ~(valid[r] >> 1))) & valid[r];
+        uint32_t rp = 0;
+        uint64_t rcz = 0, rq = 0;
 #pragma unroll
         for (int q = 0; q < kVec; ++q) {
-          if (ra + x0 + q < N) {
-            pv[q] = pb[x0 + q];
-            cv[q] = cb[x0 + q];
-            if (HIST != HIST_NONE) tv[q] = tb[x0 + q];
-          }
-        }
-      }
-    }
-    __syncthreads();
-
-    // ---- C: ordinal of each held request's batch among the tile's
-    // nonempty batches, from the batch-start bitmask
-    const uint32_t w0 = s_mask[x0 >> 5];
-    const uint32_t bits = (w0 >> (x0 & 16)) & 0xffffu;  // starts at x0 .. x0+15
-    const uint32_t next_bit = (s_mask[(x0 + kVec) >> 5] >> ((x0 + kVec) & 31)) & 1u;
-    uint32_t wave_base = 0;  // starts in the slots of earlier waves
-    if (wave > 0) {
-      uint32_t cnt = 0;
-      if (lane < 32 * wave) cnt += __builtin_popcount(s_mask[lane]);
-      if (lane + 64 < 32 * wave) cnt += __builtin_popcount(s_mask[lane + 64]);
-      for (int m = 32; m >= 1; m >>= 1) cnt += __shfl_xor(cnt, m, 64);
-      wave_base = cnt;
-    }
-    const uint32_t h = __builtin_popcount(bits);
-    uint32_t hs = h;  // inclusive wave scan of the lanes' start counts
-    hs += dpp_u32<0x111, 0xf>(hs);
-    hs += dpp_u32<0x112, 0xf>(hs);
-    hs += dpp_u32<0x114, 0xf>(hs);
-    hs += dpp_u32<0x118, 0xf>(hs);
-    hs += dpp_u32<0x142, 0xa>(hs);
-    hs += dpp_u32<0x143, 0xc>(hs);
-    const uint32_t ord0 = wave_base + hs - h;  // starts before x0
-
-    // ---- D: one pass over the lane's requests: lane-relative prefixes at
-    // batch starts and ends, lane totals
-    uint32_t ords[kVec / 4];  // 8-bit ordinal per held request
-    uint32_t valid = 0;
-    uint32_t ap = 0;
-    uint64_t acz = 0, aq = 0;
-    {
-      uint32_t ord = ord0;
-#pragma unroll
-      for (int q = 0; q < kVec; ++q) {
-        const int32_t x = x0 + q;
-        const bool v = (x >= xf) && (x < L);
-        const uint32_t st = (bits >> q) & 1u;
-        const uint32_t en = ((q + 1 < kVec ? (bits >> (q + 1)) : next_bit) & 1u) | (x + 1 == L);
-        ord += st;
-        const uint32_t k = ord - 1u;
-        if (q % 4 == 0) ords[q / 4] = 0;
-        ords[q / 4] |= (k & 0xffu) << (8 * (q % 4));
-        if (v) {
-          valid |= 1u << q;
-          const uint32_t p = (uint32_t)pv[q];
-          const uint32_t c = (uint32_t)cv[q];
-          if (st) s_xs[k] = LanePref{ap, (uint32_t)tid, acz, aq};
-          ap += p;
-          acz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
-          aq += (uint64_t)p * p;
-          if (en) s_xe[k] = LanePref{ap, (uint32_t)tid, acz, aq};
-        }
-      }
-    }
-    {
-      const uint64_t sp = wave_incl_scan((uint64_t)ap);
-      const uint64_t scz = wave_incl_scan(acz);
-      const uint64_t sq = wave_incl_scan(aq);
-      s_lb[tid] = Sums{sp - ap, scz - acz, sq - aq};
-      if (lane == 63) s_wt[wave] = Sums{sp, scz, sq};
-    }
-    __syncthreads();
-
-    // ---- E: per batch: totals from prefix differences, then the model
-    if (tid < count) {
-      const int j = tid;
-      const int64_t bg = b + j;
-      if (!ne) {
-        empty_batch<MODE>(P, bg);
-      } else {
-        uint32_t k = __builtin_popcountll(s_ball[wave] & ((1ull << lane) - 1ull));
-        for (int w = 0; w < wave; ++w) k += __builtin_popcountll(s_ball[w]);
-        const LanePref xs = s_xs[k], xe = s_xe[k];
-        const Sums ls = s_lb[xs.id], le = s_lb[xe.id];
-        uint64_t p0 = xs.p + ls.p, cz0 = xs.cz + ls.cz, q0 = xs.q + ls.q;
-        uint64_t p1 = xe.p + le.p, cz1 = xe.cz + le.cz, q1 = xe.q + le.q;
-        for (uint32_t w = 0; w < (uint32_t)kWaves; ++w) {
-          const Sums t = s_wt[w];
-          if (w < (xs.id >> 6)) { p0 += t.p; cz0 += t.cz; q0 += t.q; }
-          if (w < (xe.id >> 6)) { p1 += t.p; cz1 += t.cz; q1 += t.q; }
-        }
-        const int64_t n = (int64_t)s_lo[j + 1] - s_lo[j];
-        const uint64_t Ps = p1 - p0, CZ = cz1 - cz0, Qs = q1 - q0;
-        // decode iff every request processes one token over a nonzero context
-        const bool prefill = (Ps != (uint64_t)n) || ((CZ >> 48) != 0);
-        batch_model<MODE>(P, bg, n, Ps, CZ & kCMask, Qs, prefill, s_k[k]);
-      }
-    }
-    __syncthreads();
-
-    // ---- F: per request: share (+ tenant) or features
-    if (valid) {
-      const int64_t pos = ra + x0;
-      uint32_t kcur = 0xffffffffu;
-      double kk[4] = {0.0, 0.0, 0.0, 0.0};
-      const bool full = valid == 0xffffu;
-#pragma unroll
-      for (int g = 0; g < kVec / 4; ++g) {
-        float sv[4];
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const int q = 4 * g + qq;
-          sv[qq] = 0.0f;
-          if ((valid >> q) & 1u) {
-            const uint32_t k = (ords[g] >> (8 * qq)) & 0xffu;
-            if (k != kcur) {
-              kcur = k;
-              kk[0] = s_k[k][0]; kk[1] = s_k[k][1]; kk[2] = s_k[k][2]; kk[3] = s_k[k][3];
+          if ((valid[r] >> q) & 1u) {
+            const uint32_t p = (uint32_t)pv[r][q], c = (uint32_t)cv[r][q];
+            rp += p;
+            rcz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
+            rq += (uint64_t)p * p;
+            if ((ends >> q) & 1u) {
+              const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
+              atomicAdd((unsigned long long*)&W.acc[k].p, (unsigned long long)rp);
+              atomicAdd((unsigned long long*)&W.acc[k].cz, (unsigned long long)rcz);
+              atomicAdd((unsigned long long*)&W.acc[k].q, (unsigned long long)rq);
+              rp = 0;
+              rcz = 0;
+              rq = 0;
             }
-            sv[qq] = (float)request_out<MODE, HIST, SHARE>(P, kk, pv[q], cv[q], s_hist, tv[q],
-                                                           pos + q, !full);
           }
         }
-        if (MODE == MODE_ATTR && SHARE && full) {
-          // ordinary (write-back) stores: the four 16-byte stores of a lane
-          // land in the same lines, which L2 merges before writing them out
-          const v4f v = {sv[0], sv[1], sv[2], sv[3]};
-          *(v4f*)(P.share + pos + 4 * g) = v;
+      }
+      wave_lds_sync();
+
+      // ---- per batch (lane j holds batch b+j): the model
+      if (lane < count) {
+        const int64_t bg = b + lane;
+        if (!ne) {
+          empty_batch<MODE>(P, bg);
+        } else {
+          const uint32_t k = __builtin_popcountll(ne_ball & ((1ull << lane) - 1ull));
+          const BatchAcc a = W.acc[k];
+          const int64_t n = (int64_t)lo_next - lo;
+          // decode iff every request processes one token over a nonzero context
+          const bool prefill = (a.p != (uint64_t)n) || ((a.cz >> 48) != 0);
+          batch_model<MODE>(P, bg, n, a.p, a.cz & kCMask, a.q, prefill, W.k[k]);
         }
       }
+      wave_lds_sync();
+
+      // ---- per request: share (+ tenant) or features
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) {
+        if (r * kRoundSlots >= L) break;  // wave-uniform
+        const int64_t pos = ra + r * kRoundSlots + x0;
+        int32_t tv[kVec];
+        if (TEN) {
+          if (valid[r]) {
+            int32_t dp[kVec], dc[kVec];
+            load16<true>(P, pos, dp, dc, tv);  // only the tenant loads survive
+          } else {
+#pragma unroll
+            for (int q = 0; q < kVec; ++q) tv[q] = 0;
+          }
+        }
+        uint32_t kcur = 0xffffffffu;
+        float kk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        double kd[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int g = 0; g < kVec / 4; ++g) {
+          float sv[4];
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) {
+            const int q = 4 * g + qq;
+            sv[qq] = 0.0f;
+            if ((valid[r] >> q) & 1u) {
+              const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
+              if (k != kcur) {
+                kcur = k;
+                kd[0] = W.k[k][0]; kd[1] = W.k[k][1]; kd[2] = W.k[k][2]; kd[3] = W.k[k][3];
+                kk[0] = (float)kd[0]; kk[1] = (float)kd[1]; kk[2] = (float)kd[2]; kk[3] = (float)kd[3];
+              }
+              sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist,
+                                                      TEN ? tv[q] : 0, pos + q);
+            }
+          }
+          if (MODE == MODE_ATTR && SHARE)
+            *(v4f*)&W.stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
+        }
+        if (MODE == MODE_ATTR && SHARE) store_round(P, W, ra, r * kRoundSlots, xf, L);
+      }
+      wave_lds_sync();
     }
 
     b = e;
