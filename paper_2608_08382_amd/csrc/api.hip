@@ -89,7 +89,7 @@ int64_t grid_for(int64_t n, int cus, int per_cu) {
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
 
 struct Layout {
-  size_t wg_first, cnt, partials, part2, flag, total;
+  size_t wg_first, partials, flag, total;
 };
 
 // Workspace layout shared by every entry point.
@@ -98,13 +98,8 @@ Layout layout(int64_t grid, int32_t T) {
   size_t o = 0;
   L.wg_first = o;  // first batch of each wave worker
   o += align_up((size_t)(grid * kWaves + 1) * sizeof(int64_t));
-  const int64_t chunks = T > 0 ? (T + kTenantChunk - 1) / kTenantChunk : 0;
-  L.cnt = o;
-  o += align_up((size_t)(chunks > 0 ? chunks : 1) * sizeof(uint32_t));
   L.partials = o;
   if (lds_hist(T)) o += align_up((size_t)grid * (size_t)T * sizeof(double));
-  L.part2 = o;
-  if (lds_hist(T)) o += align_up((size_t)chunks * kReduceSplit * kTenantChunk * sizeof(double));
   L.flag = o;
   o += align_up(sizeof(int));
   L.total = o;
@@ -192,8 +187,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   const int64_t grid = grid_for(tr->n_requests, cus, blocks_per_cu(kern, dyn));
   char* base = (char*)ws;
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
-  uint32_t* cnt = (uint32_t*)(base + L.cnt);
-  const int n_cnt = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
+  const int n_chunks = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
   P.wg_first = wg_first;
   P.partials = hist == HIST_LDS ? (double*)(base + L.partials) : nullptr;
@@ -206,7 +200,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
     if (blocks > 4096) blocks = 4096;
     double* zero_buf = hist == HIST_GLOBAL ? P.tenant_sums : nullptr;
     hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, stream, tr->offsets,
-                       tr->n_batches, step, (int)workers, wg_first, cnt, n_cnt, zero_buf,
+                       tr->n_batches, step, (int)workers, wg_first, zero_buf,
                        (int64_t)(hist == HIST_GLOBAL ? T : 0));
     HIP_TRY(hipGetLastError(), "k_partition launch");
   }
@@ -217,9 +211,8 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
 
   if (hist == HIST_LDS) {
-    hipLaunchKernelGGL(k_tenant_reduce, dim3(kReduceSplit, (unsigned)n_cnt), dim3(kWG), 0, stream,
-                       (const double*)P.partials, (int)grid, (int)T, (double*)(base + L.part2),
-                       cnt, P.tenant_sums);
+    hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)n_chunks), dim3(64 * kReduceWaves), 0, stream,
+                       (const double*)P.partials, (int)grid, (int)T, P.tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
   }
   return LLMV_OK;
@@ -315,27 +308,26 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
   char* base = (char*)ws;
-  uint32_t* cnt = (uint32_t*)(base + L.cnt);
-  const int n_cnt = (n_tenants + kTenantChunk - 1) / kTenantChunk;
+  const int n_chunks = (n_tenants + kTenantChunk - 1) / kTenantChunk;
   const bool lds = lds_hist(n_tenants);
   const int64_t grid =
       lds ? grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_LDS>, (size_t)n_tenants * sizeof(double)))
           : grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_GLOBAL>, 0));
-  // Clear the counters (and the output for the atomics path) with the
-  // partition kernel on an empty batch list.
-  hipLaunchKernelGGL(k_partition, dim3(16), dim3(kWG), 0, s, (const int64_t*)nullptr, (int64_t)-1,
-                     (int64_t)1, 0, (int64_t*)(base + L.wg_first), cnt, n_cnt,
-                     lds ? (double*)nullptr : tenant_sums, (int64_t)(lds ? 0 : n_tenants));
-  HIP_TRY(hipGetLastError(), "k_partition launch");
+  if (!lds) {
+    // the atomics path accumulates into the output: clear it first
+    hipLaunchKernelGGL(k_partition, dim3(16), dim3(kWG), 0, s, (const int64_t*)nullptr,
+                       (int64_t)-1, (int64_t)1, 0, (int64_t*)nullptr, tenant_sums,
+                       (int64_t)n_tenants);
+    HIP_TRY(hipGetLastError(), "k_partition launch");
+  }
   if (lds) {
     double* partials = (double*)(base + L.partials);
     hipLaunchKernelGGL(k_tenant_hist<HIST_LDS>, dim3((unsigned)grid), dim3(kWG),
                        (size_t)n_tenants * sizeof(double), s, tenant, share, n, n_tenants,
                        partials, tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_hist launch");
-    hipLaunchKernelGGL(k_tenant_reduce, dim3(kReduceSplit, (unsigned)n_cnt), dim3(kWG), 0, s,
-                       (const double*)partials, (int)grid, (int)n_tenants,
-                       (double*)(base + L.part2), cnt, tenant_sums);
+    hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)n_chunks), dim3(64 * kReduceWaves), 0, s,
+                       (const double*)partials, (int)grid, (int)n_tenants, tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
   } else {
     hipLaunchKernelGGL(k_tenant_hist<HIST_GLOBAL>, dim3((unsigned)grid), dim3(kWG), 0, s, tenant,

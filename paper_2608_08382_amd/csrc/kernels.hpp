@@ -29,11 +29,13 @@ namespace llmv {
 
 constexpr int kWG = 256;                     // threads per workgroup
 constexpr int kWaves = kWG / 64;             // wave64
-constexpr int kVec = 16;                     // consecutive requests held per lane
-constexpr int kCap = 2048;                   // request slots per wave tile
+#ifndef LLMV_LANE_SLOTS
+#define LLMV_LANE_SLOTS 24
+#endif
+constexpr int kVec = LLMV_LANE_SLOTS;        // consecutive requests held per lane
+constexpr int kCap = 64 * kVec;              // request slots per wave tile
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 2048;                   // persistent workgroups, upper bound
-constexpr int kReduceSplit = 16;                 // row blocks in k_tenant_reduce
 constexpr int kTenantChunk = 64;                 // tenants per k_tenant_reduce block
 
 enum { MODE_ATTR = 0, MODE_FEAT = 1 };
@@ -189,11 +191,10 @@ __device__ __forceinline__ float request_out(const Params& P, const float* k, co
 // ------------------------------------------------------------ partition
 
 // wg_first[w] = first batch whose start offset is >= w*step (w < grid),
-// wg_first[grid] = nB.  Also clears the reduction counters and, for the
-// global-atomics tenant path, the tenant sums.
+// wg_first[grid] = nB.  Also clears zero_buf (the tenant sums of the
+// global-atomics tenant path).
 __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, int64_t step,
                             int grid, int64_t* __restrict__ wg_first,
-                            uint32_t* __restrict__ cnt, int n_cnt,
                             double* __restrict__ zero_buf, int64_t n_zero) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -203,8 +204,7 @@ __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, int64_t
                                   : min((int64_t)grid - 1, off[b] / step);
     for (int64_t w = wlo; w <= whi; ++w) wg_first[w] = b;
   }
-  if (gid == 0) wg_first[grid] = nB;
-  for (int64_t i = gid; i < n_cnt; i += stride) cnt[i] = 0;
+  if (gid == 0 && wg_first) wg_first[grid] = nB;
   for (int64_t i = gid; i < n_zero; i += stride) zero_buf[i] = 0.0;
 }
 
@@ -217,9 +217,9 @@ __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, int64_t
 // base.  The tile is held in registers as kRounds rounds of 1024 slots: in
 // round r lane l holds slots 1024r + 16l .. 1024r + 16l + 15.
 
-constexpr int kRounds = 2;
-constexpr int kRoundSlots = 64 * kVec;          // 1024
-constexpr int kTile = kRounds * kRoundSlots;    // 2048 request slots per wave tile
+constexpr int kRounds = 1;
+constexpr int kRoundSlots = 64 * kVec;
+constexpr int kTile = kRounds * kRoundSlots;    // request slots per wave tile
 constexpr int kTileMaskWords = kTile / 32;      // batch-start bitmask words
 constexpr int kTileBatches = 63;                // batches per wave tile (64 offsets)
 constexpr int kStagePitch = kVec + 4;           // padded lane pitch of the share stage
@@ -239,6 +239,7 @@ struct WaveLds {
   BatchAcc acc[kTileBatches];         // per nonempty batch of the tile
   double k[kTileBatches][4];          // per nonempty batch: share / feature constants
   float stage[64 * kStagePitch];      // one round of shares, lane-major
+  static_assert(kVec % 4 == 0 && kVec <= 28, "lane slots: multiple of 4, bits fit a word pair");
 };
 
 // Orders LDS accesses between the lanes of one wave (a wave's LDS accesses
@@ -304,6 +305,21 @@ __device__ __forceinline__ void load16(const Params& P, int64_t x, int32_t* pv, 
   }
 }
 
+// Loads tenant ids of slots x .. x+kVec-1 (x a multiple of 4); slots at or
+// past N read as 0.
+__device__ __forceinline__ void load_tenants(const Params& P, int64_t x, int32_t* tv) {
+  if (x + kVec <= P.N) {
+#pragma unroll
+    for (int g = 0; g < kVec / 4; ++g) {
+      const v4i t = *(const v4i*)(P.tenant + x + 4 * g);
+      tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < kVec; ++q) tv[q] = x + q < P.N ? P.tenant[x + q] : 0;
+  }
+}
+
 // Writes one round of shares staged lane-major in the wave's LDS (lane l:
 // slots s0 + 16l .. s0 + 16l + 15, pitch kStagePitch) so that every global
 // store instruction writes 1 KB of consecutive shares.  Only slots in
@@ -316,7 +332,7 @@ __device__ __forceinline__ void store_round(const Params& P, WaveLds& W, int64_t
   for (int g = 0; g < kVec / 4; ++g) {
     const int32_t e = 256 * g + 4 * lane;  // slot within the round
     const int32_t x = s0 + e;              // slot within the tile
-    const float* src = &W.stage[(e >> 4) * kStagePitch + (e & 15)];
+    const float* src = &W.stage[(e / kVec) * kStagePitch + (e % kVec)];
     if (x >= xf && x + 4 <= L) {
       *(v4f*)(P.share + ra + x) = *(const v4f*)src;
     } else {
@@ -461,13 +477,14 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
 #pragma unroll
         for (int r = 0; r < kRounds; ++r) {
           const int32_t s = r * kRoundSlots + x0;
-          bits[r] = (W.mask[s >> 5] >> (s & 16)) & 0xffffu;
+          const uint64_t w2 = ((uint64_t)W.mask[(s >> 5) + 1] << 32) | W.mask[s >> 5];
+          bits[r] = (uint32_t)(w2 >> (s & 31)) & ((1u << kVec) - 1u);
           const uint32_t h = __builtin_popcount(bits[r]);
           const uint32_t hs = wave_incl_scan_u32(h);
           ord0[r] = before + hs - h;  // nonempty batches starting before slot s
           before += (uint32_t)__builtin_amdgcn_readlane((int)hs, 63);
           const int32_t a = max(xf - s, 0), z = min(L - s, kVec);
-          valid[r] = z > a ? (((1u << (z - a)) - 1u) << a) & 0xffffu : 0u;
+          valid[r] = z > a ? (((1u << (z - a)) - 1u) << a) & ((1u << kVec) - 1u) : 0u;
         }
       }
 
@@ -525,8 +542,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
         int32_t tv[kVec];
         if (TEN) {
           if (valid[r]) {
-            int32_t dp[kVec], dc[kVec];
-            load16<true>(P, pos, dp, dc, tv);  // only the tenant loads survive
+            load_tenants(P, pos, tv);
           } else {
 #pragma unroll
             for (int q = 0; q < kVec; ++q) tv[q] = 0;
@@ -575,44 +591,37 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
 
 // ------------------------------------------------------ tenant reductions
 
-// out[u] = sum over rows w of part[w][u], rows folded in a fixed order:
-// block (s, x) sums rows of slice s for tenants x*64.., writes part2, and the
-// last block of column x (counter, reset on the way out) adds the slices in
-// order s = 0..S-1.
-__global__ __launch_bounds__(kWG) void k_tenant_reduce(const double* __restrict__ part,
-                                                       int rows, int T,
-                                                       double* __restrict__ part2,
-                                                       uint32_t* __restrict__ cnt,
-                                                       double* __restrict__ out) {
-  __shared__ double red[kWaves][kTenantChunk];
-  __shared__ int last;
-  const int S = gridDim.x, s = blockIdx.x, x = blockIdx.y;
+// out[u] = sum over rows w of part[w][u], folded in a fixed order.  One
+// block of kReduceWaves waves per 64 tenants: wave v sums rows v, v +
+// kReduceWaves, ... with eight independent partial sums (eight loads in
+// flight per lane), then the waves' sums are added in wave order.
+constexpr int kReduceWaves = 16;
+
+__global__ __launch_bounds__(64 * kReduceWaves) void k_tenant_reduce(
+    const double* __restrict__ part, int rows, int T, double* __restrict__ out) {
+  __shared__ double red[kReduceWaves][kTenantChunk];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int u = x * kTenantChunk + lane;
-  const int w0 = (int)((int64_t)s * rows / S), w1 = (int)((int64_t)(s + 1) * rows / S);
+  const int u = blockIdx.x * kTenantChunk + lane;
   double acc = 0.0;
-  if (u < T)
-    for (int w = w0 + wave; w < w1; w += kWaves) acc += part[(int64_t)w * T + u];
+  if (u < T) {
+    double a8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int w = wave;
+    for (; w + 7 * kReduceWaves < rows; w += 8 * kReduceWaves) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a8[i] += part[(int64_t)(w + i * kReduceWaves) * T + u];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (w + i * kReduceWaves < rows) a8[i] += part[(int64_t)(w + i * kReduceWaves) * T + u];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += a8[i];
+  }
   red[wave][lane] = acc;
   __syncthreads();
-  if (wave == 0) {
-    double v = red[0][lane];
-    for (int w = 1; w < kWaves; ++w) v += red[w][lane];
-    part2[((int64_t)x * S + s) * kTenantChunk + lane] = v;
-  }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) last = (atomicAdd(cnt + x, 1u) == (uint32_t)(S - 1));
-  __syncthreads();
-  if (last) {
-    __threadfence();
-    if (wave == 0 && u < T) {
-      double v = 0.0;
-      for (int k = 0; k < S; ++k)
-        v += __builtin_nontemporal_load(part2 + ((int64_t)x * S + k) * kTenantChunk + lane);
-      out[u] = v;
-    }
-    if (threadIdx.x == 0) cnt[x] = 0;
+  if (wave == 0 && u < T) {
+    double t = red[0][lane];
+    for (int v = 1; v < kReduceWaves; ++v) t += red[v][lane];
+    out[u] = t;
   }
 }
 
