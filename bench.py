@@ -98,6 +98,58 @@ def cpu_baseline(tr, coeffs, gpu_out, budget_s=30.0):
             "sample": sample, "seconds": round(dt, 3)}, stats
 
 
+def bench_sweep(hip, stream, with_oracle):
+    """What-if sweep: tenant sums of the 100k-batch mixed trace under 4 model
+    shapes x 256 coefficient vectors, one llmv_attribute_sweep call."""
+    import numpy as np
+    import torch
+    import tracegen
+    from paper_2608_08382_amd import llmv
+
+    tr = tracegen.config_trace("whatif-sweep")
+    co = tracegen.sweep_coeffs(tracegen.config_coeffs("whatif-sweep"), 256)
+    names = ["llama3.1-8b", "qwen2.5-14b", "qwen2.5-32b", "70b-like"]
+    shapes = [tracegen.SHAPES[k] for k in names]
+    dt = llmv.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    out = torch.empty((4, 256, tr.n_tenants), dtype=torch.float64, device=dt.p.device)
+    ws = llmv.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+    llmv.llmv_attribute_sweep(dt, shapes, co, tr.n_tenants, out, ws)
+    torch.cuda.synchronize()
+    reps = 3
+    evs = [(hip.create(), hip.create()) for _ in range(reps)]
+    for a, b in evs:
+        hip.record(a, stream)
+        llmv.llmv_attribute_sweep(dt, shapes, co, tr.n_tenants, out, ws)
+        hip.record(b, stream)
+    torch.cuda.synchronize()
+    ms = sorted(hip.elapsed_ms(a, b) for a, b in evs)[reps // 2]
+    variants = 4 * 256
+    res = {"metric": "attributed request-variants/sec", "value": tr.n_requests * variants / (ms / 1e3),
+           "unit": "request-variants/s", "ms": ms, "variants": variants,
+           "n_requests": tr.n_requests, "n_batches": tr.n_batches, "n_tenants": tr.n_tenants}
+    log(f"[bench] what-if sweep: {variants} variants in {ms:.2f} ms, "
+        f"{res['value']:.3e} request-variants/s")
+    if with_oracle:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import parity
+        host = out.cpu().numpy()
+        sample = [(0, 0), (1, 64), (2, 128), (3, 255)]
+        t0 = time.perf_counter()
+        worst = 0.0
+        for s, v in sample:
+            ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shapes[s], co[v],
+                                   tr.n_tenants, ("tenant_sums",))["tenant_sums"]
+            worst = max(worst, float(parity.rel_err(host[s, v], ref).max()))
+        dt_o = time.perf_counter() - t0
+        assert worst <= parity.RTOL, worst
+        res["cpu_baseline"] = {"value": tr.n_requests * len(sample) / dt_o,
+                               "unit": "request-variants/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{len(sample)} of {variants} variants, full trace"}
+        res["parity_tenant_max_rel_err"] = worst
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +160,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true",
                     help="also time the step with subsets of the outputs (stderr)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the what-if sweep measurement (4 shapes x 256 coefficient vectors)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="also run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -233,6 +287,10 @@ def main():
         result["cpu_baseline"] = cb
         result["parity"] = {k: v for k, v in stats.items()}
         log(f"[bench] oracle {cb['value']:.3e} req/s on {cb['cores']} core; parity {stats}")
+    if not args.no_sweep:
+        del gpu_out, dt, lat, reg, share, tsum, ws
+        torch.cuda.empty_cache()
+        result["whatif_sweep"] = bench_sweep(hip, stream, not args.no_cpu_baseline)
     print(json.dumps(result), flush=True)
 
 

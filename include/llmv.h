@@ -125,6 +125,24 @@ int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
                    float *share, int32_t n_tenants, double *tenant_sums,
                    void *ws, size_t ws_bytes, void *stream);
 
+/* What-if sweep (Sec. 1: fast "what-if" planning over alternative model
+ * and coefficient settings; Eq. 1 and Sec. 2 Problem formulation for each):
+ * the tenant sums of one trace under every pair (shape s, coefficient vector
+ * v).
+ *   shapes   host [n_shapes] llmv_shape, or NULL with n_shapes == 1 for the
+ *            unit shape.
+ *   coeffs   host [n_coeffs][20] finite fp32, laid out as in llmv_attribute.
+ *   n_tenants, trace->tenant as for llmv_attribute's tenant sums.
+ *   out      device [n_shapes][n_coeffs][n_tenants] fp64, overwritten:
+ *            out[(s*n_coeffs + v)*n_tenants + u] = L_u under (s, v).
+ * Equivalent to n_shapes*n_coeffs calls of llmv_attribute with only
+ * tenant_sums requested (same results); the batch partition is computed once.
+ * n_tenants must be <= 4096 here.  The workspace is llmv_workspace_size's. */
+int llmv_attribute_sweep(const llmv_trace *trace, const llmv_shape *shapes,
+                         int32_t n_shapes, const float *coeffs, int32_t n_coeffs,
+                         int32_t n_tenants, double *out, void *ws, size_t ws_bytes,
+                         void *stream);
+
 /* Request and batch features (Sec. 2.1), structure of arrays:
  *   x_req   device [5][n_requests] fp32, element k of request i at
  *           x_req[k*n_requests + i]: (S0/|B|, S1*p_i, S2*c_i, S3*p_i^2, |B|),

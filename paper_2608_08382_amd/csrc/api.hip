@@ -275,6 +275,71 @@ int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float
                    (hipStream_t)stream);
 }
 
+int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shapes,
+                         const float* coeffs, int32_t n_coeffs, int32_t n_tenants, double* out,
+                         void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_trace(trace, true);
+  if (rc) return rc;
+  if (n_shapes < 1 || (!shapes && n_shapes != 1))
+    return fail(LLMV_EINVAL, "n_shapes=%d (NULL shapes needs n_shapes == 1)", n_shapes);
+  if (n_coeffs < 1 || !coeffs) return fail(LLMV_EINVAL, "n_coeffs=%d or coeffs NULL", n_coeffs);
+  if (!lds_hist(n_tenants))
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, %d] for the sweep", n_tenants, kHistLdsMax);
+  if (!out) return fail(LLMV_EINVAL, "out is NULL");
+  for (int64_t i = 0; i < (int64_t)n_coeffs * 20; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%lld] is not finite", (long long)i);
+  double S[64][4];
+  if (n_shapes > 64) return fail(LLMV_EINVAL, "n_shapes=%d > 64", n_shapes);
+  for (int s = 0; s < n_shapes; ++s) {
+    rc = shape_constants(shapes ? &shapes[s] : nullptr, S[s]);
+    if (rc) return rc;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  int cus = 0;
+  rc = device_cus(&cus);
+  if (rc) return rc;
+  const Layout L = layout(grid_max_for(trace->n_requests), n_tenants);
+  rc = check_ws(ws, ws_bytes, L.total);
+  if (rc) return rc;
+  char* base = (char*)ws;
+  const size_t dyn = (size_t)n_tenants * sizeof(double);
+  const TileKernel kern = pick_tiles(MODE_ATTR, HIST_LDS, false);
+  const int64_t grid = grid_for(trace->n_requests, cus, blocks_per_cu(kern, dyn));
+  const int64_t workers = grid * kWaves;
+  Params P{};
+  P.off = trace->offsets;
+  P.p = trace->p;
+  P.c = trace->c;
+  P.tenant = trace->tenant;
+  P.nB = trace->n_batches;
+  P.N = trace->n_requests;
+  P.wg_first = (int64_t*)(base + L.wg_first);
+  P.partials = (double*)(base + L.partials);
+  P.n_tenants = n_tenants;
+  {
+    const int64_t step = P.N > 0 ? (P.N + workers - 1) / workers : 1;
+    int64_t blocks = (P.nB + 1 + kWG - 1) / kWG;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, st, P.off, P.nB, step,
+                       (int)workers, (int64_t*)P.wg_first, (double*)nullptr, (int64_t)0);
+    HIP_TRY(hipGetLastError(), "k_partition launch");
+  }
+  const int n_chunks = (n_tenants + kTenantChunk - 1) / kTenantChunk;
+  for (int s = 0; s < n_shapes; ++s) {
+    for (int k = 0; k < 4; ++k) P.S[k] = S[s][k];
+    for (int v = 0; v < n_coeffs; ++v) {
+      for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[(int64_t)v * 20 + i];
+      double* dst = out + ((int64_t)s * n_coeffs + v) * n_tenants;
+      hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, P);
+      HIP_TRY(hipGetLastError(), "k_tiles launch");
+      hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)n_chunks), dim3(64 * kReduceWaves), 0, st,
+                         (const double*)P.partials, (int)grid, (int)n_tenants, dst);
+      HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+    }
+  }
+  return LLMV_OK;
+}
+
 int llmv_features(const llmv_trace* trace, const llmv_shape* shape, float* x_req,
                   double* x_batch, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_trace(trace, false);

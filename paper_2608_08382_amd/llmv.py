@@ -24,8 +24,9 @@ LLMV_P_MAX = 1 << 20
 LLMV_BATCH_MAX = 1 << 22
 LLMV_TENANTS_MAX = 1 << 24
 
-EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute", "llmv_features",
-           "llmv_tenant_sums", "llmv_validate", "llmv_last_error", "llmv_set_kernel_events")
+EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute",
+           "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
+           "llmv_last_error", "llmv_set_kernel_events")
 
 
 class LlmvError(RuntimeError):
@@ -64,6 +65,7 @@ def load(path: str = LIB_PATH):
             lib.llmv_workspace_size.argtypes = [i64, i64, i32]
             lib.llmv_workspace_size.restype = sz
             lib.llmv_attribute.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
+            lib.llmv_attribute_sweep.argtypes = [P, P, i32, P, i32, i32, P, P, sz, P]
             lib.llmv_features.argtypes = [P, P, P, P, P, sz, P]
             lib.llmv_tenant_sums.argtypes = [P, P, i64, i32, P, P, sz, P]
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
@@ -71,8 +73,8 @@ def load(path: str = LIB_PATH):
             lib.llmv_last_error.restype = ctypes.c_char_p
             lib.llmv_set_kernel_events.argtypes = [P, P]
             lib.llmv_set_kernel_events.restype = ctypes.c_int
-            for f in ("llmv_shape_constants", "llmv_attribute", "llmv_features",
-                      "llmv_tenant_sums", "llmv_validate"):
+            for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
+                      "llmv_features", "llmv_tenant_sums", "llmv_validate"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -156,6 +158,25 @@ def llmv_attribute(trace: DeviceTrace, shape, coeffs, latency=None, regime=None,
                                  _ptr(ws), nbytes, _stream(stream)), "llmv_attribute")
 
 
+def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out, ws=None,
+                         stream=None):
+    """shapes: list of shape dicts (or [None] for the unit shape); coeffs:
+    array-like [n_coeffs, 20]; out: device fp64 [n_shapes, n_coeffs, n_tenants]."""
+    import numpy as np
+    co = np.ascontiguousarray(coeffs, dtype=np.float32).reshape(-1, 20)
+    if shapes == [None] or shapes is None:
+        arr, n_sh = None, 1
+    else:
+        arr = (llmv_shape * len(shapes))(*[make_shape(s) for s in shapes])
+        n_sh = len(shapes)
+    tr = trace.struct(with_tenant=True)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().llmv_attribute_sweep(
+        ctypes.byref(tr), None if arr is None else ctypes.cast(arr, ctypes.c_void_p), n_sh,
+        co.ctypes.data_as(ctypes.c_void_p), co.shape[0], int(n_tenants), _ptr(out), _ptr(ws),
+        nbytes, _stream(stream)), "llmv_attribute_sweep")
+
+
 def llmv_features(trace: DeviceTrace, shape, x_req=None, x_batch=None, ws=None, stream=None):
     sh = make_shape(shape)
     tr = trace.struct(with_tenant=False)
@@ -216,6 +237,19 @@ def attribute(trace: DeviceTrace, shape, coeffs, n_tenants: int = 0,
         ws = workspace(trace.n_batches, trace.n_requests, n_tenants, dev)
     llmv_attribute(trace, shape, coeffs, out.get("latency"), out.get("regime"), out.get("share"),
                    n_tenants, out.get("tenant_sums"), ws)
+    return out
+
+
+def attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, ws=None):
+    """Allocates out [n_shapes, n_coeffs, n_tenants] and runs the sweep."""
+    import numpy as np
+    n_sh = 1 if shapes is None else len(shapes)
+    n_co = int(np.asarray(coeffs).reshape(-1, 20).shape[0])
+    out = torch.empty((n_sh, n_co, n_tenants), dtype=torch.float64, device=trace.p.device)
+    if ws is None:
+        ws = workspace(trace.n_batches, trace.n_requests, n_tenants, trace.p.device)
+    llmv_attribute_sweep(trace, shapes if shapes is not None else [None], coeffs, n_tenants,
+                         out, ws)
     return out
 
 

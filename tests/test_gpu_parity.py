@@ -137,6 +137,8 @@ def random_fill(rng, sizes, n_tenants=5, p_hi=5000, c_hi=200000):
 SIZE_SETS = {
     "wave-edges": [1, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513],
     "tile-edges": [767, 768, 769, 1023, 1024, 1025, 3068, 3069, 3070, 3071, 3072, 3073],
+    "wave-tile-edges": [1531, 1532, 1533, 1534, 1535, 1536, 1537, 1, 2044, 2045, 2046, 2047,
+                        2048, 2049, 2, 1280, 1281, 1279],
     "big": [5000, 1, 2, 3, 100000, 7, 3075],
     "tiny": [1] * 700 + [2] * 300 + [3] * 100,
     "unaligned": [3, 5, 7, 1, 9, 11, 13, 2, 6, 10] * 50,
@@ -387,3 +389,60 @@ def full_size_sampled(L, name, n_sample=1500):
 @pytest.mark.parametrize("name", ["decode-only", "chunked-prefill", "heavy-tailed"])
 def test_full_size_sampled(L, name):
     full_size_sampled(L, name)
+
+
+# ---------------------------------------------------------- what-if sweep
+
+
+def run_sweep(L, tr, shapes, co):
+    import torch
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    out = L.attribute_sweep(dt, shapes, co, tr.n_tenants)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def test_sweep_small(L):
+    tr = tracegen.config_trace("whatif-sweep", 1500)
+    co = tracegen.sweep_coeffs(tracegen.config_coeffs("whatif-sweep"), 5)
+    shapes = [tracegen.SHAPES[k] for k in ("llama3.1-8b", "70b-like")]
+    out = run_sweep(L, tr, shapes, co)
+    assert out.shape == (2, 5, tr.n_tenants)
+    for s, sh in enumerate(shapes):
+        for v in range(5):
+            ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, sh, co[v], tr.n_tenants,
+                                   ("tenant_sums",))["tenant_sums"]
+            e = parity.rel_err(out[s, v], ref)
+            assert e.max() <= parity.RTOL, (s, v, e.max())
+    # the same numbers as single attribution calls
+    import torch
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    one = L.attribute(dt, shapes[1], co[3], tr.n_tenants, ("tenant_sums",))["tenant_sums"]
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(out[1, 3], one.cpu().numpy(), rtol=1e-12)
+
+
+def test_sweep_unit_shape_and_hand_coeffs(L):
+    tt = HAND["tenant_trace"]
+    by = {e["name"]: e for e in HAND["unit_shape_examples"]}
+    tr = tracegen.from_batches([(by[n]["p"], by[n]["c"]) for n in tt["batches"]], tt["tenants"],
+                               tt["n_tenants"])
+    th = coeff_vec(HAND["base_coeffs"])
+    out = run_sweep(L, tr, None, np.stack([th, th]))
+    assert list(out[0, 0]) == tt["tenant_sums"] and list(out[0, 1]) == tt["tenant_sums"]
+
+
+def test_sweep_full_size_sampled(L):
+    tr = tracegen.config_trace("whatif-sweep")
+    co = tracegen.sweep_coeffs(tracegen.config_coeffs("whatif-sweep"), 256)
+    names = ["llama3.1-8b", "qwen2.5-14b", "qwen2.5-32b", "70b-like"]
+    shapes = [tracegen.SHAPES[k] for k in names]
+    say(f"[sweep] N={tr.n_requests} variants={4 * 256}")
+    out = run_sweep(L, tr, shapes, co)
+    assert np.all(np.isfinite(out))
+    for s, v in [(0, 0), (1, 17), (2, 128), (3, 255), (3, 1), (0, 200)]:
+        ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shapes[s], co[v], tr.n_tenants,
+                               ("tenant_sums",))["tenant_sums"]
+        e = parity.rel_err(out[s, v], ref)
+        say(f"[sweep] shape {names[s]} variant {v}: max rel err {e.max():.2e}")
+        assert e.max() <= parity.RTOL

@@ -123,6 +123,17 @@ def test_host_argument_errors(llmv):
     assert lib.llmv_validate(None, 0, None, 0, None) == E
     tr = _trace(llmv)
     assert lib.llmv_validate(ctypes.byref(tr), 0, None, 0, None) == E  # tenant without count
+    # sweep: argument checks
+    co = (ctypes.c_float * 40)(*([1.0] * 40))
+    sw = lib.llmv_attribute_sweep
+    assert sw(ctypes.byref(tr), None, 2, co, 2, 4, FAKE, None, 0, None) == E  # NULL shapes, 2
+    assert sw(ctypes.byref(tr), None, 1, co, 0, 4, FAKE, None, 0, None) == E  # no coeffs
+    assert sw(ctypes.byref(tr), None, 1, None, 2, 4, FAKE, None, 0, None) == E
+    assert sw(ctypes.byref(tr), None, 1, co, 2, 4097, FAKE, None, 0, None) == E  # LDS limit
+    assert sw(ctypes.byref(tr), None, 1, co, 2, 4, None, None, 0, None) == E  # no out
+    co[25] = float("nan")
+    assert sw(ctypes.byref(tr), None, 1, co, 2, 4, FAKE, None, 0, None) == E
+    assert sw(ctypes.byref(_trace(llmv, t=0)), None, 1, co, 2, 4, FAKE, None, 0, None) == E
 
 
 def test_python_binding_refuses_without_library(tmp_path):
