@@ -239,16 +239,19 @@ def main():
             ms = min(hip.elapsed_ms(x, y) for x, y in ev)
             log(f"[bench] breakdown {name}: tile kernel {ms:.4f} ms")
     if args.copy_bytes:
-        src = torch.empty(args.copy_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        # plain device copy of known size (counter calibration): torch.neg
+        # reads copy_bytes and writes copy_bytes in one elementwise kernel
+        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
+        torch.cuda.synchronize()
         ev = [(hip.create(), hip.create()) for _ in range(3)]
         for x, y in ev:
             hip.record(x, stream)
-            dst.copy_(src)
+            torch.neg(src, out=dst)
             hip.record(y, stream)
         torch.cuda.synchronize()
         ms = min(hip.elapsed_ms(x, y) for x, y in ev)
-        log(f"[bench] copy of {args.copy_bytes} bytes: {ms:.4f} ms, "
+        log(f"[bench] copy (neg) of {args.copy_bytes} bytes: {ms:.4f} ms, "
             f"{2 * args.copy_bytes / ms / 1e6:.0f} GB/s read+write")
         del src, dst
 

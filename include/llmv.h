@@ -26,7 +26,9 @@
  * Conventions for every entry point below:
  *   - Pointers marked "device" must point to device memory of the current
  *     HIP device; "host" pointers to host memory.  The caller owns all
- *     memory; the library allocates nothing on these paths.
+ *     memory; the library allocates nothing on these paths.  The per-request
+ *     arrays (p, c, tenant, share) must be 16-byte aligned (any hipMalloc or
+ *     torch allocation is); they are read and written with 16-byte accesses.
  *   - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
  *     on it and the call returns without waiting; outputs are valid once the
  *     stream has reached that point.  llmv_validate is the exception: it
