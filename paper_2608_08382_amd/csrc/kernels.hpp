@@ -214,8 +214,9 @@ __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, int64_t
 // batches (no workgroup barriers inside the loop); the four waves of a
 // workgroup share only the LDS tenant histogram.  A wave tile is a run of
 // whole batches whose requests fit in kTile slots from a 16-byte aligned
-// base.  The tile is held in registers as kRounds rounds of 1024 slots: in
-// round r lane l holds slots 1024r + 16l .. 1024r + 16l + 15.
+// base.  The tile is held in registers as kRounds rounds of 64*kVec slots:
+// in round r lane l holds slots 64*kVec*r + kVec*l .. 64*kVec*r + kVec*l +
+// kVec-1.
 
 constexpr int kRounds = 1;
 constexpr int kRoundSlots = 64 * kVec;
@@ -277,10 +278,10 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
   return x;
 }
 
-// Loads slots x .. x+15 (x a multiple of 4, x >= 0) of p, c (and tenant);
-// slots at or past N read as 0.
+// Loads slots x .. x+kVec-1 (x a multiple of 4, x >= 0) of p, c (and
+// tenant); slots at or past N read as 0.
 template <bool TENANT>
-__device__ __forceinline__ void load16(const Params& P, int64_t x, int32_t* pv, int32_t* cv,
+__device__ __forceinline__ void load_slots(const Params& P, int64_t x, int32_t* pv, int32_t* cv,
                                        int32_t* tv) {
   if (x + kVec <= P.N) {
 #pragma unroll
@@ -305,23 +306,8 @@ __device__ __forceinline__ void load16(const Params& P, int64_t x, int32_t* pv, 
   }
 }
 
-// Loads tenant ids of slots x .. x+kVec-1 (x a multiple of 4); slots at or
-// past N read as 0.
-__device__ __forceinline__ void load_tenants(const Params& P, int64_t x, int32_t* tv) {
-  if (x + kVec <= P.N) {
-#pragma unroll
-    for (int g = 0; g < kVec / 4; ++g) {
-      const v4i t = *(const v4i*)(P.tenant + x + 4 * g);
-      tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < kVec; ++q) tv[q] = x + q < P.N ? P.tenant[x + q] : 0;
-  }
-}
-
 // Writes one round of shares staged lane-major in the wave's LDS (lane l:
-// slots s0 + 16l .. s0 + 16l + 15, pitch kStagePitch) so that every global
+// slots s0 + kVec*l .. s0 + kVec*l + kVec-1, pitch kStagePitch) so that every global
 // store instruction writes 1 KB of consecutive shares.  Only slots in
 // [xf, L) are written.
 __device__ __forceinline__ void store_round(const Params& P, WaveLds& W, int64_t ra, int32_t s0,
@@ -355,7 +341,7 @@ __device__ void big_batch(const Params& P, WaveLds& W, int64_t bg, int64_t rs, i
   int32_t pv[kVec], cv[kVec], tv[kVec];
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
-    load16<false>(P, x, pv, cv, tv);
+    load_slots<false>(P, x, pv, cv, tv);
 #pragma unroll
     for (int q = 0; q < kVec; ++q) {
       if (x + q >= rs && x + q < re) {
@@ -379,7 +365,7 @@ __device__ void big_batch(const Params& P, WaveLds& W, int64_t bg, int64_t rs, i
   const float k[4] = {(float)kd[0], (float)kd[1], (float)kd[2], (float)kd[3]};
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
-    load16<HIST != HIST_NONE>(P, x, pv, cv, tv);
+    load_slots<HIST != HIST_NONE>(P, x, pv, cv, tv);
 #pragma unroll
     for (int g = 0; g < kVec / 4; ++g) {
       float sv[4];
@@ -452,15 +438,15 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
       const bool ne = lane < count && lo_next > lo;  // batch b+lane is nonempty
       const uint64_t ne_ball = __ballot(ne);
 
-      // ---- held requests (tenant ids are loaded per round, when needed)
-      int32_t pv[kRounds][kVec], cv[kRounds][kVec];
+      // ---- held requests
+      int32_t pv[kRounds][kVec], cv[kRounds][kVec], tv[kRounds][kVec];
 #pragma unroll
       for (int r = 0; r < kRounds; ++r) {
         if (r * kRoundSlots + x0 < L) {
-          load16<false>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], nullptr);
+          load_slots<TEN>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], tv[r]);
         } else {
 #pragma unroll
-          for (int q = 0; q < kVec; ++q) pv[r][q] = cv[r][q] = 0;
+          for (int q = 0; q < kVec; ++q) pv[r][q] = cv[r][q] = tv[r][q] = 0;
         }
       }
 
@@ -539,15 +525,6 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
       for (int r = 0; r < kRounds; ++r) {
         if (r * kRoundSlots >= L) break;  // wave-uniform
         const int64_t pos = ra + r * kRoundSlots + x0;
-        int32_t tv[kVec];
-        if (TEN) {
-          if (valid[r]) {
-            load_tenants(P, pos, tv);
-          } else {
-#pragma unroll
-            for (int q = 0; q < kVec; ++q) tv[q] = 0;
-          }
-        }
         uint32_t kcur = 0xffffffffu;
         float kk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         double kd[4] = {0.0, 0.0, 0.0, 0.0};
@@ -566,7 +543,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
                 kk[0] = (float)kd[0]; kk[1] = (float)kd[1]; kk[2] = (float)kd[2]; kk[3] = (float)kd[3];
               }
               sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist,
-                                                      TEN ? tv[q] : 0, pos + q);
+                                                      tv[r][q], pos + q);
             }
           }
           if (MODE == MODE_ATTR && SHARE)
