@@ -89,15 +89,46 @@ int64_t grid_for(int64_t n, int cus, int per_cu) {
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
 
 struct Layout {
-  size_t wg_first, partials, flag, total;
+  size_t wg_first, claims, partials, flag, total;
 };
+
+// Chunks for `workers` wave workers over n requests.  When a worker's share
+// is at least kMinDynShare requests: kStaticEighths/8 of the requests in one
+// static chunk per worker, the rest in up to kDynPerWorker claimed chunks
+// per worker of at least kMinChunk requests.  Otherwise one static chunk per
+// worker and no claims (a claim is a device-wide atomic on one counter;
+// thousands of them cost more than a short launch can win back).
+ChunkMap chunk_map(int64_t n, int64_t workers) {
+  ChunkMap m{};
+  m.n_static = workers;
+  m.s2 = 1;
+  if (n / workers < kMinDynShare) {
+    m.s1 = (n + workers - 1) / workers;
+    if (m.s1 < 1) m.s1 = 1;
+    m.F = m.s1 * workers;
+    m.n_chunks = workers;
+    return m;
+  }
+  m.s1 = n / 8 * kStaticEighths / workers;
+  m.F = m.s1 * workers;
+  const int64_t rest = n - m.F;
+  int64_t dyn = (int64_t)kDynPerWorker * workers;
+  if (dyn > rest / kMinChunk) dyn = rest / kMinChunk;
+  if (dyn < 1) dyn = 1;
+  m.s2 = (rest + dyn - 1) / dyn;
+  if (m.s2 < 1) m.s2 = 1;
+  m.n_chunks = workers + dyn;
+  return m;
+}
 
 // Workspace layout shared by every entry point.
 Layout layout(int64_t grid, int32_t T) {
   Layout L{};
   size_t o = 0;
-  L.wg_first = o;  // first batch of each wave worker
-  o += align_up((size_t)(grid * kWaves + 1) * sizeof(int64_t));
+  L.wg_first = o;  // first batch of each chunk
+  o += align_up((size_t)(grid * kWaves * (1 + kDynPerWorker) + 1) * sizeof(int64_t));
+  L.claims = o;
+  o += align_up(sizeof(unsigned long long));
   L.partials = o;
   if (lds_hist(T)) o += align_up((size_t)grid * (size_t)T * sizeof(double));
   L.flag = o;
@@ -160,6 +191,17 @@ int check_ws(void* ws, size_t ws_bytes, size_t need) {
   return LLMV_OK;
 }
 
+// Chunk table and cleared claim counter for one or more k_tiles launches.
+int partition(const llmv_trace* tr, const ChunkMap& cm, int64_t* wg_first,
+              unsigned long long* claims, hipStream_t stream) {
+  int64_t blocks = (tr->n_batches + 1 + kWG - 1) / kWG;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, stream, tr->offsets,
+                     tr->n_batches, cm, wg_first, claims);
+  HIP_TRY(hipGetLastError(), "k_partition launch");
+  return LLMV_OK;
+}
+
 typedef void (*TileKernel)(const Params);
 
 TileKernel pick_tiles(int mode, int hist, bool share) {
@@ -189,20 +231,19 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   const int n_chunks = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
+  const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves);
   P.wg_first = wg_first;
+  P.claims = (unsigned long long*)(base + L.claims);
+  P.claim_base = 0;
+  P.n_chunks = cm.n_chunks;
   P.partials = hist == HIST_LDS ? (double*)(base + L.partials) : nullptr;
 
-  const int64_t workers = grid * kWaves;
-  const int64_t step = tr->n_requests > 0 ? (tr->n_requests + workers - 1) / workers : 1;
-  {
-    const int64_t work = tr->n_batches + 1;
-    int64_t blocks = (work + kWG - 1) / kWG;
-    if (blocks > 4096) blocks = 4096;
-    double* zero_buf = hist == HIST_GLOBAL ? P.tenant_sums : nullptr;
-    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, stream, tr->offsets,
-                       tr->n_batches, step, (int)workers, wg_first, zero_buf,
-                       (int64_t)(hist == HIST_GLOBAL ? T : 0));
-    HIP_TRY(hipGetLastError(), "k_partition launch");
+  rc = partition(tr, cm, wg_first, P.claims, stream);
+  if (rc) return rc;
+  if (hist == HIST_GLOBAL) {
+    // the atomics path accumulates into the output: clear it first
+    hipLaunchKernelGGL(k_zero_f64, dim3(16), dim3(kWG), 0, stream, P.tenant_sums, (int64_t)T);
+    HIP_TRY(hipGetLastError(), "k_zero_f64 launch");
   }
 
   if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
@@ -305,7 +346,7 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   const size_t dyn = (size_t)n_tenants * sizeof(double);
   const TileKernel kern = pick_tiles(MODE_ATTR, HIST_LDS, false);
   const int64_t grid = grid_for(trace->n_requests, cus, blocks_per_cu(kern, dyn));
-  const int64_t workers = grid * kWaves;
+  const ChunkMap cm = chunk_map(trace->n_requests, grid * kWaves);
   Params P{};
   P.off = trace->offsets;
   P.p = trace->p;
@@ -314,22 +355,21 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   P.nB = trace->n_batches;
   P.N = trace->n_requests;
   P.wg_first = (int64_t*)(base + L.wg_first);
+  P.claims = (unsigned long long*)(base + L.claims);
+  P.n_chunks = cm.n_chunks;
   P.partials = (double*)(base + L.partials);
   P.n_tenants = n_tenants;
-  {
-    const int64_t step = P.N > 0 ? (P.N + workers - 1) / workers : 1;
-    int64_t blocks = (P.nB + 1 + kWG - 1) / kWG;
-    if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(kWG), 0, st, P.off, P.nB, step,
-                       (int)workers, (int64_t*)P.wg_first, (double*)nullptr, (int64_t)0);
-    HIP_TRY(hipGetLastError(), "k_partition launch");
-  }
+  // every launch takes exactly n_chunks claims (one per chunk it runs, the
+  // static ones included), so launch i starts at claim i * n_chunks
+  rc = partition(trace, cm, (int64_t*)P.wg_first, P.claims, st);
+  if (rc) return rc;
   const int n_chunks = (n_tenants + kTenantChunk - 1) / kTenantChunk;
   for (int s = 0; s < n_shapes; ++s) {
     for (int k = 0; k < 4; ++k) P.S[k] = S[s][k];
     for (int v = 0; v < n_coeffs; ++v) {
       for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[(int64_t)v * 20 + i];
       double* dst = out + ((int64_t)s * n_coeffs + v) * n_tenants;
+      P.claim_base = (uint64_t)((int64_t)s * n_coeffs + v) * (uint64_t)cm.n_chunks;
       hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, P);
       HIP_TRY(hipGetLastError(), "k_tiles launch");
       hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)n_chunks), dim3(64 * kReduceWaves), 0, st,
@@ -380,10 +420,8 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
           : grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_GLOBAL>, 0));
   if (!lds) {
     // the atomics path accumulates into the output: clear it first
-    hipLaunchKernelGGL(k_partition, dim3(16), dim3(kWG), 0, s, (const int64_t*)nullptr,
-                       (int64_t)-1, (int64_t)1, 0, (int64_t*)nullptr, tenant_sums,
-                       (int64_t)n_tenants);
-    HIP_TRY(hipGetLastError(), "k_partition launch");
+    hipLaunchKernelGGL(k_zero_f64, dim3(16), dim3(kWG), 0, s, tenant_sums, (int64_t)n_tenants);
+    HIP_TRY(hipGetLastError(), "k_zero_f64 launch");
   }
   if (lds) {
     double* partials = (double*)(base + L.partials);

@@ -7,11 +7,13 @@
 // of the chosen set; tenant usage is the sum of its requests' shares.
 //
 // Work decomposition (memory-bound ragged reduction, no dense contraction):
-//  * k_partition: splits the batch list into one contiguous range per wave
-//    worker, balanced by request count.
+//  * k_partition: splits the batch list into contiguous chunks by request
+//    count: one large chunk per wave worker, taken statically, and many
+//    small ones that workers claim from a counter as they finish (guided
+//    self-scheduling, so no wave waits on a slower one at the end).
 //  * k_tiles: persistent workgroups of four independent wave workers.  A wave
-//    walks its range in wave tiles: runs of whole batches whose requests fit
-//    in kCap slots (lane l holds 16 consecutive requests), so every request is
+//    walks each of its chunks in wave tiles: runs of whole batches whose
+//    requests fit in kCap slots (lane l holds kVec consecutive requests), so every request is
 //    read from HBM once, held in registers while its batch totals are formed,
 //    and its share written once.  Batch totals are lane-local run sums added
 //    into per-batch LDS accumulators; batch membership comes from an LDS
@@ -37,6 +39,30 @@ constexpr int kCap = 64 * kVec;              // request slots per wave tile
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 2048;                   // persistent workgroups, upper bound
 constexpr int kTenantChunk = 64;                 // tenants per k_tenant_reduce block
+#ifndef LLMV_STATIC_EIGHTHS
+#define LLMV_STATIC_EIGHTHS 6
+#endif
+#ifndef LLMV_DYN_PER_WORKER
+#define LLMV_DYN_PER_WORKER 8
+#endif
+constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;  // requests in static chunks, in eighths
+constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave worker, at most
+constexpr int64_t kMinChunk = 4 * kCap;              // requests per claimed chunk, at least
+constexpr int64_t kMinDynShare = 32 * kCap;          // requests per worker for claimed chunks
+
+// Chunks of the tile kernel's work.  Chunk w < n_static (one per wave
+// worker, taken statically) starts at request w*s1; chunk n_static + j
+// (claimed) starts at request F + j*s2, F = n_static*s1.  A chunk holds the
+// batches whose start offset lies in [its start, the next chunk's start).
+struct ChunkMap {
+  int64_t s1, s2, F, n_static, n_chunks;
+  // Number of chunks that start at or before request x (x >= 0).
+  __host__ __device__ int64_t count_le(int64_t x) const {
+    if (x < F) return x / s1 + 1;
+    const int64_t j = (x - F) / s2 + 1, m = n_chunks - n_static;
+    return n_static + (j < m ? j : m);
+  }
+};
 
 enum { MODE_ATTR = 0, MODE_FEAT = 1 };
 
@@ -51,7 +77,10 @@ struct Params {
   const int32_t* c;
   const int32_t* tenant;
   int64_t nB, N;
-  const int64_t* wg_first;  // [grid+1] first batch of each workgroup
+  const int64_t* wg_first;  // [n_chunks+1] first batch of each chunk
+  unsigned long long* claims;  // chunk claim counter
+  uint64_t claim_base;      // counter value when this launch starts
+  int64_t n_chunks;
   float* latency;           // [nB] or null
   uint8_t* regime;          // [nB] or null
   float* share;             // [N] or null
@@ -190,22 +219,26 @@ __device__ __forceinline__ float request_out(const Params& P, const float* k, co
 
 // ------------------------------------------------------------ partition
 
-// wg_first[w] = first batch whose start offset is >= w*step (w < grid),
-// wg_first[grid] = nB.  Also clears zero_buf (the tenant sums of the
-// global-atomics tenant path).
-__global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, int64_t step,
-                            int grid, int64_t* __restrict__ wg_first,
-                            double* __restrict__ zero_buf, int64_t n_zero) {
+// wg_first[w] = first batch whose start offset is >= the start of chunk w
+// (w < n_chunks), wg_first[n_chunks] = nB; clears the claim counter.
+__global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, const ChunkMap cm,
+                            int64_t* __restrict__ wg_first, unsigned long long* claims) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t b = gid; b <= nB; b += stride) {
-    const int64_t wlo = (b == 0) ? 0 : off[b - 1] / step + 1;
-    const int64_t whi = (b == nB) ? (int64_t)grid - 1
-                                  : min((int64_t)grid - 1, off[b] / step);
+    const int64_t wlo = (b == 0) ? 0 : cm.count_le(off[b - 1]);
+    const int64_t whi = (b == nB) ? cm.n_chunks - 1 : min(cm.n_chunks - 1, cm.count_le(off[b]) - 1);
     for (int64_t w = wlo; w <= whi; ++w) wg_first[w] = b;
   }
-  if (gid == 0 && wg_first) wg_first[grid] = nB;
-  for (int64_t i = gid; i < n_zero; i += stride) zero_buf[i] = 0.0;
+  if (gid == 0) {
+    wg_first[cm.n_chunks] = nB;
+    *claims = 0ull;
+  }
+}
+
+__global__ void k_zero_f64(double* __restrict__ x, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) x[i] = 0.0;
 }
 
 // ------------------------------------------------------------ wave tiles
@@ -400,163 +433,173 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P) {
     for (int u = tid; u < P.n_tenants; u += kWG) s_hist[u] = 0.0;
   __syncthreads();
 
-  const int64_t worker = (int64_t)blockIdx.x * kWaves + (tid >> 6);
-  const int64_t bw0 = uni(P.wg_first[worker]);
-  const int64_t bw1 = uni(P.wg_first[worker + 1]);
-  int64_t b = bw0;
-  // offsets window: lane j holds offsets[b + j] for j <= min(kTileBatches, bw1 - b)
-  int64_t wv = (b < bw1 && lane <= min((int64_t)kTileBatches, bw1 - b)) ? P.off[b + lane] : 0;
-  int64_t r0 = uni(readlane_i64(wv, 0));  // first request of batch b
+  // the first chunk of each wave is its static one; later ones are claimed
+  const int64_t workers = (int64_t)gridDim.x * kWaves;
+  int64_t chunk = (int64_t)blockIdx.x * kWaves + (tid >> 6);
+  while (chunk < P.n_chunks) {
+    // claim the next chunk now: the value is first read once this one is done
+    unsigned long long claim = ~0ull;
+    if (P.n_chunks > workers && lane == 0) claim = atomicAdd(P.claims, 1ull);
+    const int64_t bw0 = uni(P.wg_first[chunk]);
+    const int64_t bw1 = uni(P.wg_first[chunk + 1]);
+    int64_t b = bw0;
+    // offsets window: lane j holds offsets[b + j] for j <= min(kTileBatches, bw1 - b)
+    int64_t wv = (b < bw1 && lane <= min((int64_t)kTileBatches, bw1 - b)) ? P.off[b + lane] : 0;
+    int64_t r0 = uni(readlane_i64(wv, 0));  // first request of batch b
 
-  while (b < bw1) {
-    // ---- tile: the longest run of whole batches from b within kTile slots
-    const int64_t lim = min((int64_t)kTileBatches, bw1 - b);
-    const int64_t ra = r0 & ~(int64_t)3;
-    const int64_t rel = wv - ra;
-    const uint64_t fits = __ballot(lane >= 1 && lane <= lim && rel <= kTile);
-    const int32_t count = uni((int32_t)__builtin_popcountll(fits));  // a prefix of lanes
-    const int32_t adv = count > 0 ? count : 1;  // batches consumed by this step
-    const int64_t e = b + adv;
-    const int64_t r1 = uni(readlane_i64(wv, adv));
+    while (b < bw1) {
+      // ---- tile: the longest run of whole batches from b within kTile slots
+      const int64_t lim = min((int64_t)kTileBatches, bw1 - b);
+      const int64_t ra = r0 & ~(int64_t)3;
+      const int64_t rel = wv - ra;
+      const uint64_t fits = __ballot(lane >= 1 && lane <= lim && rel <= kTile);
+      const int32_t count = uni((int32_t)__builtin_popcountll(fits));  // a prefix of lanes
+      const int32_t adv = count > 0 ? count : 1;  // batches consumed by this step
+      const int64_t e = b + adv;
+      const int64_t r1 = uni(readlane_i64(wv, adv));
 
-    // next window: lane j takes offsets[e + j] from lane j + adv, or loads it
-    int64_t nwv;
-    {
-      const int64_t sh = __shfl(wv, min(lane + adv, 63), 64);
-      const bool have = lane + adv <= lim;
-      nwv = have ? sh
-                 : ((e < bw1 && lane <= min((int64_t)kTileBatches, bw1 - e)) ? P.off[e + lane] : 0);
-    }
-
-    if (count == 0) {
-      big_batch<MODE, HIST, SHARE>(P, W, b, r0, r1, s_hist);
-    } else {
-      const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
-      const int32_t lo_next = __shfl_down(lo, 1, 64);
-      const int32_t L = (int32_t)(r1 - ra);
-      const int32_t xf = (int32_t)(r0 - ra);
-      const bool ne = lane < count && lo_next > lo;  // batch b+lane is nonempty
-      const uint64_t ne_ball = __ballot(ne);
-
-      // ---- held requests
-      int32_t pv[kRounds][kVec], cv[kRounds][kVec], tv[kRounds][kVec];
-#pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
-        if (r * kRoundSlots + x0 < L) {
-          load_slots<TEN>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], tv[r]);
-        } else {
-#pragma unroll
-          for (int q = 0; q < kVec; ++q) pv[r][q] = cv[r][q] = tv[r][q] = 0;
-        }
+      // next window: lane j takes offsets[e + j] from lane j + adv, or loads it
+      int64_t nwv;
+      {
+        const int64_t sh = __shfl(wv, min(lane + adv, 63), 64);
+        const bool have = lane + adv <= lim;
+        nwv = have ? sh
+                   : ((e < bw1 && lane <= min((int64_t)kTileBatches, bw1 - e)) ? P.off[e + lane] : 0);
       }
 
-      // ---- batch-start bitmask, accumulators
-      if (lane < kTileMaskWords + 2) W.mask[lane] = 0u;
-      if (lane < count) W.acc[lane] = BatchAcc{0, 0, 0};
-      wave_lds_sync();
-      if (ne) atomicOr(&W.mask[lo >> 5], 1u << (lo & 31));
-      wave_lds_sync();
+      if (count == 0) {
+        big_batch<MODE, HIST, SHARE>(P, W, b, r0, r1, s_hist);
+      } else {
+        const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
+        const int32_t lo_next = __shfl_down(lo, 1, 64);
+        const int32_t L = (int32_t)(r1 - ra);
+        const int32_t xf = (int32_t)(r0 - ra);
+        const bool ne = lane < count && lo_next > lo;  // batch b+lane is nonempty
+        const uint64_t ne_ball = __ballot(ne);
 
-      uint32_t bits[kRounds], ord0[kRounds], valid[kRounds];
-      {
-        uint32_t before = 0;  // starts in earlier rounds
+        // ---- held requests
+        int32_t pv[kRounds][kVec], cv[kRounds][kVec], tv[kRounds][kVec];
 #pragma unroll
         for (int r = 0; r < kRounds; ++r) {
-          const int32_t s = r * kRoundSlots + x0;
-          const uint64_t w2 = ((uint64_t)W.mask[(s >> 5) + 1] << 32) | W.mask[s >> 5];
-          bits[r] = (uint32_t)(w2 >> (s & 31)) & ((1u << kVec) - 1u);
-          const uint32_t h = __builtin_popcount(bits[r]);
-          const uint32_t hs = wave_incl_scan_u32(h);
-          ord0[r] = before + hs - h;  // nonempty batches starting before slot s
-          before += (uint32_t)__builtin_amdgcn_readlane((int)hs, 63);
-          const int32_t a = max(xf - s, 0), z = min(L - s, kVec);
-          valid[r] = z > a ? (((1u << (z - a)) - 1u) << a) & ((1u << kVec) - 1u) : 0u;
-        }
-      }
-
-      // ---- batch sums: lane-local runs, added into the batch accumulators
+          if (r * kRoundSlots + x0 < L) {
+            load_slots<TEN>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], tv[r]);
+          } else {
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
-        // a run ends where a batch starts at the next slot, at the last valid
-        // slot, or at the end of the lane's slots
-        const uint32_t ends =
-            ((bits[r] >> 1) | (1u << (kVec - 1)) | (valid[r] & ~(valid[r] >> 1))) & valid[r];
-        uint32_t rp = 0;
-        uint64_t rcz = 0, rq = 0;
-#pragma unroll
-        for (int q = 0; q < kVec; ++q) {
-          if ((valid[r] >> q) & 1u) {
-            const uint32_t p = (uint32_t)pv[r][q], c = (uint32_t)cv[r][q];
-            rp += p;
-            rcz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
-            rq += (uint64_t)p * p;
-            if ((ends >> q) & 1u) {
-              const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
-              atomicAdd((unsigned long long*)&W.acc[k].p, (unsigned long long)rp);
-              atomicAdd((unsigned long long*)&W.acc[k].cz, (unsigned long long)rcz);
-              atomicAdd((unsigned long long*)&W.acc[k].q, (unsigned long long)rq);
-              rp = 0;
-              rcz = 0;
-              rq = 0;
-            }
+            for (int q = 0; q < kVec; ++q) pv[r][q] = cv[r][q] = tv[r][q] = 0;
           }
         }
-      }
-      wave_lds_sync();
 
-      // ---- per batch (lane j holds batch b+j): the model
-      if (lane < count) {
-        const int64_t bg = b + lane;
-        if (!ne) {
-          empty_batch<MODE>(P, bg);
-        } else {
-          const uint32_t k = __builtin_popcountll(ne_ball & ((1ull << lane) - 1ull));
-          const BatchAcc a = W.acc[k];
-          const int64_t n = (int64_t)lo_next - lo;
-          // decode iff every request processes one token over a nonzero context
-          const bool prefill = (a.p != (uint64_t)n) || ((a.cz >> 48) != 0);
-          batch_model<MODE>(P, bg, n, a.p, a.cz & kCMask, a.q, prefill, W.k[k]);
+        // ---- batch-start bitmask, accumulators
+        if (lane < kTileMaskWords + 2) W.mask[lane] = 0u;
+        if (lane < count) W.acc[lane] = BatchAcc{0, 0, 0};
+        wave_lds_sync();
+        if (ne) atomicOr(&W.mask[lo >> 5], 1u << (lo & 31));
+        wave_lds_sync();
+
+        uint32_t bits[kRounds], ord0[kRounds], valid[kRounds];
+        {
+          uint32_t before = 0;  // starts in earlier rounds
+#pragma unroll
+          for (int r = 0; r < kRounds; ++r) {
+            const int32_t s = r * kRoundSlots + x0;
+            const uint64_t w2 = ((uint64_t)W.mask[(s >> 5) + 1] << 32) | W.mask[s >> 5];
+            bits[r] = (uint32_t)(w2 >> (s & 31)) & ((1u << kVec) - 1u);
+            const uint32_t h = __builtin_popcount(bits[r]);
+            const uint32_t hs = wave_incl_scan_u32(h);
+            ord0[r] = before + hs - h;  // nonempty batches starting before slot s
+            before += (uint32_t)__builtin_amdgcn_readlane((int)hs, 63);
+            const int32_t a = max(xf - s, 0), z = min(L - s, kVec);
+            valid[r] = z > a ? (((1u << (z - a)) - 1u) << a) & ((1u << kVec) - 1u) : 0u;
+          }
         }
-      }
-      wave_lds_sync();
 
-      // ---- per request: share (+ tenant) or features
+        // ---- batch sums: lane-local runs, added into the batch accumulators
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
-        if (r * kRoundSlots >= L) break;  // wave-uniform
-        const int64_t pos = ra + r * kRoundSlots + x0;
-        uint32_t kcur = 0xffffffffu;
-        float kk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        double kd[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int r = 0; r < kRounds; ++r) {
+          // a run ends where a batch starts at the next slot, at the last valid
+          // slot, or at the end of the lane's slots
+          const uint32_t ends =
+              ((bits[r] >> 1) | (1u << (kVec - 1)) | (valid[r] & ~(valid[r] >> 1))) & valid[r];
+          uint32_t rp = 0;
+          uint64_t rcz = 0, rq = 0;
 #pragma unroll
-        for (int g = 0; g < kVec / 4; ++g) {
-          float sv[4];
-#pragma unroll
-          for (int qq = 0; qq < 4; ++qq) {
-            const int q = 4 * g + qq;
-            sv[qq] = 0.0f;
+          for (int q = 0; q < kVec; ++q) {
             if ((valid[r] >> q) & 1u) {
-              const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
-              if (k != kcur) {
-                kcur = k;
-                kd[0] = W.k[k][0]; kd[1] = W.k[k][1]; kd[2] = W.k[k][2]; kd[3] = W.k[k][3];
-                kk[0] = (float)kd[0]; kk[1] = (float)kd[1]; kk[2] = (float)kd[2]; kk[3] = (float)kd[3];
+              const uint32_t p = (uint32_t)pv[r][q], c = (uint32_t)cv[r][q];
+              rp += p;
+              rcz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
+              rq += (uint64_t)p * p;
+              if ((ends >> q) & 1u) {
+                const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
+                atomicAdd((unsigned long long*)&W.acc[k].p, (unsigned long long)rp);
+                atomicAdd((unsigned long long*)&W.acc[k].cz, (unsigned long long)rcz);
+                atomicAdd((unsigned long long*)&W.acc[k].q, (unsigned long long)rq);
+                rp = 0;
+                rcz = 0;
+                rq = 0;
               }
-              sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist,
-                                                      tv[r][q], pos + q);
             }
           }
-          if (MODE == MODE_ATTR && SHARE)
-            *(v4f*)&W.stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
         }
-        if (MODE == MODE_ATTR && SHARE) store_round(P, W, ra, r * kRoundSlots, xf, L);
-      }
-      wave_lds_sync();
-    }
+        wave_lds_sync();
 
-    b = e;
-    r0 = r1;
-    wv = nwv;
+        // ---- per batch (lane j holds batch b+j): the model
+        if (lane < count) {
+          const int64_t bg = b + lane;
+          if (!ne) {
+            empty_batch<MODE>(P, bg);
+          } else {
+            const uint32_t k = __builtin_popcountll(ne_ball & ((1ull << lane) - 1ull));
+            const BatchAcc a = W.acc[k];
+            const int64_t n = (int64_t)lo_next - lo;
+            // decode iff every request processes one token over a nonzero context
+            const bool prefill = (a.p != (uint64_t)n) || ((a.cz >> 48) != 0);
+            batch_model<MODE>(P, bg, n, a.p, a.cz & kCMask, a.q, prefill, W.k[k]);
+          }
+        }
+        wave_lds_sync();
+
+        // ---- per request: share (+ tenant) or features
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) {
+          if (r * kRoundSlots >= L) break;  // wave-uniform
+          const int64_t pos = ra + r * kRoundSlots + x0;
+          uint32_t kcur = 0xffffffffu;
+          float kk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+          double kd[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+          for (int g = 0; g < kVec / 4; ++g) {
+            float sv[4];
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+              const int q = 4 * g + qq;
+              sv[qq] = 0.0f;
+              if ((valid[r] >> q) & 1u) {
+                const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
+                if (k != kcur) {
+                  kcur = k;
+                  kd[0] = W.k[k][0]; kd[1] = W.k[k][1]; kd[2] = W.k[k][2]; kd[3] = W.k[k][3];
+                  kk[0] = (float)kd[0]; kk[1] = (float)kd[1]; kk[2] = (float)kd[2]; kk[3] = (float)kd[3];
+                }
+                sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist,
+                                                        tv[r][q], pos + q);
+              }
+            }
+            if (MODE == MODE_ATTR && SHARE)
+              *(v4f*)&W.stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
+          }
+          if (MODE == MODE_ATTR && SHARE) store_round(P, W, ra, r * kRoundSlots, xf, L);
+        }
+        wave_lds_sync();
+      }
+
+      b = e;
+      r0 = r1;
+      wv = nwv;
+    }
+    // claim k of this launch names chunk workers + k; past the last chunk, stop
+    const uint64_t k = readlane_u64((uint64_t)claim, 0) - P.claim_base;
+    chunk = k < (uint64_t)(P.n_chunks - workers) ? workers + (int64_t)k : P.n_chunks;
   }
 
   if (HIST == HIST_LDS) {

@@ -348,41 +348,51 @@ def test_validate(L):
 
 
 def full_size_sampled(L, name, n_sample=1500):
+    """Latency, regime and tenant sums of every batch against the oracle;
+    shares of sampled batches against it, and of every request by property.
+    Outputs start as NaN (regime 0xEE), so an unwritten one fails."""
     import torch
     tr = tracegen.config_trace(name)
     co = tracegen.config_coeffs(name)
     say(f"[full] {name}: nB={tr.n_batches} N={tr.n_requests}")
     dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
-    out = L.attribute(dt, tr.shape, co, tr.n_tenants)
+    dev = dt.p.device
+    lat_d = torch.full((tr.n_batches,), float("nan"), dtype=torch.float32, device=dev)
+    reg_d = torch.full((tr.n_batches,), 0xEE, dtype=torch.uint8, device=dev)
+    share = torch.full((tr.n_requests,), float("nan"), dtype=torch.float32, device=dev)
+    ts_d = torch.full((tr.n_tenants,), float("nan"), dtype=torch.float64, device=dev)
+    ws = L.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+    L.llmv_attribute(dt, tr.shape, co, lat_d, reg_d, share, tr.n_tenants, ts_d, ws)
     torch.cuda.synchronize()
-    lat = out["latency"].cpu().numpy()
-    reg = out["regime"].cpu().numpy()
-    ts = out["tenant_sums"].cpu().numpy()
+    lat = lat_d.cpu().numpy()
+    reg = reg_d.cpu().numpy()
+    ts = ts_d.cpu().numpy()
+    # every share written; per batch they add up to the latency, so in total too
+    assert not bool(torch.isnan(share).any())
+    share_total = float(share.double().sum())
     rng = np.random.default_rng(99)
     sizes = tr.sizes()
     bids = np.unique(np.concatenate([
         rng.integers(0, tr.n_batches, n_sample), np.arange(5), tr.n_batches - 1 - np.arange(5),
         np.argsort(sizes)[-20:]]))
     # shares of the sampled batches only
-    share = out["share"]
     idx = np.concatenate([np.arange(tr.offsets[b], tr.offsets[b + 1]) for b in bids])
     g_share = np.zeros(tr.n_requests, np.float32)
     g_share[idx] = share[torch.from_numpy(idx).cuda()].cpu().numpy()
-    del out, share, dt
+    del share, dt, ws
     torch.cuda.empty_cache()
     off, p, c, t = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
     ref = oracle.attribute(off, p, c, t, tr.shape, co, tr.n_tenants,
                            ("T", "TM", "TC", "phase", "regime", "share", "share_alt"))
     st = parity.compare(ref, tr.offsets, lat, reg, g_share, None, batch_ids=bids)
-    # tenant sums over the whole trace
-    ref_ts = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co, tr.n_tenants,
-                              ("tenant_sums",))["tenant_sums"]
-    e = parity.rel_err(ts, ref_ts)
-    st["tenant"] = float(e.max())
-    assert st["tenant"] <= parity.RTOL
-    # properties at full size: tenant sums add up to the total latency
+    # every batch and tenant of the whole trace
+    ref_all = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co, tr.n_tenants,
+                               ("T", "TM", "TC", "phase", "regime", "tenant_sums"))
+    st_all = parity.compare(ref_all, tr.offsets, lat, reg, None, ts)
+    st["all_batches"] = st_all
     tot = lat.astype(np.float64).sum()
     assert abs(ts.sum() - tot) / tot <= parity.RTOL
+    assert abs(share_total - tot) / tot <= parity.RTOL
     say(f"[full] {name}: {st}")
 
 
