@@ -103,9 +103,8 @@ typedef struct {
  * constant >= 2^53. */
 int llmv_shape_constants(const llmv_shape *shape, double S[4]);
 
-/* Bytes of device workspace the calls below need for a trace of this size
- * on the current device (0 if none).  Depends on the device's compute-unit
- * count; query it on the device that will run the call. */
+/* Bytes of device workspace every call below needs for a trace of this
+ * size (the what-if sweep's per-workgroup histograms included). */
 size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
 
 /* Batched attribution (Sec. 2 Problem formulation; Sec. 2.1, Eq. 1).
@@ -120,8 +119,10 @@ size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tena
  *   n_tenants number of tenant ids; needed when tenant_sums != NULL.
  *   tenant_sums device [n_tenants] fp64 L_u, or NULL.  Overwritten (not
  *             accumulated); needs trace->tenant.
- * Shares are evaluated in fp64 and rounded once to fp32; tenant sums add the
- * fp64 shares.  Every output is independent of the others being requested. */
+ * Per batch, the model and the share constants are evaluated in fp64 from
+ * exact integer sums; the constants are rounded to fp32 and each share is
+ * evaluated in fp32 (a few ulp); tenant sums add the fp32 shares in fp64.
+ * Every output is independent of the others being requested. */
 int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
                    const float coeffs[20], float *latency, uint8_t *regime,
                    float *share, int32_t n_tenants, double *tenant_sums,
@@ -138,7 +139,9 @@ int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
  *   out      device [n_shapes][n_coeffs][n_tenants] fp64, overwritten:
  *            out[(s*n_coeffs + v)*n_tenants + u] = L_u under (s, v).
  * Equivalent to n_shapes*n_coeffs calls of llmv_attribute with only
- * tenant_sums requested (same results); the batch partition is computed once.
+ * tenant_sums requested (the same shares, summed in another order).  Each
+ * pass over the trace evaluates 8 consecutive variants (4 above 1024 tenants,
+ * 2 above 2048): every tile is loaded and its batch sums formed once per pass.
  * n_tenants must be <= 4096 here.  The workspace is llmv_workspace_size's. */
 int llmv_attribute_sweep(const llmv_trace *trace, const llmv_shape *shapes,
                          int32_t n_shapes, const float *coeffs, int32_t n_coeffs,

@@ -88,8 +88,26 @@ int64_t grid_for(int64_t n, int cus, int per_cu) {
 
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
 
+// Variants per what-if pass for T tenants (T <= kHistLdsMax): 8, 4 or 2
+// fp64 histograms of T + hot-tenant replicas, at most 65 KiB of LDS, so that
+// with the kernel's own LDS two workgroups fit in a CU's 160 KiB.
+constexpr size_t kSweepHistLds = 65 * 1024;
+int sweep_group(int32_t T) {
+  for (int g = kSweepG; g > 1; g /= 2)
+    if ((size_t)g * (size_t)(T + kHotSlots) * sizeof(double) <= kSweepHistLds) return g;
+  return 1;
+}
+static_assert(2 * (kHistLdsMax + kHotSlots) * sizeof(double) <= kSweepHistLds, "sweep LDS");
+
+typedef void (*SweepKernel)(const Params, const VarTable);
+SweepKernel pick_sweep(int g) {
+  if (g >= 8) return k_tiles<MODE_SWEEP, HIST_LDS, false, 8>;
+  if (g >= 4) return k_tiles<MODE_SWEEP, HIST_LDS, false, 4>;
+  return k_tiles<MODE_SWEEP, HIST_LDS, false, 2>;
+}
+
 struct Layout {
-  size_t wg_first, claims, partials, flag, total;
+  size_t wg_first, claims, partials, counts, hot, flag, total;
 };
 
 // Chunks for `workers` wave workers over n requests.  When a worker's share
@@ -129,8 +147,12 @@ Layout layout(int64_t grid, int32_t T) {
   o += align_up((size_t)(grid * kWaves * (1 + kDynPerWorker) + 1) * sizeof(int64_t));
   L.claims = o;
   o += align_up(sizeof(unsigned long long));
-  L.partials = o;
-  if (lds_hist(T)) o += align_up((size_t)grid * (size_t)T * sizeof(double));
+  L.partials = o;  // [grid][variants of a what-if pass][T]
+  if (lds_hist(T)) o += align_up((size_t)grid * (size_t)sweep_group(T) * (size_t)T * sizeof(double));
+  L.counts = o;  // what-if sweep: requests per tenant, and the hot tenants
+  if (lds_hist(T)) o += align_up((size_t)T * sizeof(unsigned long long));
+  L.hot = o;
+  o += align_up(kHot * sizeof(int32_t));
   L.flag = o;
   o += align_up(sizeof(int));
   L.total = o;
@@ -202,15 +224,15 @@ int partition(const llmv_trace* tr, const ChunkMap& cm, int64_t* wg_first,
   return LLMV_OK;
 }
 
-typedef void (*TileKernel)(const Params);
+typedef void (*TileKernel)(const Params, const NoVars);
 
 TileKernel pick_tiles(int mode, int hist, bool share) {
-  if (mode == MODE_FEAT) return k_tiles<MODE_FEAT, HIST_NONE, false>;
+  if (mode == MODE_FEAT) return k_tiles<MODE_FEAT, HIST_NONE, false, 1>;
   if (hist == HIST_NONE)
-    return share ? k_tiles<MODE_ATTR, HIST_NONE, true> : k_tiles<MODE_ATTR, HIST_NONE, false>;
+    return share ? k_tiles<MODE_ATTR, HIST_NONE, true, 1> : k_tiles<MODE_ATTR, HIST_NONE, false, 1>;
   if (hist == HIST_LDS)
-    return share ? k_tiles<MODE_ATTR, HIST_LDS, true> : k_tiles<MODE_ATTR, HIST_LDS, false>;
-  return share ? k_tiles<MODE_ATTR, HIST_GLOBAL, true> : k_tiles<MODE_ATTR, HIST_GLOBAL, false>;
+    return share ? k_tiles<MODE_ATTR, HIST_LDS, true, 1> : k_tiles<MODE_ATTR, HIST_LDS, false, 1>;
+  return share ? k_tiles<MODE_ATTR, HIST_GLOBAL, true, 1> : k_tiles<MODE_ATTR, HIST_GLOBAL, false, 1>;
 }
 
 // Partition + tiles (+ tenant reduction) shared by attribute and features.
@@ -247,7 +269,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   }
 
   if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, stream, P);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, stream, P, NoVars{});
   HIP_TRY(hipGetLastError(), "k_tiles launch");
   if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
 
@@ -343,8 +365,11 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
   char* base = (char*)ws;
-  const size_t dyn = (size_t)n_tenants * sizeof(double);
-  const TileKernel kern = pick_tiles(MODE_ATTR, HIST_LDS, false);
+  // One pass over the trace per group of G consecutive variants (shape-major,
+  // as in out); each pass keeps G tenant histograms in LDS.
+  const int G = sweep_group(n_tenants);
+  const size_t dyn = (size_t)G * (size_t)(n_tenants + kHotSlots) * sizeof(double);
+  const SweepKernel kern = pick_sweep(G);
   const int64_t grid = grid_for(trace->n_requests, cus, blocks_per_cu(kern, dyn));
   const ChunkMap cm = chunk_map(trace->n_requests, grid * kWaves);
   Params P{};
@@ -359,23 +384,48 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   P.n_chunks = cm.n_chunks;
   P.partials = (double*)(base + L.partials);
   P.n_tenants = n_tenants;
+  {
+    // the most frequent tenants get replicated histogram entries
+    unsigned long long* counts = (unsigned long long*)(base + L.counts);
+    int32_t* hot = (int32_t*)(base + L.hot);
+    hipLaunchKernelGGL(k_zero_u64, dim3(16), dim3(kWG), 0, st, counts, (int64_t)n_tenants);
+    HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
+    int64_t blocks = (P.N + (int64_t)kWG * 64 - 1) / ((int64_t)kWG * 64);
+    blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+    hipLaunchKernelGGL(k_tenant_count, dim3((unsigned)blocks), dim3(kWG),
+                       (size_t)n_tenants * sizeof(unsigned int), st, P.tenant, P.N, n_tenants, counts);
+    HIP_TRY(hipGetLastError(), "k_tenant_count launch");
+    hipLaunchKernelGGL(k_hot_tenants, dim3(1), dim3(kWG), 0, st, (const unsigned long long*)counts,
+                       n_tenants, hot);
+    HIP_TRY(hipGetLastError(), "k_hot_tenants launch");
+    P.hot = hot;
+  }
   // every launch takes exactly n_chunks claims (one per chunk it runs, the
   // static ones included), so launch i starts at claim i * n_chunks
   rc = partition(trace, cm, (int64_t*)P.wg_first, P.claims, st);
   if (rc) return rc;
-  const int n_chunks = (n_tenants + kTenantChunk - 1) / kTenantChunk;
-  for (int s = 0; s < n_shapes; ++s) {
-    for (int k = 0; k < 4; ++k) P.S[k] = S[s][k];
-    for (int v = 0; v < n_coeffs; ++v) {
-      for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[(int64_t)v * 20 + i];
-      double* dst = out + ((int64_t)s * n_coeffs + v) * n_tenants;
-      P.claim_base = (uint64_t)((int64_t)s * n_coeffs + v) * (uint64_t)cm.n_chunks;
-      hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, P);
-      HIP_TRY(hipGetLastError(), "k_tiles launch");
-      hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)n_chunks), dim3(64 * kReduceWaves), 0, st,
-                         (const double*)P.partials, (int)grid, (int)n_tenants, dst);
-      HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+  const int64_t n_var = (int64_t)n_shapes * n_coeffs;
+  int64_t launch = 0;
+  for (int64_t v0 = 0; v0 < n_var; v0 += G, ++launch) {
+    VarTable V{};
+    V.n = (int32_t)(n_var - v0 < G ? n_var - v0 : G);
+    for (int g = 0; g < V.n; ++g) {
+      const int64_t v = v0 + g;
+      const int s = (int)(v / n_coeffs);
+      const int64_t j = v % n_coeffs;
+      for (int k = 0; k < 4; ++k) V.S[g][k] = S[s][k];
+      for (int i = 0; i < 20; ++i) V.th[g][i] = (double)coeffs[j * 20 + i];
+      for (int r = 0; r < 4; ++r)
+        for (int k = 1; k < 4; ++k) V.K[g][r][k - 1] = (float)(V.th[g][r * 5 + k] * S[s][k]);
     }
+    P.claim_base = (uint64_t)launch * (uint64_t)cm.n_chunks;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, P, V);
+    HIP_TRY(hipGetLastError(), "k_tiles launch");
+    const int n_hist = V.n * n_tenants;
+    hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)((n_hist + kTenantChunk - 1) / kTenantChunk)),
+                       dim3(64 * kReduceWaves), 0, st, (const double*)P.partials, (int)grid, n_hist,
+                       out + v0 * n_tenants);
+    HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
   }
   return LLMV_OK;
 }

@@ -432,6 +432,46 @@ def test_sweep_small(L):
     np.testing.assert_allclose(out[1, 3], one.cpu().numpy(), rtol=1e-12)
 
 
+def skewed_tenants(rng, N, T, s=1.2):
+    """Tenant ids with Zipf-like skew over T ids, most frequent first (the
+    top ids collect a large share, as in the what-if workload)."""
+    w = 1.0 / np.arange(1, T + 1) ** s
+    return rng.choice(T, N, p=w / w.sum()).astype(np.int32)
+
+
+SWEEP_CASES = {
+    # name: (n_tenants, skewed) -- 1024 tenants run 8 variants per pass,
+    # up to 2048 four, up to 4096 two; 1 and 3 tenants have fewer tenants
+    # than the replicated hot set
+    "T1": (1, False),
+    "T3-skewed": (3, True),
+    "T1024-skewed": (1024, True),
+    "T1025-uniform": (1025, False),
+    "T2049-skewed": (2049, True),
+    "T4096-uniform": (4096, False),
+}
+
+
+@pytest.mark.parametrize("case", sorted(SWEEP_CASES))
+def test_sweep_tenant_counts(L, case):
+    T, skewed = SWEEP_CASES[case]
+    rng = np.random.default_rng(sum(map(ord, case)))
+    sizes = rng.integers(0, 300, 900)
+    sizes[::97] = 2000  # a few batches larger than a wave tile
+    tr = random_fill(rng, sizes, n_tenants=T)
+    if skewed:
+        tr = tracegen.Trace(tr.offsets, tr.p, tr.c, skewed_tenants(rng, tr.n_requests, T), T, None)
+    co = tracegen.sweep_coeffs(tracegen.base_coeffs(77), 11)  # 22 variants: a partial last pass
+    shapes = [tracegen.SHAPES["qwen2.5-14b"], tracegen.SHAPES["llama3.1-8b"]]
+    out = run_sweep(L, tr, shapes, co)
+    for s_ in range(2):
+        for v in range(11):
+            ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shapes[s_], co[v], T,
+                                   ("tenant_sums",))["tenant_sums"]
+            e = parity.rel_err(out[s_, v], ref)
+            assert e.max() <= parity.RTOL, (case, s_, v, e.max())
+
+
 def test_sweep_unit_shape_and_hand_coeffs(L):
     tt = HAND["tenant_trace"]
     by = {e["name"]: e for e in HAND["unit_shape_examples"]}
