@@ -88,6 +88,14 @@ int64_t grid_for(int64_t n, int cus, int per_cu) {
 
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
 
+// Replicas of the attribution path's LDS tenant histogram: 4, 2 or 1, within
+// 32 KiB (two workgroups per CU keep fitting).
+int hist_replicas(int32_t T) {
+  for (int r = 4; r > 1; r /= 2)
+    if ((size_t)r * (size_t)T * sizeof(double) <= 32 * 1024) return r;
+  return 1;
+}
+
 // Variants per what-if pass for T tenants (T <= kHistLdsMax): 8, 4 or 2
 // fp64 histograms of T + hot-tenant replicas, at most 65 KiB of LDS, so that
 // with the kernel's own LDS two workgroups fit in a CU's 160 KiB.
@@ -246,7 +254,8 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
   const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
-  const size_t dyn = hist == HIST_LDS ? (size_t)T * sizeof(double) : 0;
+  const int rep = hist == HIST_LDS ? hist_replicas(T) : 1;
+  const size_t dyn = hist == HIST_LDS ? (size_t)rep * (size_t)T * sizeof(double) : 0;
   const TileKernel kern = pick_tiles(mode, hist, want_share);
   const int64_t grid = grid_for(tr->n_requests, cus, blocks_per_cu(kern, dyn));
   char* base = (char*)ws;
@@ -255,6 +264,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
 
   const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves);
   P.wg_first = wg_first;
+  P.hist_rep = rep;
   P.claims = (unsigned long long*)(base + L.claims);
   P.claim_base = 0;
   P.n_chunks = cm.n_chunks;
@@ -384,6 +394,7 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   P.n_chunks = cm.n_chunks;
   P.partials = (double*)(base + L.partials);
   P.n_tenants = n_tenants;
+  P.hist_rep = 1;
   {
     // the most frequent tenants get replicated histogram entries
     unsigned long long* counts = (unsigned long long*)(base + L.counts);

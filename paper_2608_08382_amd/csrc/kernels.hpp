@@ -93,6 +93,7 @@ struct Params {
   double* x_batch;          // [5][nB] (MODE_FEAT) or null
   const int32_t* hot;       // [kHot] most frequent tenants, -1 for none (MODE_SWEEP)
   int32_t n_tenants;
+  int32_t hist_rep;         // MODE_ATTR, HIST_LDS: histogram replicas (1, 2 or 4)
   double S[4];              // shape constants
   double th[20];            // theta[phase][segment][k]
 };
@@ -520,12 +521,14 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
   wave_lds_sync();
 }
 
-// Entries of the LDS tenant histogram: n_tenants, or in a sweep NV rows of
-// n_tenants + hot-tenant replicas.
+// Entries of the LDS tenant histogram: hist_rep replicas of n_tenants
+// (lane l adds into replica l % hist_rep, so that lanes of one atomic that
+// share a frequent tenant spread over hist_rep entries), or in a sweep NV
+// rows of n_tenants + hot-tenant replicas.
 template <int MODE, int NV>
 __device__ __forceinline__ int32_t hist_len(const Params& P) {
   if constexpr (MODE == MODE_SWEEP) return NV * (P.n_tenants + kHotSlots);
-  else return P.n_tenants;
+  else return P.hist_rep * P.n_tenants;
 }
 
 // NV (MODE_SWEEP): histogram rows, i.e. variants per pass, >= V.n; 1
@@ -555,6 +558,10 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
 
   if (HIST == HIST_LDS)
     for (int u = tid; u < n_hist; u += kWG) s_hist[u] = 0.0;
+  // this lane's replica of the histogram (MODE_ATTR, MODE_FEAT)
+  double* s_hist_lane = s_hist;
+  if constexpr (MODE != MODE_SWEEP)
+    if (HIST == HIST_LDS) s_hist_lane = s_hist + (lane & (P.hist_rep - 1)) * P.n_tenants;
   __syncthreads();
 
   // the first chunk of each wave is its static one; later ones are claimed
@@ -592,7 +599,8 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
       }
 
       if (count == 0) {
-        big_batch<MODE, HIST, SHARE, NV>(P, V, W, stage, b, r0, r1, s_hist);
+        big_batch<MODE, HIST, SHARE, NV>(P, V, W, stage, b, r0, r1,
+                                         MODE == MODE_SWEEP ? s_hist : s_hist_lane);
       } else {
         const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
         const int32_t lo_next = __shfl_down(lo, 1, 64);
@@ -759,7 +767,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
                     kd[0] = W.k[k][0]; kd[1] = W.k[k][1]; kd[2] = W.k[k][2]; kd[3] = W.k[k][3];
                     kk[0] = (float)kd[0]; kk[1] = (float)kd[1]; kk[2] = (float)kd[2]; kk[3] = (float)kd[3];
                   }
-                  sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist,
+                  sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist_lane,
                                                           tv[r][q], pos + q);
                 }
               }
@@ -798,9 +806,15 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
     double* dst = P.partials + (int64_t)blockIdx.x * V.n * T;
     for (int i = tid; i < V.n * T; i += kWG) dst[i] = s_hist[(i / T) * TS + i % T];
   } else if (HIST == HIST_LDS) {
+    // fold the replicas in a fixed order
     __syncthreads();
-    double* dst = P.partials + (int64_t)blockIdx.x * n_hist;
-    for (int u = tid; u < n_hist; u += kWG) dst[u] = s_hist[u];
+    const int32_t T = P.n_tenants;
+    double* dst = P.partials + (int64_t)blockIdx.x * T;
+    for (int u = tid; u < T; u += kWG) {
+      double acc = s_hist[u];
+      for (int r = 1; r < P.hist_rep; ++r) acc += s_hist[r * T + u];
+      dst[u] = acc;
+    }
   }
 }
 

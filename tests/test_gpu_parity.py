@@ -190,10 +190,15 @@ def test_request_count_tails(L, N):
     check(L, tr, None, tracegen.base_coeffs(33), tr.n_tenants, f"N={N}")
 
 
-@pytest.mark.parametrize("n_tenants", [1, 2, 4096, 4097, 100000])
+# 1..1024 tenants: 4 LDS histogram replicas, 2048: 2, 3000 and 4096: 1,
+# above 4096: global atomics
+@pytest.mark.parametrize("n_tenants", [1, 2, 1024, 2048, 3000, 4096, 4097, 100000])
 def test_tenant_counts(L, n_tenants):
     rng = np.random.default_rng(n_tenants)
     tr = random_fill(rng, rng.integers(1, 300, 400), n_tenants=n_tenants)
+    if n_tenants in (1024, 2048):  # skewed, so that lanes of one atomic share tenants
+        tr = tracegen.Trace(tr.offsets, tr.p, tr.c, skewed_tenants(rng, tr.n_requests, n_tenants),
+                            n_tenants, None)
     check(L, tr, tracegen.SHAPES["qwen2.5-32b"], tracegen.base_coeffs(34), n_tenants,
           f"T={n_tenants}")
 
