@@ -133,8 +133,6 @@ ChunkMap chunk_map(int64_t n, int64_t workers) {
     if (m.s1 < 1) m.s1 = 1;
     m.F = m.s1 * workers;
     m.n_chunks = workers;
-    m.inv_s1 = 1.0 / (double)m.s1;
-    m.inv_s2 = 1.0;
     return m;
   }
   m.s1 = n / 8 * kStaticEighths / workers;
@@ -146,8 +144,6 @@ ChunkMap chunk_map(int64_t n, int64_t workers) {
   m.s2 = (rest + dyn - 1) / dyn;
   if (m.s2 < 1) m.s2 = 1;
   m.n_chunks = workers + dyn;
-  m.inv_s1 = 1.0 / (double)m.s1;
-  m.inv_s2 = 1.0 / (double)m.s2;
   return m;
 }
 

@@ -56,25 +56,13 @@ constexpr int64_t kMinDynShare = 32 * kCap;          // requests per worker for 
 // batches whose start offset lies in [its start, the next chunk's start).
 struct ChunkMap {
   int64_t s1, s2, F, n_static, n_chunks;
-  double inv_s1, inv_s2;  // 1/s1, 1/s2
+  // Number of chunks that start at or before request x (x >= 0).
+  __host__ __device__ int64_t count_le(int64_t x) const {
+    if (x < F) return x / s1 + 1;
+    const int64_t j = (x - F) / s2 + 1, m = n_chunks - n_static;
+    return n_static + (j < m ? j : m);
+  }
 };
-
-// floor(x / d) for 0 <= x < 2^53, 0 < d: the fp64 estimate from 1/d is off
-// by less than 2^-51 * x/d (here x/d is at most the chunk count, so by less
-// than one), then corrected exactly in integers.
-__device__ __forceinline__ int64_t div_floor(int64_t x, int64_t d, double inv_d) {
-  int64_t q = (int64_t)((double)x * inv_d);
-  while (q * d > x) --q;
-  while ((q + 1) * d <= x) ++q;
-  return q;
-}
-
-// Number of chunks that start at or before request x (x >= 0).
-__device__ __forceinline__ int64_t chunks_le(const ChunkMap& cm, int64_t x) {
-  if (x < cm.F) return div_floor(x, cm.s1, cm.inv_s1) + 1;
-  const int64_t j = div_floor(x - cm.F, cm.s2, cm.inv_s2) + 1, m = cm.n_chunks - cm.n_static;
-  return cm.n_static + (j < m ? j : m);
-}
 
 // MODE_ATTR: latency, regime, share, tenant sums of one (shape, theta).
 // MODE_FEAT: the feature rows.  MODE_SWEEP: tenant sums of up to kSweepG
@@ -311,21 +299,12 @@ __device__ __forceinline__ float request_out(const Params& P, const float* k, co
 // (w < n_chunks), wg_first[n_chunks] = nB; clears the claim counter.
 __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, const ChunkMap cm,
                             int64_t* __restrict__ wg_first, unsigned long long* claims) {
-  const int lane = threadIdx.x & 63;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;  // a multiple of 64
-  // lanes of a wave take consecutive batches: each start offset is mapped
-  // once, and lane l takes batch b-1's count from lane l-1
-  for (int64_t b = gid; b - lane <= nB; b += stride) {
-    int64_t c = 0;  // chunks that start at or before off[b]
-    if (b < nB) c = chunks_le(cm, off[b]);
-    int64_t cp = __shfl_up(c, 1, 64);
-    if (lane == 0 && b >= 1 && b <= nB) cp = chunks_le(cm, off[b - 1]);
-    if (b <= nB) {
-      const int64_t wlo = (b == 0) ? 0 : cp;
-      const int64_t whi = (b == nB) ? cm.n_chunks - 1 : min(cm.n_chunks - 1, c - 1);
-      for (int64_t w = wlo; w <= whi; ++w) wg_first[w] = b;
-    }
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t b = gid; b <= nB; b += stride) {
+    const int64_t wlo = (b == 0) ? 0 : cm.count_le(off[b - 1]);
+    const int64_t whi = (b == nB) ? cm.n_chunks - 1 : min(cm.n_chunks - 1, cm.count_le(off[b]) - 1);
+    for (int64_t w = wlo; w <= whi; ++w) wg_first[w] = b;
   }
   if (gid == 0) {
     wg_first[cm.n_chunks] = nB;
