@@ -102,8 +102,10 @@ class Oracle:
         lib.orc_attribute.argtypes = [i64, i64, P, P, P, P, P, P, i32,
                                       P, P, P, P, P, P, P, P]
         lib.orc_tenant_sums.argtypes = [P, P, i64, i32, P]
+        lib.orc_batch_sums.argtypes = [i64, i64, P, P, P, P, P]
+        lib.orc_admit.argtypes = [i64, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
         for f in ("orc_shape_constants", "orc_validate", "orc_features",
-                  "orc_attribute", "orc_tenant_sums"):
+                  "orc_attribute", "orc_tenant_sums", "orc_batch_sums", "orc_admit"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
         self.path = so_path
@@ -163,6 +165,37 @@ class Oracle:
         _check(rc, "attribute")
         return out
 
+    def batch_sums(self, offsets, p, c):
+        """Returns (sums [4, nB] int64 = (|B|, sum p, sum c, sum p^2), phase [nB] uint8)."""
+        off = _arr(offsets, np.int64)
+        p, c = _arr(p, np.int32), _arr(c, np.int32)
+        nB, N = len(off) - 1, len(p)
+        sums = np.zeros((4, nB), np.int64)
+        phase = np.zeros(nB, np.uint8)
+        _check(self.lib.orc_batch_sums(nB, N, _ptr(off), _ptr(p), _ptr(c), _ptr(sums),
+                                       _ptr(phase)), "batch_sums")
+        return sums, phase
+
+    def admit(self, p, c, cand_p, cand_c, shape, coeffs) -> dict:
+        """Admission query for the batch of requests (p, c) and one candidate
+        request (cand_p, cand_c): T_after, delta, share, share_alt, TM_after,
+        TC_after, regime."""
+        p, c = _arr(p, np.int32), _arr(c, np.int32)
+        co = _arr(coeffs, np.float32)
+        if co.shape != (20,):
+            raise ValueError("coeffs must hold 20 fp32 values")
+        vals = [ctypes.c_double() for _ in range(6)]
+        reg = ctypes.c_uint8()
+        keep, sp = _shape_ptr(shape)
+        rc = self.lib.orc_admit(len(p), _ptr(p), _ptr(c), int(cand_p), int(cand_c), sp, _ptr(co),
+                                *[ctypes.addressof(v) for v in vals], ctypes.addressof(reg))
+        del keep
+        _check(rc, "admit")
+        names = ("T_after", "delta", "share", "share_alt", "TM_after", "TC_after")
+        out = {k: v.value for k, v in zip(names, vals)}
+        out["regime"] = reg.value
+        return out
+
     def tenant_sums(self, tenant, share, n_tenants) -> np.ndarray:
         t = _arr(tenant, np.int32)
         s = _arr(share, np.float64)
@@ -201,3 +234,11 @@ def attribute(offsets, p, c, tenant, shape, coeffs, n_tenants, outputs=ALL_OUTPU
 
 def tenant_sums(tenant, share, n_tenants):
     return default().tenant_sums(tenant, share, n_tenants)
+
+
+def batch_sums(offsets, p, c):
+    return default().batch_sums(offsets, p, c)
+
+
+def admit(p, c, cand_p, cand_c, shape, coeffs):
+    return default().admit(p, c, cand_p, cand_c, shape, coeffs)

@@ -13,6 +13,8 @@
  */
 #include "orc.h"
 
+#include <stdlib.h>
+
 #include <stddef.h>
 
 /* Largest integer below which every integer is exact in fp64. */
@@ -235,6 +237,67 @@ int orc_attribute(int64_t nB, int64_t N, const int64_t *off, const int32_t *p,
     }
   }
   return ORC_OK;
+}
+
+int orc_batch_sums(int64_t nB, int64_t N, const int64_t *off, const int32_t *p,
+                   const int32_t *c, int64_t *sums, uint8_t *phase) {
+  int rc = orc_validate(nB, N, off, p, c, NULL, 0);
+  if (rc != ORC_OK) return rc;
+  for (int64_t b = 0; b < nB; ++b) {
+    const int64_t n = off[b + 1] - off[b];
+    int64_t P = 0, C = 0, Q = 0;
+    int ph = ORC_REGIME_EMPTY;
+    if (n > 0) batch_sums(off[b], off[b + 1], p, c, &P, &C, &Q, &ph);
+    if (sums) {
+      sums[0 * nB + b] = n;
+      sums[1 * nB + b] = P;
+      sums[2 * nB + b] = C;
+      sums[3 * nB + b] = Q;
+    }
+    if (phase) phase[b] = (uint8_t)ph;
+  }
+  return ORC_OK;
+}
+
+int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
+              const orc_shape *shape, const float coeffs[20], double *T_after,
+              double *delta, double *share, double *share_alt, double *TM_after,
+              double *TC_after, uint8_t *regime) {
+  if (n < 0 || (n > 0 && (!p || !c)) || !coeffs) return ORC_EINVAL;
+  /* B' = B followed by the candidate. */
+  int32_t *p1 = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
+  int32_t *c1 = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
+  double *f1 = (double *)malloc(sizeof(double) * (size_t)(n + 1));
+  double *g1 = (double *)malloc(sizeof(double) * (size_t)(n + 1));
+  if (!p1 || !c1 || !f1 || !g1) {
+    free(p1); free(c1); free(f1); free(g1);
+    return ORC_EINVAL;
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    p1[i] = p[i];
+    c1[i] = c[i];
+  }
+  p1[n] = cp;
+  c1[n] = cc;
+  const int64_t off0[2] = {0, n}, off1[2] = {0, n + 1};
+  double T0 = 0.0, T1 = 0.0, tm1 = 0.0, tc1 = 0.0;
+  uint8_t reg1 = ORC_REGIME_EMPTY;
+  int rc = orc_attribute(1, n, off0, p, c, NULL, shape, coeffs, 0, &T0, NULL, NULL, NULL, NULL,
+                         NULL, NULL, NULL);
+  if (rc == ORC_OK)
+    rc = orc_attribute(1, n + 1, off1, p1, c1, NULL, shape, coeffs, 0, &T1, &tm1, &tc1, NULL,
+                       &reg1, f1, g1, NULL);
+  if (rc == ORC_OK) {
+    if (T_after) *T_after = T1;
+    if (delta) *delta = T1 - T0;
+    if (share) *share = f1[n];
+    if (share_alt) *share_alt = g1[n];
+    if (TM_after) *TM_after = tm1;
+    if (TC_after) *TC_after = tc1;
+    if (regime) *regime = reg1;
+  }
+  free(p1); free(c1); free(f1); free(g1);
+  return rc;
 }
 
 int orc_tenant_sums(const int32_t *tenant, const double *share, int64_t N,

@@ -102,6 +102,30 @@ int orc_attribute(int64_t n_batches, int64_t n_requests, const int64_t *offsets,
                   uint8_t *phase, uint8_t *regime, double *share,
                   double *share_alt, double *tenant_sums);
 
+/* Exact per-batch sums of Eq. 1 and the batch phase (Sec. 2.1):
+ *   sums[4][nB] = (|B|, sum p, sum c, sum p^2), zeros for an empty batch;
+ *   phase[nB]   ORC_PREFILL / ORC_DECODE, 255 for an empty batch.
+ * Both outputs are optional. */
+int orc_batch_sums(int64_t n_batches, int64_t n_requests, const int64_t *offsets,
+                   const int32_t *p, const int32_t *c, int64_t *sums, uint8_t *phase);
+
+/* Admission query (Sec. 1: admission control that rejects or defers a
+ * request whose share would exceed its budget; Sec. 2 Problem formulation).
+ * B is the batch of the n requests (p, c) (n may be 0); B' is B with one more
+ * request, the candidate (cp, cc).  Evaluated as that definition: the
+ * attribution of B' and of B (orc_attribute on each, one batch).
+ *   T_after    f(B')
+ *   delta      f(B') - f(B), f of an empty batch being 0
+ *   share      f(candidate | B'), the candidate's share in B'
+ *   share_alt  the candidate's share under B''s other segment
+ *   TM_after, TC_after  both segment values of B'
+ *   regime     2*phase + segment of B'
+ * Every output is optional. */
+int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
+              const orc_shape *shape, const float coeffs[20], double *T_after,
+              double *delta, double *share, double *share_alt, double *TM_after,
+              double *TC_after, uint8_t *regime);
+
 /* Tenant sums of given shares, in request order:
  * out[u] = sum_{i : tenant[i] == u} share[i].  ORC_ERANGE for a tenant id
  * outside [0, n_tenants). */

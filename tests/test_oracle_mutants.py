@@ -19,6 +19,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "orc.c")
 HAND = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_examples.json")))
 PIN = json.load(open(os.path.join(ROOT, "tests", "golden", "model_shapes.json")))
+ADM = json.load(open(os.path.join(ROOT, "tests", "golden", "admission_examples.json")))
 
 MUTANTS = [
     ("p feature reads c", "x[1] = S[1] * (double)p;", "x[1] = S[1] * (double)c;"),
@@ -47,6 +48,11 @@ MUTANTS = [
     ("tenant sums of other segment", "if (tenant_sums) tenant_sums[tenant[i]] += f;",
      "if (tenant_sums) tenant_sums[tenant[i]] += dot5(th[ph][1 - seg], x);"),
     ("per-request p^2 uses p", "x[3] = S[3] * (double)p2;", "x[3] = S[3] * (double)p;"),
+    ("admission delta sign", "if (delta) *delta = T1 - T0;", "if (delta) *delta = T0 - T1;"),
+    ("admission share of the first request", "if (share) *share = f1[n];",
+     "if (share) *share = f1[0];"),
+    ("admission drops the candidate's context", "c1[n] = cc;", "c1[n] = 0;"),
+    ("admission batch not grown", "off1[2] = {0, n + 1};", "off1[2] = {0, n > 0 ? n : 1};"),
 ]
 
 
@@ -87,6 +93,13 @@ def battery(orc: oracle.Oracle):
         - (2 * sh["n_layers"] + 1) * sh["hidden"]
     assert S[0] == 2 * streamed
     assert S[2] == PIN["llama3_1_8b"]["kv_cache_bytes_per_token_bf16"]
+    # admission queries (hand-worked)
+    for ex in ADM["examples"]:
+        r = orc.admit(ex["p"], ex["c"], ex["cand_p"], ex["cand_c"], None, th)
+        assert r["T_after"] == ex["T_after"] and r["delta"] == ex["delta"]
+        assert r["regime"] == ex["regime"]
+        want = ex["share"] if "share" in ex else ex["share_num"] / ex["share_den"]
+        assert abs(r["share"] - want) <= 4e-16 * want
     # attention FLOPs: p^2 coefficient of the brute-force pair count
     pairs2 = 3  # (q0,k0), (q1,k0), (q1,k1)
     per_pair = sh["n_layers"] * sh["n_q_heads"] * 4 * sh["head_dim"]
