@@ -148,6 +148,39 @@ int llmv_attribute_sweep(const llmv_trace *trace, const llmv_shape *shapes,
                          int32_t n_tenants, double *out, void *ws, size_t ws_bytes,
                          void *stream);
 
+/* Exact per-batch sums of Eq. 1 and the batch phase (Sec. 2.1), the state
+ * an admission query starts from:
+ *   sums    device [4][n_batches] int64, row k at sums[k*n_batches + b]:
+ *           (|B|, sum p, sum c, sum p^2); zeros for an empty batch.
+ *   phase   device [n_batches] uint8 LLMV_PREFILL / LLMV_DECODE (prefill iff
+ *           some request has p > 1 or c = 0), LLMV_REGIME_EMPTY for an empty
+ *           batch.
+ * Either output may be NULL.  Workspace as for llmv_attribute. */
+int llmv_batch_sums(const llmv_trace *trace, int64_t *sums, uint8_t *phase, void *ws,
+                    size_t ws_bytes, void *stream);
+
+/* Admission query (Sec. 1: admission control that rejects or defers a
+ * request whose share would exceed its budget; Sec. 2 Problem formulation;
+ * Eq. 1).  Candidate j, a request (cand_p[j], cand_c[j]), is proposed for
+ * batch cand_batch[j]; B' is that batch with the candidate added.
+ *   sums, phase  device, as written by llmv_batch_sums for n_batches batches.
+ *   shape, coeffs  as for llmv_attribute.
+ *   cand_batch, cand_p, cand_c  device [n_cand]; 1 <= cand_p <= 2^20,
+ *                  cand_c >= 0 (not checked).
+ *   t_after  device [n_cand] fp32 f(B'), or NULL.
+ *   delta    device [n_cand] fp32 f(B') - f(B) (f of an empty batch is 0),
+ *            or NULL.
+ *   share    device [n_cand] fp32 f(candidate | B'), or NULL.
+ *   regime   device [n_cand] uint8 2*phase + segment of B', or NULL.
+ * B' is a prefill batch if B is one or the candidate has p > 1 or c = 0.
+ * Everything is evaluated in fp64 and rounded once.  A candidate whose
+ * batch index is outside [0, n_batches) gets NaN outputs and regime
+ * LLMV_REGIME_EMPTY.  No workspace.  One thread per candidate. */
+int llmv_admit(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
+               const llmv_shape *shape, const float coeffs[20], const int64_t *cand_batch,
+               const int32_t *cand_p, const int32_t *cand_c, int64_t n_cand, float *t_after,
+               float *delta, float *share, uint8_t *regime, void *stream);
+
 /* Request and batch features (Sec. 2.1), structure of arrays:
  *   x_req   device [5][n_requests] fp32, element k of request i at
  *           x_req[k*n_requests + i]: (S0/|B|, S1*p_i, S2*c_i, S3*p_i^2, |B|),

@@ -4,7 +4,7 @@ The computation lives in libllmv.so (HIP kernels for gfx950, C ABI in
 include/llmv.h); ``llmv`` is its ctypes binding.
 """
 from . import llmv  # noqa: F401
-from .llmv import (DeviceTrace, LlmvError, attribute, attribute_sweep, features,  # noqa: F401
-                   llmv_attribute, llmv_attribute_sweep, llmv_features, llmv_last_error,
-                   llmv_shape_constants, llmv_tenant_sums, llmv_validate, llmv_workspace_size,
-                   tenant_sums, workspace)
+from .llmv import (DeviceTrace, LlmvError, admit, attribute, attribute_sweep,  # noqa: F401
+                   batch_sums, features, llmv_admit, llmv_attribute, llmv_attribute_sweep,
+                   llmv_batch_sums, llmv_features, llmv_last_error, llmv_shape_constants,
+                   llmv_tenant_sums, llmv_validate, llmv_workspace_size, tenant_sums, workspace)

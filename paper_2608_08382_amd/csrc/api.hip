@@ -441,6 +441,51 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   return LLMV_OK;
 }
 
+int llmv_batch_sums(const llmv_trace* trace, int64_t* sums, uint8_t* phase, void* ws,
+                    size_t ws_bytes, void* stream) {
+  int rc = check_trace(trace, false);
+  if (rc) return rc;
+  Params P{};
+  rc = shape_constants(nullptr, P.S);
+  if (rc) return rc;
+  P.off = trace->offsets;
+  P.p = trace->p;
+  P.c = trace->c;
+  P.nB = trace->n_batches;
+  P.N = trace->n_requests;
+  P.bsums = sums;
+  P.bphase = phase;
+  if (!sums && !phase) return LLMV_OK;
+  return run_tiles(MODE_FEAT, trace, P, 0, false, false, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int llmv_admit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+               const llmv_shape* shape, const float coeffs[20], const int64_t* cand_batch,
+               const int32_t* cand_p, const int32_t* cand_c, int64_t n_cand, float* t_after,
+               float* delta, float* share, uint8_t* regime, void* stream) {
+  if (n_batches < 0 || n_cand < 0)
+    return fail(LLMV_EINVAL, "negative sizes (n_batches=%lld, n_cand=%lld)",
+                (long long)n_batches, (long long)n_cand);
+  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
+  for (int i = 0; i < 20; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
+  AdmitParams A{};
+  int rc = shape_constants(shape, A.S);
+  if (rc) return rc;
+  for (int i = 0; i < 20; ++i) A.th[i] = (double)coeffs[i];
+  if (n_cand == 0) return LLMV_OK;
+  if (!cand_batch || !cand_p || !cand_c)
+    return fail(LLMV_EINVAL, "candidate arrays must not be NULL");
+  if (n_batches > 0 && (!sums || !phase)) return fail(LLMV_EINVAL, "sums or phase is NULL");
+  const int64_t blocks = (n_cand + kWG - 1) / kWG;
+  if (blocks > 0x7fffffff) return fail(LLMV_EINVAL, "n_cand=%lld too large", (long long)n_cand);
+  hipLaunchKernelGGL(k_admit, dim3((unsigned)blocks), dim3(kWG), 0, (hipStream_t)stream, sums,
+                     phase, n_batches, A, cand_batch, cand_p, cand_c, n_cand, t_after, delta,
+                     share, regime);
+  HIP_TRY(hipGetLastError(), "k_admit launch");
+  return LLMV_OK;
+}
+
 int llmv_features(const llmv_trace* trace, const llmv_shape* shape, float* x_req,
                   double* x_batch, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_trace(trace, false);

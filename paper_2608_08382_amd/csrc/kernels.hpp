@@ -91,6 +91,8 @@ struct Params {
   double* tenant_sums;      // [n_tenants] (HIST_GLOBAL: atomics target)
   float* x_req;             // [5][N] (MODE_FEAT) or null
   double* x_batch;          // [5][nB] (MODE_FEAT) or null
+  int64_t* bsums;           // [4][nB] (|B|, sum p, sum c, sum p^2) (MODE_FEAT) or null
+  uint8_t* bphase;          // [nB] phase, 255 for an empty batch (MODE_FEAT) or null
   const int32_t* hot;       // [kHot] most frequent tenants, -1 for none (MODE_SWEEP)
   int32_t n_tenants;
   int32_t hist_rep;         // MODE_ATTR, HIST_LDS: histogram replicas (1, 2 or 4)
@@ -188,6 +190,13 @@ __device__ __forceinline__ void batch_model(const Params& P, int64_t bg, int64_t
   if (MODE == MODE_FEAT) {
     if (P.x_batch)
       for (int q = 0; q < 5; ++q) P.x_batch[q * P.nB + bg] = X[q];
+    if (P.bsums) {
+      P.bsums[0 * P.nB + bg] = n;
+      P.bsums[1 * P.nB + bg] = (int64_t)Psum;
+      P.bsums[2 * P.nB + bg] = (int64_t)Csum;
+      P.bsums[3 * P.nB + bg] = (int64_t)Qsum;
+    }
+    if (P.bphase) P.bphase[bg] = prefill ? 0 : 1;
     k[0] = P.S[0] / (double)n;
     k[1] = (double)n;
     return;
@@ -262,6 +271,9 @@ __device__ __forceinline__ void empty_batch(const Params& P, int64_t bg) {
   if (MODE == MODE_FEAT) {
     if (P.x_batch)
       for (int q = 0; q < 5; ++q) P.x_batch[q * P.nB + bg] = 0.0;
+    if (P.bsums)
+      for (int q = 0; q < 4; ++q) P.bsums[q * P.nB + bg] = 0;
+    if (P.bphase) P.bphase[bg] = 255;
   } else {
     if (P.latency) P.latency[bg] = 0.0f;
     if (P.regime) P.regime[bg] = 255;
@@ -816,6 +828,75 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
       dst[u] = acc;
     }
   }
+}
+
+// ------------------------------------------------------ admission queries
+
+struct AdmitParams {
+  double S[4];    // shape constants
+  double th[20];  // theta[phase][segment][k]
+};
+
+// One admission query per thread (Sec. 1: admission control): candidate j
+// (p_j, c_j) joins batch b_j, whose exact sums and phase are given.  B' =
+// B + candidate has |B|+1 requests, the sums plus the candidate's terms, and
+// is a prefill batch if B is one or the candidate is prefill-type (p > 1 or
+// c = 0).  Outputs (each optional): f(B'), f(B') - f(B), the candidate's
+// share in B' (its own Eq. 1 terms under B''s segment, fp64, rounded once),
+// and B''s regime.  A batch index outside [0, nB) gives NaN and regime 255.
+__global__ __launch_bounds__(kWG) void k_admit(const int64_t* __restrict__ sums,
+                                               const uint8_t* __restrict__ phase, int64_t nB,
+                                               const AdmitParams A,
+                                               const int64_t* __restrict__ cand_b,
+                                               const int32_t* __restrict__ cand_p,
+                                               const int32_t* __restrict__ cand_c, int64_t m,
+                                               float* __restrict__ t_after,
+                                               float* __restrict__ delta,
+                                               float* __restrict__ share,
+                                               uint8_t* __restrict__ regime) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= m) return;
+  const int64_t b = cand_b[j];
+  if (b < 0 || b >= nB) {
+    const float nan = __builtin_nanf("");
+    if (t_after) t_after[j] = nan;
+    if (delta) delta[j] = nan;
+    if (share) share[j] = nan;
+    if (regime) regime[j] = 255;
+    return;
+  }
+  const int64_t n = sums[b], Ps = sums[nB + b], Cs = sums[2 * nB + b], Qs = sums[3 * nB + b];
+  const int64_t p = cand_p[j], c = cand_c[j];
+  // f(B): 0 for an empty batch
+  double t0 = 0.0;
+  const bool pre0 = n > 0 && phase[b] == 0;
+  if (n > 0) {
+    const double X[5] = {A.S[0], A.S[1] * (double)Ps, A.S[2] * (double)Cs, A.S[3] * (double)Qs,
+                         (double)n * (double)n};
+    const double* thm = A.th + ((pre0 ? 0 : 1) * 2 + 0) * 5;
+    const double* thc = A.th + ((pre0 ? 0 : 1) * 2 + 1) * 5;
+    const double tm = eq1(thm, X), tc = eq1(thc, X);
+    t0 = (tc > tm) ? tc : tm;
+  }
+  // f(B')
+  const int64_t n1 = n + 1;
+  const int ph1 = (pre0 || p > 1 || c == 0) ? 0 : 1;
+  const double X1[5] = {A.S[0], A.S[1] * (double)(Ps + p), A.S[2] * (double)(Cs + c),
+                        A.S[3] * (double)(Qs + p * p), (double)n1 * (double)n1};
+  const double* thm = A.th + (ph1 * 2 + 0) * 5;
+  const double* thc = A.th + (ph1 * 2 + 1) * 5;
+  const double tm = eq1(thm, X1), tc = eq1(thc, X1);
+  // Roofline max of the two segments; ties stay memory-bound.
+  const int seg = (tc > tm) ? 1 : 0;
+  const double t1 = seg ? tc : tm;
+  // the candidate's own terms of Eq. 1 in B'
+  const double x[5] = {A.S[0] / (double)n1, A.S[1] * (double)p, A.S[2] * (double)c,
+                       A.S[3] * (double)(p * p), (double)n1};
+  const double f = eq1(seg ? thc : thm, x);
+  if (t_after) t_after[j] = (float)t1;
+  if (delta) delta[j] = (float)(t1 - t0);
+  if (share) share[j] = (float)f;
+  if (regime) regime[j] = (uint8_t)(2 * ph1 + seg);
 }
 
 // ------------------------------------------------------ hot tenants

@@ -26,7 +26,7 @@ LLMV_TENANTS_MAX = 1 << 24
 
 EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute",
            "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
-           "llmv_last_error", "llmv_set_kernel_events")
+           "llmv_batch_sums", "llmv_admit", "llmv_last_error", "llmv_set_kernel_events")
 
 
 class LlmvError(RuntimeError):
@@ -68,13 +68,16 @@ def load(path: str = LIB_PATH):
             lib.llmv_attribute_sweep.argtypes = [P, P, i32, P, i32, i32, P, P, sz, P]
             lib.llmv_features.argtypes = [P, P, P, P, P, sz, P]
             lib.llmv_tenant_sums.argtypes = [P, P, i64, i32, P, P, sz, P]
+            lib.llmv_batch_sums.argtypes = [P, P, P, P, sz, P]
+            lib.llmv_admit.argtypes = [P, P, i64, P, P, P, P, P, i64, P, P, P, P, P]
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
             lib.llmv_last_error.argtypes = []
             lib.llmv_last_error.restype = ctypes.c_char_p
             lib.llmv_set_kernel_events.argtypes = [P, P]
             lib.llmv_set_kernel_events.restype = ctypes.c_int
             for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
-                      "llmv_features", "llmv_tenant_sums", "llmv_validate"):
+                      "llmv_features", "llmv_tenant_sums", "llmv_validate", "llmv_batch_sums",
+                      "llmv_admit"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -177,6 +180,27 @@ def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out
         nbytes, _stream(stream)), "llmv_attribute_sweep")
 
 
+def llmv_batch_sums(trace: DeviceTrace, sums=None, phase=None, ws=None, stream=None):
+    """sums: device int64 [4, n_batches]; phase: device uint8 [n_batches]."""
+    tr = trace.struct(with_tenant=False)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().llmv_batch_sums(ctypes.byref(tr), _ptr(sums), _ptr(phase), _ptr(ws), nbytes,
+                                  _stream(stream)), "llmv_batch_sums")
+
+
+def llmv_admit(sums, phase, n_batches: int, shape, coeffs, cand_batch, cand_p, cand_c,
+               t_after=None, delta=None, share=None, regime=None, stream=None):
+    """Device tensors: sums int64 [4, n_batches], phase uint8 [n_batches],
+    cand_batch int64 [m], cand_p / cand_c int32 [m]; outputs fp32 / uint8 [m]."""
+    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    sh = make_shape(shape)
+    m = int(cand_p.numel())
+    _check(load().llmv_admit(_ptr(sums), _ptr(phase), int(n_batches), _shape_ref(sh), co,
+                             _ptr(cand_batch), _ptr(cand_p), _ptr(cand_c), m, _ptr(t_after),
+                             _ptr(delta), _ptr(share), _ptr(regime), _stream(stream)),
+           "llmv_admit")
+
+
 def llmv_features(trace: DeviceTrace, shape, x_req=None, x_batch=None, ws=None, stream=None):
     sh = make_shape(shape)
     tr = trace.struct(with_tenant=False)
@@ -268,4 +292,29 @@ def tenant_sums(tenant, share, n_tenants: int, ws=None):
     if ws is None:
         ws = workspace(0, share.numel(), n_tenants, share.device)
     llmv_tenant_sums(tenant, share, n_tenants, out, ws)
+    return out
+
+
+def batch_sums(trace: DeviceTrace, ws=None):
+    """Allocates and returns (sums int64 [4, n_batches], phase uint8 [n_batches])."""
+    dev = trace.p.device
+    sums = torch.empty((4, trace.n_batches), dtype=torch.int64, device=dev)
+    phase = torch.empty(trace.n_batches, dtype=torch.uint8, device=dev)
+    if ws is None:
+        ws = workspace(trace.n_batches, trace.n_requests, 0, dev)
+    llmv_batch_sums(trace, sums, phase, ws)
+    return sums, phase
+
+
+def admit(sums, phase, shape, coeffs, cand_batch, cand_p, cand_c):
+    """Allocates the outputs (t_after, delta, share fp32; regime uint8) and
+    runs llmv_admit; returns them in a dict."""
+    m = int(cand_p.numel())
+    dev = cand_p.device
+    out = {"t_after": torch.empty(m, dtype=torch.float32, device=dev),
+           "delta": torch.empty(m, dtype=torch.float32, device=dev),
+           "share": torch.empty(m, dtype=torch.float32, device=dev),
+           "regime": torch.empty(m, dtype=torch.uint8, device=dev)}
+    llmv_admit(sums, phase, int(phase.numel()), shape, coeffs, cand_batch, cand_p, cand_c,
+               out["t_after"], out["delta"], out["share"], out["regime"])
     return out

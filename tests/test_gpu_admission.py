@@ -1,0 +1,201 @@
+"""GPU parity of llmv_batch_sums and llmv_admit (through the C ABI) against
+the CPU oracle: batch sums bit-exact; admission latency, delta and share
+within parity.RTOL; the regime exact outside the tie zone."""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import tracegen
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HAND = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_examples.json")))
+ADM = json.load(open(os.path.join(ROOT, "tests", "golden", "admission_examples.json")))
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def L():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_08382_amd import llmv
+    llmv.load()
+    torch.cuda.set_device(0)
+    return llmv
+
+
+def base_coeffs():
+    d = HAND["base_coeffs"]
+    return np.array(d["prefill_mem"] + d["prefill_comp"] + d["decode_mem"] + d["decode_comp"],
+                    np.float32)
+
+
+def gpu_sums(L, tr):
+    import torch
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, None)
+    sums, phase = L.batch_sums(dt)
+    torch.cuda.synchronize()
+    return sums, phase
+
+
+def gpu_admit(L, sums, phase, shape, co, cb, cp, cc):
+    import torch
+    dev = sums.device
+    out = L.admit(sums, phase, shape, co, torch.as_tensor(np.asarray(cb, np.int64), device=dev),
+                  torch.as_tensor(np.asarray(cp, np.int32), device=dev),
+                  torch.as_tensor(np.asarray(cc, np.int32), device=dev))
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+@pytest.mark.parametrize("name,nb", [("tiny-mixed", None), ("chunked-prefill", 3000),
+                                     ("heavy-tailed", 5000)])
+def test_batch_sums_exact(L, name, nb):
+    tr = tracegen.config_trace(name, nb)
+    say(f"[admit] batch sums {name}: nB={tr.n_batches}")
+    sums, phase = gpu_sums(L, tr)
+    ref_s, ref_p = oracle.batch_sums(tr.offsets, tr.p, tr.c)
+    assert np.array_equal(sums.cpu().numpy(), ref_s)
+    assert np.array_equal(phase.cpu().numpy(), ref_p)
+
+
+def test_batch_sums_edges(L):
+    """Empty batches, a batch larger than a wave tile, extreme values."""
+    rng = np.random.default_rng(3)
+    sizes = np.array([0, 1, 0, 0, 2000, 3, 0, 70000, 5, 0], np.int64)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    p = np.where(rng.random(N) < 0.5, 1 << 20, 1).astype(np.int32)
+    c = np.where(rng.random(N) < 0.5, (1 << 31) - 1, 1).astype(np.int32)
+    tr = tracegen.Trace(off, p, c, np.zeros(N, np.int32), 1, None)
+    sums, phase = gpu_sums(L, tr)
+    ref_s, ref_p = oracle.batch_sums(off, p, c)
+    assert np.array_equal(sums.cpu().numpy(), ref_s)
+    assert np.array_equal(phase.cpu().numpy(), ref_p)
+
+
+def test_admit_hand_examples(L):
+    exs = ADM["examples"]
+    tr = tracegen.from_batches([(e["p"], e["c"]) for e in exs], [[0] * len(e["p"]) for e in exs], 1)
+    sums, phase = gpu_sums(L, tr)
+    g = gpu_admit(L, sums, phase, None, base_coeffs(), np.arange(len(exs)),
+                  [e["cand_p"] for e in exs], [e["cand_c"] for e in exs])
+    for j, e in enumerate(exs):
+        assert g["t_after"][j] == np.float32(e["T_after"]), e["name"]
+        assert g["delta"][j] == np.float32(e["delta"]), e["name"]
+        want = e["share"] if "share" in e else e["share_num"] / e["share_den"]
+        assert g["share"][j] == np.float32(want), e["name"]
+        assert g["regime"][j] == e["regime"], e["name"]
+
+
+def check_admission(L, tr, shape, co, cb, cp, cc, tag):
+    sums, phase = gpu_sums(L, tr)
+    g = gpu_admit(L, sums, phase, shape, co, cb, cp, cc)
+    worst = {"t_after": 0.0, "delta": 0.0, "share": 0.0}
+    ties = 0
+    for j in range(len(cb)):
+        b = cb[j]
+        lo, hi = tr.offsets[b], tr.offsets[b + 1]
+        r = oracle.admit(tr.p[lo:hi], tr.c[lo:hi], cp[j], cc[j], shape, co)
+        tie = parity.tie_zone(np.array([r["TM_after"]]), np.array([r["TC_after"]]))[0]
+        if tie:  # either segment is right: check against the one the GPU took
+            ties += 1
+            continue
+        assert g["regime"][j] == r["regime"], (tag, j)
+        for k, ref in (("t_after", r["T_after"]), ("delta", r["delta"]), ("share", r["share"])):
+            e = float(parity.rel_err(np.array([g[k][j]], np.float64), np.array([ref]))[0])
+            # a delta that cancels to near zero is judged against the latency it is a
+            # difference of
+            if k == "delta":
+                e = abs(float(g[k][j]) - ref) / max(abs(ref), abs(r["T_after"]), 1e-30)
+            worst[k] = max(worst[k], e)
+    say(f"[admit] {tag}: {len(cb)} candidates, ties {ties}, max rel err {worst}")
+    for k, v in worst.items():
+        assert v <= parity.RTOL, (tag, k, v)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_admit_random(L, seed):
+    rng = np.random.default_rng(200 + seed)
+    names = sorted(tracegen.SHAPES)
+    tr = tracegen.config_trace(["tiny-mixed", "decode-only", "chunked-prefill", "heavy-tailed"][seed],
+                               None if seed == 0 else 1500)
+    # empty batches too
+    sizes = np.diff(tr.offsets)
+    keep = np.ones(len(sizes), bool)
+    m = 3000
+    cb = rng.integers(0, tr.n_batches, m)
+    pre = rng.random(m) < 0.3
+    cp = np.where(pre, rng.integers(1, 8192, m), 1).astype(np.int32)
+    cc = np.where(pre, 0, rng.integers(1, 131072, m)).astype(np.int32)
+    del keep, sizes
+    co = tracegen.config_coeffs(["tiny-mixed", "decode-only", "chunked-prefill", "heavy-tailed"][seed])
+    check_admission(L, tr, tracegen.SHAPES[names[seed]], co, cb, cp, cc, f"seed {seed}")
+
+
+def test_admit_empty_batches_and_unit_shape(L):
+    rng = np.random.default_rng(9)
+    sizes = rng.choice([0, 0, 1, 2, 50], 400)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    tr = tracegen.Trace(off, np.ones(N, np.int32), rng.integers(1, 5000, N).astype(np.int32),
+                        np.zeros(N, np.int32), 1, None)
+    m = 2000
+    cb = rng.integers(0, len(sizes), m)
+    cp = rng.choice([1, 1, 1, 7], m).astype(np.int32)
+    cc = rng.choice([0, 10, 1000], m).astype(np.int32)
+    check_admission(L, tr, None, base_coeffs(), cb, cp, cc, "empty batches, unit shape")
+
+
+def test_admit_batch_index_out_of_range(L):
+    tr = tracegen.config_trace("tiny-mixed")
+    sums, phase = gpu_sums(L, tr)
+    g = gpu_admit(L, sums, phase, None, base_coeffs(), [-1, tr.n_batches, 0],
+                  [1, 1, 1], [10, 10, 10])
+    assert np.isnan(g["t_after"][:2]).all() and np.isnan(g["share"][:2]).all()
+    assert np.isnan(g["delta"][:2]).all() and list(g["regime"][:2]) == [255, 255]
+    assert np.isfinite(g["t_after"][2])
+
+
+def test_admit_full_size_sampled(L):
+    """1M candidates against the 4M batches of the heavy-tailed trace; a
+    sample checked against the oracle."""
+    import torch
+    tr = tracegen.config_trace("heavy-tailed")
+    co = tracegen.config_coeffs("heavy-tailed")
+    rng = np.random.default_rng(77)
+    m = 1 << 20
+    cb = rng.integers(0, tr.n_batches, m)
+    pre = rng.random(m) < 0.2
+    cp = np.where(pre, rng.integers(1, 16384, m), 1).astype(np.int32)
+    cc = np.where(pre, 0, rng.integers(1, 131072, m)).astype(np.int32)
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, None)
+    sums, phase = L.batch_sums(dt)
+    del dt
+    g = gpu_admit(L, sums, phase, tr.shape, co, cb, cp, cc)
+    assert np.isfinite(g["t_after"]).all() and (g["regime"] < 4).all()
+    torch.cuda.empty_cache()
+    idx = rng.choice(m, 1500, replace=False)
+    worst = 0.0
+    for j in idx:
+        b = cb[j]
+        lo, hi = tr.offsets[b], tr.offsets[b + 1]
+        r = oracle.admit(tr.p[lo:hi], tr.c[lo:hi], cp[j], cc[j], tr.shape, co)
+        if parity.tie_zone(np.array([r["TM_after"]]), np.array([r["TC_after"]]))[0]:
+            continue
+        assert g["regime"][j] == r["regime"]
+        for k, ref in (("t_after", r["T_after"]), ("share", r["share"])):
+            worst = max(worst, abs(float(g[k][j]) - ref) / abs(ref))
+        worst = max(worst, abs(float(g["delta"][j]) - r["delta"]) / abs(r["T_after"]))
+    say(f"[admit] full size: max rel err {worst:.2e}")
+    assert worst <= parity.RTOL

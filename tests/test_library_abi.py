@@ -136,6 +136,33 @@ def test_host_argument_errors(llmv):
     assert sw(ctypes.byref(_trace(llmv, t=0)), None, 1, co, 2, 4, FAKE, None, 0, None) == E
 
 
+def test_batch_sums_and_admit_argument_errors(llmv):
+    """Host-side checks only: every call below fails (or returns) before any
+    launch."""
+    lib = llmv.load()
+    E = llmv.LLMV_EINVAL
+    assert lib.llmv_batch_sums(None, FAKE, FAKE, None, 0, None) == E
+    assert lib.llmv_batch_sums(ctypes.byref(_trace(llmv, nB=-1)), FAKE, FAKE, None, 0, None) == E
+    assert lib.llmv_batch_sums(ctypes.byref(_trace(llmv, p=0)), FAKE, FAKE, None, 0, None) == E
+    co = (ctypes.c_float * 20)(*([1.0] * 20))
+    adm = lib.llmv_admit
+    #       sums  phase  nB  shape coeffs  cb    cp    cc    m   outputs x4               stream
+    assert adm(FAKE, FAKE, -1, None, co, FAKE, FAKE, FAKE, 4, None, None, None, None, None) == E
+    assert adm(FAKE, FAKE, 8, None, co, FAKE, FAKE, FAKE, -4, None, None, None, None, None) == E
+    assert adm(FAKE, FAKE, 8, None, None, FAKE, FAKE, FAKE, 4, None, None, None, None, None) == E
+    assert adm(FAKE, FAKE, 8, None, co, None, FAKE, FAKE, 4, None, None, None, None, None) == E
+    assert adm(FAKE, FAKE, 8, None, co, FAKE, FAKE, None, 4, None, None, None, None, None) == E
+    assert adm(None, FAKE, 8, None, co, FAKE, FAKE, FAKE, 4, None, None, None, None, None) == E
+    bad = llmv.llmv_shape(n_layers=0)
+    assert adm(FAKE, FAKE, 8, ctypes.byref(bad), co, FAKE, FAKE, FAKE, 4, None, None, None, None,
+               None) == E
+    co[7] = float("nan")
+    assert adm(FAKE, FAKE, 8, None, co, FAKE, FAKE, FAKE, 4, None, None, None, None, None) == E
+    co[7] = 1.0
+    # no candidates: nothing to do, nothing launched
+    assert adm(None, None, 0, None, co, None, None, None, 0, None, None, None, None, None) == 0
+
+
 def test_python_binding_refuses_without_library(tmp_path):
     from paper_2608_08382_amd import llmv as mod
     saved = mod._lib
