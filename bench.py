@@ -150,6 +150,118 @@ def bench_sweep(hip, stream, with_oracle):
     return res
 
 
+def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
+    """Admission queries on the trace's batches: llmv_batch_sums over every
+    batch, then 2^20 candidate requests (20% prefill-type) in one llmv_admit
+    call; plus the host-side latency of one query and of one single-batch
+    attribution step (median of 50 synchronous calls)."""
+    import numpy as np
+    import torch
+    from paper_2608_08382_amd import llmv
+
+    dev = dt.p.device
+    sums = torch.empty((4, tr.n_batches), dtype=torch.int64, device=dev)
+    phase = torch.empty(tr.n_batches, dtype=torch.uint8, device=dev)
+    rng = np.random.default_rng(11)
+    m = 1 << 20
+    cb_h = rng.integers(0, tr.n_batches, m)
+    pre = rng.random(m) < 0.2
+    cp_h = np.where(pre, rng.integers(1, 16384, m), 1).astype(np.int32)
+    cc_h = np.where(pre, 0, rng.integers(1, 131072, m)).astype(np.int32)
+    cb = torch.as_tensor(cb_h, device=dev)
+    cp = torch.as_tensor(cp_h, device=dev)
+    cc = torch.as_tensor(cc_h, device=dev)
+    out = {k: torch.empty(m, dtype=torch.float32, device=dev) for k in ("t_after", "delta", "share")}
+    out["regime"] = torch.empty(m, dtype=torch.uint8, device=dev)
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        ev = [(hip.create(), hip.create()) for _ in range(reps)]
+        for a, b in ev:
+            hip.record(a, stream)
+            fn()
+            hip.record(b, stream)
+        torch.cuda.synchronize()
+        return sorted(hip.elapsed_ms(a, b) for a, b in ev)[reps // 2]
+
+    ms_sums = timed(lambda: llmv.llmv_batch_sums(dt, sums, phase, ws))
+    ms_admit = timed(lambda: llmv.llmv_admit(sums, phase, tr.n_batches, tr.shape, coeffs, cb, cp,
+                                             cc, out["t_after"], out["delta"], out["share"],
+                                             out["regime"]))
+    # host-side latency of a single query (launch + completion)
+    one = [x[:1] for x in (cb, cp, cc)]
+    lat_q = []
+    for _ in range(50):
+        t0 = time.perf_counter()
+        llmv.llmv_admit(sums, phase, tr.n_batches, tr.shape, coeffs, *one, out["t_after"][:1],
+                        out["delta"][:1], out["share"][:1], out["regime"][:1])
+        torch.cuda.synchronize()
+        lat_q.append(time.perf_counter() - t0)
+    # one scheduler step: attribution of a single 256-request batch
+    st = tracegen_single_batch(256)
+    sdt = llmv.DeviceTrace.from_host(st.offsets, st.p, st.c, st.tenant)
+    s_out = llmv.attribute(sdt, tr.shape, coeffs, st.n_tenants)
+    sws = llmv.workspace(st.n_batches, st.n_requests, st.n_tenants)
+    lat_s = []
+    for _ in range(50):
+        t0 = time.perf_counter()
+        llmv.llmv_attribute(sdt, tr.shape, coeffs, s_out["latency"], s_out["regime"],
+                            s_out["share"], st.n_tenants, s_out["tenant_sums"], sws)
+        torch.cuda.synchronize()
+        lat_s.append(time.perf_counter() - t0)
+    # the same two calls on the GPU's clock (HIP events around each call)
+    gq = timed(lambda: llmv.llmv_admit(sums, phase, tr.n_batches, tr.shape, coeffs, *one,
+                                       out["t_after"][:1], out["delta"][:1], out["share"][:1],
+                                       out["regime"][:1]), reps=21)
+    gs = timed(lambda: llmv.llmv_attribute(sdt, tr.shape, coeffs, s_out["latency"], s_out["regime"],
+                                           s_out["share"], st.n_tenants, s_out["tenant_sums"],
+                                           sws), reps=21)
+    res = {"metric": "admission queries/sec", "value": m / (ms_admit / 1e3), "unit": "queries/s",
+           "n_candidates": m, "admit_ms": ms_admit, "n_batches": tr.n_batches,
+           "batch_sums_ms": ms_sums,
+           "batch_sums_gbps": (8 * tr.n_requests + 41 * tr.n_batches) / (ms_sums / 1e3) / 1e9,
+           "single_query_us": float(np.median(lat_q)) * 1e6,
+           "single_step_256_us": float(np.median(lat_s)) * 1e6,
+           "single_query_gpu_us": gq * 1e3, "single_step_256_gpu_us": gs * 1e3}
+    log(f"[bench] admission: batch sums {ms_sums:.3f} ms, {m} queries in {ms_admit:.3f} ms "
+        f"({res['value']:.3e}/s); one query {res['single_query_us']:.1f} us, one 256-request "
+        f"step {res['single_step_256_us']:.1f} us (host, synchronous); on the GPU's clock "
+        f"{res['single_query_gpu_us']:.1f} and {res['single_step_256_gpu_us']:.1f} us")
+    if with_oracle:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import parity
+        host = {k: v.cpu().numpy() for k, v in out.items()}
+        idx = rng.choice(m, 300, replace=False)
+        worst = 0.0
+        t0 = time.perf_counter()
+        for j in idx:
+            b = cb_h[j]
+            lo, hi = tr.offsets[b], tr.offsets[b + 1]
+            r = oracle.admit(tr.p[lo:hi], tr.c[lo:hi], cp_h[j], cc_h[j], tr.shape, coeffs)
+            if parity.tie_zone(np.array([r["TM_after"]]), np.array([r["TC_after"]]))[0]:
+                continue
+            worst = max(worst, abs(float(host["t_after"][j]) - r["T_after"]) / r["T_after"],
+                        abs(float(host["share"][j]) - r["share"]) / abs(r["share"]))
+        dt_o = time.perf_counter() - t0
+        assert worst <= parity.RTOL, worst
+        res["cpu_baseline"] = {"value": len(idx) / dt_o, "unit": "queries/s", "cores": 1,
+                               "kind": "oracle", "sample": f"{len(idx)} of {m} queries"}
+        res["parity_max_rel_err"] = worst
+    return res
+
+
+def tracegen_single_batch(n):
+    """One decode batch of n requests (context U[128, 8192]), 16 tenants."""
+    import numpy as np
+    import tracegen
+    rng = np.random.default_rng(3)
+    c = rng.integers(128, 8193, n).tolist()
+    t = rng.integers(0, 16, n).tolist()
+    return tracegen.from_batches([([1] * n, c)], [t], 16)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,6 +274,8 @@ def main():
                     help="also time the step with subsets of the outputs (stderr)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the what-if sweep measurement (4 shapes x 256 coefficient vectors)")
+    ap.add_argument("--no-admission", action="store_true",
+                    help="skip the admission-query measurement")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="also run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -290,8 +404,13 @@ def main():
         result["cpu_baseline"] = cb
         result["parity"] = {k: v for k, v in stats.items()}
         log(f"[bench] oracle {cb['value']:.3e} req/s on {cb['cores']} core; parity {stats}")
+    if not args.no_admission:
+        del share
+        torch.cuda.empty_cache()
+        result["admission"] = bench_admission(hip, stream, dt, tr, coeffs, ws,
+                                              not args.no_cpu_baseline)
     if not args.no_sweep:
-        del gpu_out, dt, lat, reg, share, tsum, ws
+        del gpu_out, dt, lat, reg, tsum, ws
         torch.cuda.empty_cache()
         result["whatif_sweep"] = bench_sweep(hip, stream, not args.no_cpu_baseline)
     print(json.dumps(result), flush=True)

@@ -88,6 +88,11 @@ int64_t grid_for(int64_t n, int cus, int per_cu) {
 
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
 
+// Traces up to this many requests run as one workgroup in one launch: two
+// wave tiles per wave at most, so a longer serial walk never costs more than
+// the launches it saves.
+constexpr int64_t kSmallN = 2 * (int64_t)kCap * kWaves;
+
 // Replicas of the attribution path's LDS tenant histogram: 4, 2 or 1, within
 // 32 KiB (two workgroups per CU keep fitting).
 int hist_replicas(int32_t T) {
@@ -257,6 +262,24 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   const int rep = hist == HIST_LDS ? hist_replicas(T) : 1;
   const size_t dyn = hist == HIST_LDS ? (size_t)rep * (size_t)T * sizeof(double) : 0;
   const TileKernel kern = pick_tiles(mode, hist, want_share);
+  P.hist_rep = rep;
+
+  if (tr->n_requests <= kSmallN && hist != HIST_GLOBAL) {
+    // A small trace (one scheduler step, say) in one launch: one workgroup,
+    // its waves split the batches by count (no chunk table), and the
+    // workgroup's tenant histogram is the result (no reduction).
+    P.split_by_count = 1;
+    P.n_chunks = kWaves;
+    P.wg_first = nullptr;
+    P.claims = nullptr;
+    P.partials = hist == HIST_LDS ? P.tenant_sums : nullptr;
+    if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
+    hipLaunchKernelGGL(kern, dim3(1), dim3(kWG), dyn, stream, P, NoVars{});
+    HIP_TRY(hipGetLastError(), "k_tiles launch");
+    if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
+    return LLMV_OK;
+  }
+
   const int64_t grid = grid_for(tr->n_requests, cus, blocks_per_cu(kern, dyn));
   char* base = (char*)ws;
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
@@ -264,7 +287,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
 
   const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves);
   P.wg_first = wg_first;
-  P.hist_rep = rep;
+  P.split_by_count = 0;
   P.claims = (unsigned long long*)(base + L.claims);
   P.claim_base = 0;
   P.n_chunks = cm.n_chunks;

@@ -84,6 +84,8 @@ struct Params {
   unsigned long long* claims;  // chunk claim counter
   uint64_t claim_base;      // counter value when this launch starts
   int64_t n_chunks;
+  int32_t split_by_count;   // one workgroup, no chunk table: wave w takes batches
+                            // [w*nB/4, (w+1)*nB/4) (small traces, one launch)
   float* latency;           // [nB] or null
   uint8_t* regime;          // [nB] or null
   float* share;             // [N] or null
@@ -583,8 +585,8 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
     // claim the next chunk now: the value is first read once this one is done
     unsigned long long claim = ~0ull;
     if (P.n_chunks > workers && lane == 0) claim = atomicAdd(P.claims, 1ull);
-    const int64_t bw0 = uni(P.wg_first[chunk]);
-    const int64_t bw1 = uni(P.wg_first[chunk + 1]);
+    const int64_t bw0 = P.split_by_count ? P.nB * chunk / workers : uni(P.wg_first[chunk]);
+    const int64_t bw1 = P.split_by_count ? P.nB * (chunk + 1) / workers : uni(P.wg_first[chunk + 1]);
     int64_t b = bw0;
     // offsets window: lane j holds offsets[b + j] for j <= min(kTileBatches, bw1 - b)
     int64_t wv = (b < bw1 && lane <= min((int64_t)kTileBatches, bw1 - b)) ? P.off[b + lane] : 0;

@@ -190,6 +190,19 @@ def test_request_count_tails(L, N):
     check(L, tr, None, tracegen.base_coeffs(33), tr.n_tenants, f"N={N}")
 
 
+@pytest.mark.parametrize("N", [1, 12287, 12288, 12289])
+def test_single_launch_boundary(L, N):
+    """Traces of up to 12288 requests run as one workgroup in one launch;
+    one more request takes the partitioned multi-workgroup path."""
+    rng = np.random.default_rng(N)
+    sizes = []
+    while sum(sizes) < N:
+        sizes.append(int(min(rng.integers(0, 400), N - sum(sizes))))
+    tr = random_fill(rng, np.array(sizes), n_tenants=37)
+    assert tr.n_requests == N
+    check(L, tr, tracegen.SHAPES["llama3.1-8b"], tracegen.base_coeffs(61), 37, f"N={N}")
+
+
 # 1..1024 tenants: 4 LDS histogram replicas, 2048: 2, 3000 and 4096: 1,
 # above 4096: global atomics
 @pytest.mark.parametrize("n_tenants", [1, 2, 1024, 2048, 3000, 4096, 4097, 100000])
