@@ -30,7 +30,8 @@ Readings where the paper is silent (each applied in the function below):
   C == 0 for every batch, a2 does.  The remaining coefficients are fitted by
   OLS to y minus the kept terms.  A set with fewer batches than free
   coefficients, or whose free columns have lower rank, keeps all its
-  coefficients.
+  coefficients; the rank is a property of the columns, not of their units,
+  so it is judged (numerically) on the columns scaled to unit norm.
 * F3 r^2 = 1 - sum (y - yhat)^2 / sum (y - mean y)^2 over the nonempty
   batches of the group (0 batches: NaN; all y equal: NaN).
 * F4 Relative error |yhat - y| / y over the nonempty batches with y > 0,
@@ -103,9 +104,15 @@ def fit(offsets, p, c, shape, y, theta0, rounds):
             if counts[g] < len(free):
                 continue
             yf = y[idx] - X[idx][:, kept] @ theta[g * 5 + np.array(kept, int)] if kept else y[idx]
-            sol, _, rank, _ = np.linalg.lstsq(X[idx][:, free], yf, rcond=None)
+            # The rank of the free columns does not depend on their scale,
+            # but a numerical rank on raw columns does (S1*P and |B|^2 differ
+            # by up to 17 orders of magnitude): rank and solution are taken on
+            # unit-norm columns, then unscaled.  Every free column is nonzero.
+            Xf = X[idx][:, free]
+            D = np.linalg.norm(Xf, axis=0)
+            sol, _, rank, _ = np.linalg.lstsq(Xf / D, yf, rcond=None)
             if rank == len(free):
-                new[g * 5 + np.array(free, int)] = sol
+                new[g * 5 + np.array(free, int)] = sol / D
         theta = new
     return theta, counts
 

@@ -81,6 +81,54 @@ def test_chunked_prefill_identifies_every_coefficient():
     assert np.array_equal(theta[10:], theta0[10:])  # no decode batches: kept
 
 
+def model_shape_trace(seed, nb=8000):
+    """10% small prefill batches (1-3 requests, p < 40: memory-bound under
+    the heavy-tailed workload's coefficients), 60% large ones (up to 63
+    requests, p < 4096), 30% decode batches (up to 255 requests,
+    c < 32768); Llama3.1-8B shape.  The compute-bound prefill set then has
+    thousands of batches whose raw columns span ~1e12."""
+    rng = np.random.default_rng(seed)
+    batches = []
+    for _ in range(nb):
+        u = rng.random()
+        if u < 0.1:
+            n = int(rng.integers(1, 4))
+            batches.append((rng.integers(2, 40, n).tolist(), [0] * n))
+        elif u < 0.7:
+            n = int(rng.integers(1, 64))
+            batches.append((rng.integers(2, 4096, n).tolist(), [0] * n))
+        else:
+            n = int(rng.integers(1, 256))
+            batches.append(([1] * n, rng.integers(1, 32768, n).tolist()))
+    tr = tracegen.from_batches(batches, None, 1)
+    tr.shape = tracegen.SHAPES["llama3.1-8b"]
+    return tr
+
+
+def test_planted_recovery_model_shape():
+    """Planted recovery under a real model shape (Llama3.1-8B constants):
+    the raw feature columns then differ by many orders of magnitude (S1*P
+    up to ~1e15, |B|^2 ~ 1), which must not make a well-determined set
+    (condition number ~60 on unit-norm columns) look rank deficient (F2)."""
+    tr = model_shape_trace(12)
+    co = tracegen.config_coeffs("heavy-tailed")
+    T = oracle.attribute(tr.offsets, tr.p, tr.c, None, tr.shape, co, 0, ("T", "regime"))
+    counts_true = np.bincount(T["regime"][T["regime"] != 255], minlength=4)
+    assert (counts_true >= 100).all(), counts_true
+    truth = co.astype(np.float64)
+    theta0 = truth * np.random.default_rng(6).uniform(0.9, 1.1, 20)
+    theta, counts = F.fit(tr.offsets, tr.p, tr.c, tr.shape, T["T"], theta0, rounds=6)
+    assert np.array_equal(counts, counts_true)
+    want = truth.copy()
+    for g in (0, 1):  # prefill: C == 0 everywhere, a2 keeps its start
+        want[g * 5 + 2] = theta0[g * 5 + 2]
+    S = oracle.shape_constants(tr.shape)
+    for g in (2, 3):  # decode: Q == P, a3 keeps its start, a1 absorbs (a3 - a3_0) S3/S1
+        want[g * 5 + 3] = theta0[g * 5 + 3]
+        want[g * 5 + 1] = truth[g * 5 + 1] + (truth[g * 5 + 3] - theta0[g * 5 + 3]) * S[3] / S[1]
+    assert np.max(np.abs(theta - want) / np.abs(want)) < 1e-6, np.abs(theta - want) / np.abs(want)
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_ols_normal_equations_hold(seed):
     """With noise, each set's solution makes the residuals orthogonal to its

@@ -24,6 +24,7 @@ MUTANTS = [
     ("kept terms not subtracted",
      "yf = y[idx] - X[idx][:, kept] @ theta[g * 5 + np.array(kept, int)] if kept else y[idx]",
      "yf = y[idx]"),
+    ("rank judged on raw columns", "D = np.linalg.norm(Xf, axis=0)", "D = np.ones(Xf.shape[1])"),
 ]
 
 
@@ -40,6 +41,7 @@ def battery(F):
         pins.F = F
         pins.test_planted_coefficients_recovered()
         pins.test_chunked_prefill_identifies_every_coefficient()
+        pins.test_planted_recovery_model_shape()
         for seed in range(2):
             pins.test_ols_normal_equations_hold(seed)
         pins.test_small_set_keeps_its_coefficients()
