@@ -252,6 +252,71 @@ def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
     return res
 
 
+def bench_fit(hip, stream, dt, tr, lat, with_oracle):
+    """Fitting and accuracy metrics on the trace's batches: llmv_batch_sums,
+    then llmv_fit (4 rounds) and llmv_fit_metrics against synthetic measured
+    latencies, the model's latency times exp(0.05 Z)."""
+    import numpy as np
+    import torch
+    import tracegen
+    from paper_2608_08382_amd import llmv
+
+    dev = dt.p.device
+    sums, phase = llmv.batch_sums(dt)
+    z = torch.as_tensor(tracegen.normal(10, 21, 0, tr.n_batches), device=dev)
+    y = lat.double() * torch.exp(0.05 * z)
+    del z
+    theta0 = tracegen.perturbed_coeffs(tracegen.config_coeffs(tr.name), 80).astype(np.float64)
+    theta = torch.empty(20, dtype=torch.float64, device=dev)
+    counts = torch.empty(4, dtype=torch.int64, device=dev)
+    out = torch.empty((3, 4), dtype=torch.float64, device=dev)
+    err = torch.empty(tr.n_batches, dtype=torch.float32, device=dev)
+    fws = llmv.fit_workspace(tr.n_batches, dev)
+    rounds = 4
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        ev = [(hip.create(), hip.create()) for _ in range(reps)]
+        for a, b in ev:
+            hip.record(a, stream)
+            fn()
+            hip.record(b, stream)
+        torch.cuda.synchronize()
+        return sorted(hip.elapsed_ms(a, b) for a, b in ev)[reps // 2]
+
+    ms_fit = timed(lambda: llmv.llmv_fit(sums, phase, tr.shape, y, theta0, rounds, theta, counts,
+                                         fws))
+    fitted = theta.cpu().numpy().astype(np.float32)
+    ms_met = timed(lambda: llmv.llmv_fit_metrics(sums, phase, tr.shape, fitted, y, out, err, fws))
+    o = out.cpu().numpy()
+    # bytes a round must move per batch: the four sums, the phase and y
+    round_bytes = 41 * tr.n_batches
+    res = {"metric": "fitting rounds/sec", "value": rounds / (ms_fit / 1e3), "unit": "rounds/s",
+           "n_batches": tr.n_batches, "rounds": rounds, "fit_ms": ms_fit,
+           "round_ms": ms_fit / rounds,
+           "round_gbps": round_bytes / (ms_fit / rounds / 1e3) / 1e9,
+           "metrics_ms": ms_met, "counts": counts.cpu().tolist(),
+           "r2": {"prefill": o[0, 0], "decode": o[1, 0], "all": o[2, 0]},
+           "p90": {"prefill": o[0, 1], "decode": o[1, 1], "all": o[2, 1]},
+           "p99": {"prefill": o[0, 2], "decode": o[1, 2], "all": o[2, 2]}}
+    log(f"[bench] fit: {rounds} rounds over {tr.n_batches} batches in {ms_fit:.3f} ms "
+        f"({res['round_gbps']:.0f} GB/s per round); metrics {ms_met:.3f} ms; r2 {res['r2']}")
+    if with_oracle:
+        from oracle import fit as F
+        nb = 200_000
+        n = int(tr.offsets[nb])
+        y_h = y[:nb].cpu().numpy()
+        t0 = time.perf_counter()
+        F.fit(tr.offsets[:nb + 1], tr.p[:n], tr.c[:n], tr.shape, y_h, theta0, rounds=1)
+        dt_o = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": 1.0 / dt_o * nb / tr.n_batches, "unit": "rounds/s",
+                               "cores": 1, "kind": "oracle",
+                               "sample": f"one round over the first {nb} batches, scaled to "
+                                         f"{tr.n_batches}"}
+    return res
+
+
 def tracegen_single_batch(n):
     """One decode batch of n requests (context U[128, 8192]), 16 tenants."""
     import numpy as np
@@ -274,6 +339,8 @@ def main():
                     help="also time the step with subsets of the outputs (stderr)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the what-if sweep measurement (4 shapes x 256 coefficient vectors)")
+    ap.add_argument("--no-fit", action="store_true",
+                    help="skip the fitting and metrics measurement")
     ap.add_argument("--no-admission", action="store_true",
                     help="skip the admission-query measurement")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -409,6 +476,9 @@ def main():
         torch.cuda.empty_cache()
         result["admission"] = bench_admission(hip, stream, dt, tr, coeffs, ws,
                                               not args.no_cpu_baseline)
+    if not args.no_fit:
+        result["fit"] = bench_fit(hip, stream, dt, tr, lat, not args.no_cpu_baseline)
+        torch.cuda.empty_cache()
     if not args.no_sweep:
         del gpu_out, dt, lat, reg, tsum, ws
         torch.cuda.empty_cache()

@@ -181,6 +181,70 @@ int llmv_admit(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
                const int32_t *cand_p, const int32_t *cand_c, int64_t n_cand, float *t_after,
                float *delta, float *share, uint8_t *regime, void *stream);
 
+/* Fitting Eq. 1 (Sec. 2.1: the coefficients are fitted by ordinary least
+ * squares on profiled batch latencies, one set per phase and segment) and
+ * the accuracy metrics (Sec. 3 and Appendix A: r^2 and the 90th / 99th
+ * percentile of the relative error).  Both start from the batch state that
+ * llmv_batch_sums writes, plus a measured latency per batch:
+ *   sums, phase  device, as written by llmv_batch_sums for n_batches
+ *                batches (n_batches <= 2^31).
+ *   y            device [n_batches] fp64 measured latency (ignored for
+ *                empty batches).
+ * Readings of points the paper leaves open:
+ *   - segment membership: fitting runs in rounds; a round assigns every
+ *     nonempty batch to the segment whose prediction under the current
+ *     coefficients is larger (ties to MEM), then refits each set;
+ *   - identifiability: when every batch of a set has sum p^2 == sum p (all
+ *     decode requests process one token), a3 keeps its current value; when
+ *     every batch has sum c == 0, a2 does; the other coefficients are fitted
+ *     to y minus the kept terms.  A set with fewer batches than free
+ *     coefficients, or with (numerically) dependent free columns, keeps all
+ *     of its coefficients;
+ *   - r^2 = 1 - SSE / sum (y - mean y)^2 over a group's nonempty batches;
+ *   - relative error |f(B) - y| / y over nonempty batches with y > 0,
+ *     rounded to fp32; the p-th percentile of m errors is the
+ *     ceil(p*m)-th smallest (nearest rank, exact integer ranks).
+ * `ws` is a device workspace of llmv_fit_workspace_size(n_batches) bytes
+ * (256-byte aligned, clobbered).  Results are written to device memory on
+ * `stream`; nothing waits. */
+size_t llmv_fit_workspace_size(int64_t n_batches);
+
+/* Ordinary least squares for the four coefficient sets:
+ *   shape    host, or NULL for the unit shape (as for llmv_attribute).
+ *   theta0   host [20] finite fp64, the starting coefficients (layout of
+ *            llmv_attribute's coeffs); they decide the first round's segment
+ *            membership and the values of coefficients a set cannot fit.
+ *   rounds   0..1024 rounds of (assign, refit); 0 copies theta0.
+ *   theta    device [20] fp64 out: the fitted coefficients.
+ *   counts   device [4] int64 out: batches of each (phase, segment) set in
+ *            the last round (zeros for rounds == 0), or NULL.
+ * Each round forms every set's normal equations (X^T X, X^T y over the
+ * batch features of Eq. 1: S0, S1*sum p, S2*sum c, S3*sum p^2, |B|^2) in
+ * fp64 and solves them by a Cholesky factorisation after scaling each
+ * column to unit diagonal; the batch sums are added in a fixed order, so the
+ * result does not depend on scheduling.  Coefficients are not constrained
+ * to be nonnegative. */
+int llmv_fit(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
+             const llmv_shape *shape, const double *y, const double theta0[20],
+             int32_t rounds, double *theta, int64_t *counts, void *ws, size_t ws_bytes,
+             void *stream);
+
+/* Accuracy of fp32 coefficients (the model every other entry point
+ * evaluates) against measured latencies:
+ *   coeffs   host [20] finite fp32.
+ *   rel_err  device [n_batches] fp32 out: the relative error of each batch,
+ *            NaN for an empty batch or y <= 0; or NULL.
+ *   out      device [12] fp64 out: for g = prefill, decode, all,
+ *            out[4g .. 4g+3] = (r^2, p90, p99, nonempty batches); r^2 is NaN
+ *            without batches or with all y equal, a percentile NaN without
+ *            errors.
+ * Predictions are Eq. 1 in fp64 with the segment max; percentiles are exact
+ * (a radix select over the fp32 errors), r^2 takes two passes (mean, then
+ * the sums of squares) with fixed-order sums. */
+int llmv_fit_metrics(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
+                     const llmv_shape *shape, const float coeffs[20], const double *y,
+                     float *rel_err, double *out, void *ws, size_t ws_bytes, void *stream);
+
 /* Request and batch features (Sec. 2.1), structure of arrays:
  *   x_req   device [5][n_requests] fp32, element k of request i at
  *           x_req[k*n_requests + i]: (S0/|B|, S1*p_i, S2*c_i, S3*p_i^2, |B|),

@@ -26,7 +26,8 @@ LLMV_TENANTS_MAX = 1 << 24
 
 EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute",
            "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
-           "llmv_batch_sums", "llmv_admit", "llmv_last_error", "llmv_set_kernel_events")
+           "llmv_batch_sums", "llmv_admit", "llmv_fit_workspace_size", "llmv_fit",
+           "llmv_fit_metrics", "llmv_last_error", "llmv_set_kernel_events")
 
 
 class LlmvError(RuntimeError):
@@ -71,13 +72,17 @@ def load(path: str = LIB_PATH):
             lib.llmv_batch_sums.argtypes = [P, P, P, P, sz, P]
             lib.llmv_admit.argtypes = [P, P, i64, P, P, P, P, P, i64, P, P, P, P, P]
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
+            lib.llmv_fit_workspace_size.argtypes = [i64]
+            lib.llmv_fit_workspace_size.restype = sz
+            lib.llmv_fit.argtypes = [P, P, i64, P, P, P, i32, P, P, P, sz, P]
+            lib.llmv_fit_metrics.argtypes = [P, P, i64, P, P, P, P, P, P, sz, P]
             lib.llmv_last_error.argtypes = []
             lib.llmv_last_error.restype = ctypes.c_char_p
             lib.llmv_set_kernel_events.argtypes = [P, P]
             lib.llmv_set_kernel_events.restype = ctypes.c_int
             for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
                       "llmv_features", "llmv_tenant_sums", "llmv_validate", "llmv_batch_sums",
-                      "llmv_admit"):
+                      "llmv_admit", "llmv_fit", "llmv_fit_metrics"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -201,6 +206,39 @@ def llmv_admit(sums, phase, n_batches: int, shape, coeffs, cand_batch, cand_p, c
            "llmv_admit")
 
 
+def llmv_fit_workspace_size(n_batches: int) -> int:
+    return int(load().llmv_fit_workspace_size(int(n_batches)))
+
+
+def llmv_fit(sums, phase, shape, y, theta0, rounds: int, theta, counts=None, ws=None,
+             stream=None):
+    """Device tensors: sums int64 [4, n_batches], phase uint8 [n_batches],
+    y fp64 [n_batches]; outputs theta fp64 [20], counts int64 [4] (or None).
+    theta0: 20 host numbers."""
+    n = int(phase.numel())
+    th0 = (ctypes.c_double * 20)(*[float(v) for v in theta0])
+    sh = make_shape(shape)
+    if ws is None:
+        ws = fit_workspace(n, theta.device)
+    _check(load().llmv_fit(_ptr(sums), _ptr(phase), n, _shape_ref(sh), _ptr(y), th0, int(rounds),
+                           _ptr(theta), _ptr(counts), _ptr(ws), ws.numel(), _stream(stream)),
+           "llmv_fit")
+
+
+def llmv_fit_metrics(sums, phase, shape, coeffs, y, out, rel_err=None, ws=None, stream=None):
+    """Device tensors as for llmv_fit; out fp64 [3, 4] (prefill, decode, all)
+    x (r2, p90, p99, batches); rel_err fp32 [n_batches] or None."""
+    n = int(phase.numel())
+    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    sh = make_shape(shape)
+    if ws is None:
+        ws = fit_workspace(n, out.device)
+    _check(load().llmv_fit_metrics(_ptr(sums), _ptr(phase), n, _shape_ref(sh), co, _ptr(y),
+                                   _ptr(rel_err), _ptr(out), _ptr(ws), ws.numel(),
+                                   _stream(stream)),
+           "llmv_fit_metrics")
+
+
 def llmv_features(trace: DeviceTrace, shape, x_req=None, x_batch=None, ws=None, stream=None):
     sh = make_shape(shape)
     tr = trace.struct(with_tenant=False)
@@ -318,3 +356,38 @@ def admit(sums, phase, shape, coeffs, cand_batch, cand_p, cand_c):
     llmv_admit(sums, phase, int(phase.numel()), shape, coeffs, cand_batch, cand_p, cand_c,
                out["t_after"], out["delta"], out["share"], out["regime"])
     return out
+
+
+def fit_workspace(n_batches: int, device="cuda"):
+    """A device workspace tensor of llmv_fit_workspace_size bytes."""
+    return torch.empty(max(llmv_fit_workspace_size(n_batches), 1), dtype=torch.uint8,
+                       device=device)
+
+
+def fit(sums, phase, shape, y, theta0, rounds: int, ws=None):
+    """Allocates the outputs and runs llmv_fit; returns (theta fp64 [20],
+    counts int64 [4]) as device tensors."""
+    dev = y.device
+    theta = torch.empty(20, dtype=torch.float64, device=dev)
+    counts = torch.empty(4, dtype=torch.int64, device=dev)
+    llmv_fit(sums, phase, shape, y, theta0, rounds, theta, counts, ws)
+    return theta, counts
+
+
+METRIC_GROUPS = ("prefill", "decode", "all")
+
+
+def fit_metrics(sums, phase, shape, coeffs, y, ws=None, rel_err=False):
+    """Runs llmv_fit_metrics; returns {"prefill"|"decode"|"all": {"r2",
+    "p90", "p99", "n"}} (waits for the result), plus the per-batch relative
+    errors under "rel_err" when asked for."""
+    dev = y.device
+    out = torch.empty((3, 4), dtype=torch.float64, device=dev)
+    err = torch.empty(int(phase.numel()), dtype=torch.float32, device=dev) if rel_err else None
+    llmv_fit_metrics(sums, phase, shape, coeffs, y, out, err, ws)
+    o = out.cpu().tolist()
+    res = {g: {"r2": o[i][0], "p90": o[i][1], "p99": o[i][2], "n": int(o[i][3])}
+           for i, g in enumerate(METRIC_GROUPS)}
+    if rel_err:
+        res["rel_err"] = err
+    return res

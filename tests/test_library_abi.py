@@ -163,6 +163,57 @@ def test_batch_sums_and_admit_argument_errors(llmv):
     assert adm(None, None, 0, None, co, None, None, None, 0, None, None, None, None, None) == 0
 
 
+def test_fit_argument_errors(llmv):
+    """Host-side checks of llmv_fit / llmv_fit_metrics: every call below fails
+    before any launch (the workspace check is the last one)."""
+    lib = llmv.load()
+    E, EW = llmv.LLMV_EINVAL, llmv.LLMV_EWORKSPACE
+    th0 = (ctypes.c_double * 20)(*([1.0] * 20))
+    fit = lib.llmv_fit
+    #          sums  phase  nB  shape  y    theta0 rounds theta counts ws   bytes stream
+    assert fit(FAKE, FAKE, -1, None, FAKE, th0, 1, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, FAKE, (1 << 31) + 1, None, FAKE, th0, 1, FAKE, None, None, 0, None) == E
+    assert fit(None, FAKE, 8, None, FAKE, th0, 1, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, None, 8, None, FAKE, th0, 1, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, FAKE, 8, None, None, th0, 1, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, FAKE, 8, None, FAKE, None, 1, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, -1, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, 1025, FAKE, None, None, 0, None) == E
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, 1, None, None, None, 0, None) == E
+    bad = llmv.llmv_shape(n_layers=0)
+    assert fit(FAKE, FAKE, 8, ctypes.byref(bad), FAKE, th0, 1, FAKE, None, None, 0, None) == E
+    th0[3] = float("inf")
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, 1, FAKE, None, None, 0, None) == E
+    th0[3] = 1.0
+    need = lib.llmv_fit_workspace_size(8)
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, 1, FAKE, None, None, 0, None) == EW
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, 1, FAKE, None, FAKE, need - 1, None) == EW
+    assert fit(FAKE, FAKE, 8, None, FAKE, th0, 1, FAKE, None, FAKE + 16,
+               need, None) == EW
+    co = (ctypes.c_float * 20)(*([1.0] * 20))
+    met = lib.llmv_fit_metrics
+    #          sums  phase  nB  shape coeffs  y   rel_err out   ws   bytes stream
+    assert met(FAKE, FAKE, -1, None, co, FAKE, None, FAKE, None, 0, None) == E
+    assert met(None, FAKE, 8, None, co, FAKE, None, FAKE, None, 0, None) == E
+    assert met(FAKE, FAKE, 8, None, co, None, None, FAKE, None, 0, None) == E
+    assert met(FAKE, FAKE, 8, None, None, FAKE, None, FAKE, None, 0, None) == E
+    assert met(FAKE, FAKE, 8, None, co, FAKE, None, None, None, 0, None) == E
+    co[19] = float("nan")
+    assert met(FAKE, FAKE, 8, None, co, FAKE, None, FAKE, None, 0, None) == E
+    co[19] = 1.0
+    assert met(FAKE, FAKE, 8, None, co, FAKE, None, FAKE, None, 0, None) == EW
+    assert met(FAKE, FAKE, 8, None, co, FAKE, None, FAKE, FAKE, need - 1, None) == EW
+
+
+def test_fit_workspace_size(llmv):
+    """Fixed part plus 4 bytes per batch (the relative errors), 256-aligned."""
+    lib = llmv.load()
+    a, b = lib.llmv_fit_workspace_size(0), lib.llmv_fit_workspace_size(1 << 20)
+    assert a % 256 == 0 and b % 256 == 0
+    assert b - a == 4 << 20
+    assert lib.llmv_fit_workspace_size(1) == a + 256
+
+
 def test_python_binding_refuses_without_library(tmp_path):
     from paper_2608_08382_amd import llmv as mod
     saved = mod._lib
