@@ -44,9 +44,17 @@ FitLayout fit_layout(int64_t nB) {
 }
 
 // One workgroup per kFitWG batches, at most kFitMaxGrid and at least one
-// (the kernels write their partial sums even with no batches).
+// (the kernels write their partial sums even with no batches).  Every
+// workgroup of the grid starts inside the batch range.
 int fit_grid(int64_t nB) {
   const int64_t g = (nB + kFitWG - 1) / kFitWG;
+  return g < 1 ? 1 : (g > kFitMaxGrid ? kFitMaxGrid : (int)g);
+}
+
+// Radix passes take kSelUnroll errors per thread per iteration.
+int select_grid(int64_t nB) {
+  const int64_t per = (int64_t)kFitWG * kSelUnroll;
+  const int64_t g = (nB + per - 1) / per;
   return g < 1 ? 1 : (g > kFitMaxGrid ? kFitMaxGrid : (int)g);
 }
 
@@ -96,7 +104,7 @@ int llmv_fit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
     hipLaunchKernelGGL(k_fit_accum, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, F, y,
                        (const double*)theta, partials);
     HIP_TRY(hipGetLastError(), "k_fit_accum launch");
-    hipLaunchKernelGGL(k_fit_solve, dim3(1), dim3(kFitVals * kFitReduceParts), 0, s,
+    hipLaunchKernelGGL(k_fit_solve, dim3(1), dim3(kReduceWG), 0, s,
                        (const double*)partials, grid, theta, cnt);
     HIP_TRY(hipGetLastError(), "k_fit_solve launch");
   }
@@ -130,26 +138,31 @@ int llmv_fit_metrics(const int64_t* sums, const uint8_t* phase, int64_t n_batche
   hipStream_t s = (hipStream_t)stream;
   const int grid = fit_grid(n_batches);
 
+  // pass 1 (with the first radix pass of the percentile selection), its sums
+  // and the first pick; then pass 2 for r^2
+  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(256), 0, s, sel, hist);
+  HIP_TRY(hipGetLastError(), "k_select_init launch");
   hipLaunchKernelGGL(k_fit_metrics1, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, M, y,
-                     err, partials);
+                     err, partials, hist);
   HIP_TRY(hipGetLastError(), "k_fit_metrics1 launch");
-  hipLaunchKernelGGL(k_fit_metrics_sum, dim3(1), dim3(kMetricVals * kFitReduceParts), 0, s,
-                     (const double*)partials, grid, kMetricVals, tot1);
+  hipLaunchKernelGGL(k_fit_metrics_sum, dim3(1), dim3(kReduceWG), 0, s, (const double*)partials,
+                     grid, tot1);
   HIP_TRY(hipGetLastError(), "k_fit_metrics_sum launch");
+  hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(256), 0, s, sel, hist, (const double*)tot1);
+  HIP_TRY(hipGetLastError(), "k_select_pick launch");
   hipLaunchKernelGGL(k_fit_metrics2, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, M, y,
                      (const double*)tot1, partials);
   HIP_TRY(hipGetLastError(), "k_fit_metrics2 launch");
-  hipLaunchKernelGGL(k_fit_metrics_sum, dim3(1), dim3(kMetricVals * kFitReduceParts), 0, s,
-                     (const double*)partials, grid, kMetricVals, tot2);
+  hipLaunchKernelGGL(k_fit_metrics_sum, dim3(1), dim3(kReduceWG), 0, s, (const double*)partials,
+                     grid, tot2);
   HIP_TRY(hipGetLastError(), "k_fit_metrics_sum launch");
-  // exact percentiles: four radix passes of 8 bits over the fp32 errors
-  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(64), 0, s, (const double*)tot1, sel, hist);
-  HIP_TRY(hipGetLastError(), "k_select_init launch");
-  for (int pass = 0; pass < 4; ++pass) {
-    hipLaunchKernelGGL(k_select_hist, dim3(grid), dim3(kFitWG), 0, s, (const float*)err, phase,
+  // the remaining radix passes of 8 bits over the fp32 errors
+  const int sel_grid = select_grid(n_batches);
+  for (int pass = 1; pass < 4; ++pass) {
+    hipLaunchKernelGGL(k_select_hist, dim3(sel_grid), dim3(kFitWG), 0, s, (const float*)err, phase,
                        n_batches, pass, (const SelState*)sel, hist);
     HIP_TRY(hipGetLastError(), "k_select_hist launch");
-    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(64), 0, s, sel, hist);
+    hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(256), 0, s, sel, hist, (const double*)nullptr);
     HIP_TRY(hipGetLastError(), "k_select_pick launch");
   }
   hipLaunchKernelGGL(k_fit_metrics_final, dim3(1), dim3(64), 0, s, (const double*)tot1,

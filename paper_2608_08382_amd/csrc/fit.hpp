@@ -37,7 +37,7 @@ constexpr int kFitSet = 23;            // per set: X X^T upper triangle (15), X 
                                        // batches, batches with Q != P, batches with C != 0
 constexpr int kFitVals = 4 * kFitSet;  // the four (phase, segment) sets
 constexpr int kFitWG = 256;
-constexpr int kFitReduceParts = 8;     // partial sums per column in the fixed-order reduction
+constexpr int kReduceWG = 1024;        // threads of the fixed-order column reductions
 constexpr int kMetricVals = 8;         // per phase: n, sum y, m (y > 0), unused; x2 phases
 constexpr int kSelections = 6;         // (prefill, decode, all) x (p90, p99)
 
@@ -61,14 +61,14 @@ __device__ __forceinline__ double fit_eq1(const double* th, const double X[5]) {
   return acc;
 }
 
-// Eq. 1's feature vector of batch b from its exact sums (Sec. 2.1).
-__device__ __forceinline__ void fit_features(const double* S, const int64_t* __restrict__ sums,
-                                             int64_t nB, int64_t b, double X[5]) {
-  const int64_t n = sums[b];
+// Eq. 1's feature vector of a batch from its exact sums (Sec. 2.1):
+// (S0, S1*P, S2*C, S3*Q, |B|^2).
+__device__ __forceinline__ void fit_features(const double* S, int64_t n, int64_t P, int64_t C,
+                                             int64_t Q, double X[5]) {
   X[0] = S[0];
-  X[1] = S[1] * (double)sums[nB + b];
-  X[2] = S[2] * (double)sums[2 * nB + b];
-  X[3] = S[3] * (double)sums[3 * nB + b];
+  X[1] = S[1] * (double)P;
+  X[2] = S[2] * (double)C;
+  X[3] = S[3] * (double)Q;
   X[4] = (double)n * (double)n;
 }
 
@@ -77,11 +77,35 @@ __device__ __forceinline__ double wave_sum_f64(double x) {
   return x;
 }
 
+// The state of one batch: exact sums, measured latency and phase.
+struct BatchRegs {
+  int64_t n, P, C, Q;
+  double y;
+  int ph;  // 0 prefill, 1 decode, -1 empty or past the end
+};
+
+__device__ __forceinline__ BatchRegs load_batch(const int64_t* __restrict__ sums,
+                                                const uint8_t* __restrict__ phase,
+                                                const double* __restrict__ y, int64_t nB,
+                                                int64_t b) {
+  BatchRegs r{0, 0, 0, 0, 0.0, -1};
+  if (b < nB) {
+    r.n = sums[b];
+    r.P = sums[nB + b];
+    r.C = sums[2 * nB + b];
+    r.Q = sums[3 * nB + b];
+    r.y = y[b];
+    r.ph = r.n == 0 ? -1 : (phase[b] == 0 ? 0 : 1);
+  }
+  return r;
+}
+
 // Per-workgroup sums of the normal equations of each set under the current
-// coefficients theta (device [20]): partials[block][set*kFitSet + k].  Wave
-// w of a workgroup owns set w: the four waves walk the same batches (one
-// HBM read, the other three mostly cache hits), each lane adds the batches
-// of its wave's set into 23 register accumulators.
+// coefficients theta (device [20]): partials[block][set*kFitSet + k].
+// A workgroup walks chunks of kFitWG batches: the chunk is loaded once,
+// coalesced (the next chunk's loads are issued before the current one is
+// processed) and staged in LDS; wave w then folds the chunk's batches of set
+// w (phase w/2, segment w%2) into 23 register accumulators per lane.
 __global__ __launch_bounds__(kFitWG) void k_fit_accum(const int64_t* __restrict__ sums,
                                                       const uint8_t* __restrict__ phase,
                                                       int64_t nB, const FitShape F,
@@ -89,7 +113,10 @@ __global__ __launch_bounds__(kFitWG) void k_fit_accum(const int64_t* __restrict_
                                                       const double* __restrict__ theta,
                                                       double* __restrict__ partials) {
   static_assert(kFitWG == 4 * 64, "one wave per (phase, segment) set");
-  const int lane = threadIdx.x & 63, set = threadIdx.x >> 6;
+  __shared__ int64_t s_n[kFitWG], s_P[kFitWG], s_C[kFitWG], s_Q[kFitWG];
+  __shared__ double s_y[kFitWG];
+  __shared__ int s_ph[kFitWG];
+  const int tid = threadIdx.x, lane = tid & 63, set = tid >> 6;
   const int set_phase = set >> 1, set_seg = set & 1;
   double th[10];  // the two segment sets of this wave's phase
 #pragma unroll
@@ -98,26 +125,41 @@ __global__ __launch_bounds__(kFitWG) void k_fit_accum(const int64_t* __restrict_
 #pragma unroll
   for (int i = 0; i < kFitSet; ++i) acc[i] = 0.0;
 
-  const int64_t stride = (int64_t)gridDim.x * 64;
-  for (int64_t b = (int64_t)blockIdx.x * 64 + lane; b < nB; b += stride) {
-    const int64_t n = sums[b];
-    if (n == 0 || (phase[b] == 0 ? 0 : 1) != set_phase) continue;
-    double X[5];
-    fit_features(F.S, sums, nB, b, X);
-    // Roofline max of the two segments; ties stay memory-bound.
-    const int seg = fit_eq1(th + 5, X) > fit_eq1(th, X) ? 1 : 0;
-    if (seg != set_seg) continue;
-    const double yb = y[b];
-    int k = 0;
+  const int64_t stride = (int64_t)gridDim.x * kFitWG;
+  int64_t base = (int64_t)blockIdx.x * kFitWG;
+  BatchRegs cur = load_batch(sums, phase, y, nB, base + tid);
+  for (; base < nB; base += stride) {
+    s_n[tid] = cur.n;
+    s_P[tid] = cur.P;
+    s_C[tid] = cur.C;
+    s_Q[tid] = cur.Q;
+    s_y[tid] = cur.y;
+    s_ph[tid] = cur.ph;
+    __syncthreads();
+    cur = load_batch(sums, phase, y, nB, base + stride + tid);  // next chunk, in flight
 #pragma unroll
-    for (int i = 0; i < 5; ++i)
+    for (int k = 0; k < kFitWG / 64; ++k) {
+      const int i = k * 64 + lane;
+      if (s_ph[i] != set_phase) continue;
+      const int64_t P = s_P[i], C = s_C[i], Q = s_Q[i];
+      double X[5];
+      fit_features(F.S, s_n[i], P, C, Q, X);
+      // Roofline max of the two segments; ties stay memory-bound.
+      const int seg = fit_eq1(th + 5, X) > fit_eq1(th, X) ? 1 : 0;
+      if (seg != set_seg) continue;
+      const double yb = s_y[i];
+      int q = 0;
 #pragma unroll
-      for (int j = i; j < 5; ++j) acc[k++] += X[i] * X[j];
+      for (int a = 0; a < 5; ++a)
 #pragma unroll
-    for (int i = 0; i < 5; ++i) acc[15 + i] += X[i] * yb;
-    acc[20] += 1.0;
-    acc[21] += sums[3 * nB + b] != sums[nB + b] ? 1.0 : 0.0;
-    acc[22] += sums[2 * nB + b] != 0 ? 1.0 : 0.0;
+        for (int c = a; c < 5; ++c) acc[q++] += X[a] * X[c];
+#pragma unroll
+      for (int a = 0; a < 5; ++a) acc[15 + a] += X[a] * yb;
+      acc[20] += 1.0;
+      acc[21] += Q != P ? 1.0 : 0.0;
+      acc[22] += C != 0 ? 1.0 : 0.0;
+    }
+    __syncthreads();
   }
 #pragma unroll
   for (int i = 0; i < kFitSet; ++i) {
@@ -126,81 +168,110 @@ __global__ __launch_bounds__(kFitWG) void k_fit_accum(const int64_t* __restrict_
   }
 }
 
-// Column sums of partials[grid][ncols] in a fixed order, by one workgroup of
-// ncols * kFitReduceParts threads (ncols <= 128); the result lands in LDS
-// tot[ncols].
+// Column sums of partials[grid][NCOLS] in a fixed order by one workgroup of
+// kReduceWG threads: thread (part, col) adds rows part, part + PARTS, ...;
+// then thread col adds the PARTS results in order.  The totals land in LDS
+// tot[NCOLS].
+template <int NCOLS>
 __device__ __forceinline__ void reduce_columns(const double* __restrict__ partials, int grid,
-                                               int ncols, double* red, double* tot) {
+                                               double* red, double* tot) {
+  constexpr int PARTS = kReduceWG / NCOLS;
   const int t = threadIdx.x;
-  if (t < ncols * kFitReduceParts) {
-    const int col = t % ncols, part = t / ncols;
+  if (t < PARTS * NCOLS) {
+    const int col = t % NCOLS, part = t / NCOLS;
     double s = 0.0;
-    for (int blk = part; blk < grid; blk += kFitReduceParts) s += partials[(int64_t)blk * ncols + col];
-    red[part * ncols + col] = s;
+#pragma unroll 8
+    for (int blk = part; blk < grid; blk += PARTS) s += partials[(int64_t)blk * NCOLS + col];
+    red[part * NCOLS + col] = s;
   }
   __syncthreads();
-  if (t < ncols) {
+  if (t < NCOLS) {
     double s = 0.0;
-    for (int part = 0; part < kFitReduceParts; ++part) s += red[part * ncols + t];
+#pragma unroll 8
+    for (int part = 0; part < PARTS; ++part) s += red[part * NCOLS + t];
     tot[t] = s;
   }
   __syncthreads();
 }
 
-// Solves one set's normal equations over its free coefficients (Jacobi
-// scaling, then Cholesky); returns false when the set keeps its
-// coefficients.  A: 15 upper-triangle entries, r: 5 entries of X y.
+// Solves one set's normal equations over its free coefficients; returns
+// false when the set keeps its coefficients.  A15: the 15 upper-triangle
+// entries of X^T X, r: X^T y.  The free columns are scaled to unit diagonal
+// and factorised by Cholesky; a kept column becomes an identity row (its
+// term is moved to the right-hand side first), so the 5x5 code is fully
+// unrolled and stays in registers.  A pivot below 1e-12 (condition number of
+// the scaled columns beyond ~1e6) counts as dependent columns.
 __device__ inline bool solve_set(const double* A15, const double* r, double cnt, double npq,
-                                 double nc, double* th) {
-  int free_[5], nf = 0;
-  bool kept[5] = {false, false, false, false, false};
-  if (nc == 0.0) kept[2] = true;
-  if (npq == 0.0) kept[3] = true;
-  for (int i = 0; i < 5; ++i)
-    if (!kept[i]) free_[nf++] = i;
+                                 double nc, double th[5]) {
+  const bool kept[5] = {false, false, nc == 0.0, npq == 0.0, false};
+  const int nf = 5 - (kept[2] ? 1 : 0) - (kept[3] ? 1 : 0);
   if (cnt < (double)nf) return false;
   double A[5][5];
-  int k = 0;
+  int q = 0;
+#pragma unroll
   for (int i = 0; i < 5; ++i)
-    for (int j = i; j < 5; ++j) A[i][j] = A[j][i] = A15[k++];
-  double M[5][5], b[5], d[5];
-  for (int a = 0; a < nf; ++a) {
-    const int i = free_[a];
+#pragma unroll
+    for (int j = i; j < 5; ++j) {
+      A[i][j] = A15[q];
+      A[j][i] = A15[q];
+      ++q;
+    }
+  double d[5], b[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
     double rhs = r[i];
+#pragma unroll
     for (int j = 0; j < 5; ++j)
       if (kept[j]) rhs -= A[i][j] * th[j];
-    if (!(A[i][i] > 0.0)) return false;
-    d[a] = sqrt(A[i][i]);
-    b[a] = rhs / d[a];
+    if (kept[i]) {
+      d[i] = 1.0;
+      b[i] = 0.0;
+    } else {
+      if (!(A[i][i] > 0.0)) return false;
+      d[i] = sqrt(A[i][i]);
+      b[i] = rhs / d[i];
+    }
   }
-  for (int a = 0; a < nf; ++a)
-    for (int c = 0; c < nf; ++c) M[a][c] = A[free_[a]][free_[c]] / (d[a] * d[c]);
-  // Cholesky M = L L^T (unit diagonal after scaling); a tiny pivot means
-  // dependent columns
+  double M[5][5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i)
+#pragma unroll
+    for (int j = 0; j < 5; ++j)
+      M[i][j] = (kept[i] || kept[j]) ? (i == j ? 1.0 : 0.0) : A[i][j] / (d[i] * d[j]);
   double L[5][5];
-  for (int j = 0; j < nf; ++j) {
+#pragma unroll
+  for (int j = 0; j < 5; ++j) {
     double s = M[j][j];
-    for (int q = 0; q < j; ++q) s -= L[j][q] * L[j][q];
+#pragma unroll
+    for (int k = 0; k < j; ++k) s -= L[j][k] * L[j][k];
     if (!(s > 1e-12)) return false;
     L[j][j] = sqrt(s);
-    for (int i = j + 1; i < nf; ++i) {
+#pragma unroll
+    for (int i = j + 1; i < 5; ++i) {
       double t = M[i][j];
-      for (int q = 0; q < j; ++q) t -= L[i][q] * L[j][q];
+#pragma unroll
+      for (int k = 0; k < j; ++k) t -= L[i][k] * L[j][k];
       L[i][j] = t / L[j][j];
     }
   }
   double z[5], x[5];
-  for (int i = 0; i < nf; ++i) {
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
     double t = b[i];
-    for (int q = 0; q < i; ++q) t -= L[i][q] * z[q];
+#pragma unroll
+    for (int k = 0; k < i; ++k) t -= L[i][k] * z[k];
     z[i] = t / L[i][i];
   }
-  for (int i = nf - 1; i >= 0; --i) {
+#pragma unroll
+  for (int i = 4; i >= 0; --i) {
     double t = z[i];
-    for (int q = i + 1; q < nf; ++q) t -= L[q][i] * x[q];
+#pragma unroll
+    for (int k = i + 1; k < 5; ++k) t -= L[k][i] * x[k];
     x[i] = t / L[i][i];
   }
-  for (int a = 0; a < nf; ++a) th[free_[a]] = x[a] / d[a];
+#pragma unroll
+  for (int i = 0; i < 5; ++i)
+    if (!kept[i]) th[i] = x[i] / d[i];
   return true;
 }
 
@@ -208,19 +279,22 @@ __device__ inline bool solve_set(const double* A15, const double* r, double cnt,
 // per-workgroup partials in a fixed order, then each set solved; theta
 // (device [20]) is updated in place and counts[4] receives each set's batch
 // count.
-__global__ __launch_bounds__(kFitVals * kFitReduceParts) void k_fit_solve(
-    const double* __restrict__ partials, int grid, double* __restrict__ theta,
-    long long* __restrict__ counts) {
-  __shared__ double s_red[kFitReduceParts * kFitVals];
+__global__ __launch_bounds__(kReduceWG) void k_fit_solve(const double* __restrict__ partials,
+                                                         int grid, double* __restrict__ theta,
+                                                         long long* __restrict__ counts) {
+  __shared__ double s_red[kReduceWG];
   __shared__ double s_tot[kFitVals];
-  reduce_columns(partials, grid, kFitVals, s_red, s_tot);
+  reduce_columns<kFitVals>(partials, grid, s_red, s_tot);
   const int g = threadIdx.x;
   if (g < 4) {
     const double* a = s_tot + g * kFitSet;
     double th[5];
+#pragma unroll
     for (int i = 0; i < 5; ++i) th[i] = theta[g * 5 + i];
-    if (solve_set(a, a + 15, a[20], a[21], a[22], th))
+    if (solve_set(a, a + 15, a[20], a[21], a[22], th)) {
+#pragma unroll
       for (int i = 0; i < 5; ++i) theta[g * 5 + i] = th[i];
+    }
     counts[g] = (long long)a[20];
   }
 }
@@ -236,93 +310,19 @@ __global__ __launch_bounds__(64) void k_fit_init(const FitModel M, double* __res
 
 // ------------------------------------------------------------ metrics
 
-// Pass 1: prediction and relative error of every batch (NaN for an empty
-// batch or y <= 0) and, per phase, the batch count, sum y and the count of
-// relative errors: partials[block][8].
-__global__ __launch_bounds__(kFitWG) void k_fit_metrics1(const int64_t* __restrict__ sums,
-                                                         const uint8_t* __restrict__ phase,
-                                                         int64_t nB, const FitModel A,
-                                                         const double* __restrict__ y,
-                                                         float* __restrict__ rel_err,
-                                                         double* __restrict__ partials) {
-  __shared__ double s_red[kFitWG / 64][kMetricVals];
-  double acc[kMetricVals] = {0, 0, 0, 0, 0, 0, 0, 0};
-  const int64_t stride = (int64_t)gridDim.x * kFitWG;
-  for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
-    float e = __builtin_nanf("");
-    if (sums[b] != 0) {
-      double X[5];
-      fit_features(A.S, sums, nB, b, X);
-      const int ph = phase[b] == 0 ? 0 : 1;
-      const double tm = fit_eq1(A.th + (ph * 2 + 0) * 5, X), tc = fit_eq1(A.th + (ph * 2 + 1) * 5, X);
-      const double yhat = tc > tm ? tc : tm, yb = y[b];
-      if (yb > 0) e = (float)(fabs(yhat - yb) / yb);
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        acc[q * 4 + 0] += ph == q ? 1.0 : 0.0;
-        acc[q * 4 + 1] += ph == q ? yb : 0.0;
-        acc[q * 4 + 2] += (ph == q && yb > 0) ? 1.0 : 0.0;
-      }
-    }
-    if (rel_err) rel_err[b] = e;
-  }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int i = 0; i < kMetricVals; ++i) {
-    const double t = wave_sum_f64(acc[i]);
-    if (lane == 0) s_red[wave][i] = t;
-  }
-  __syncthreads();
-  if (threadIdx.x < kMetricVals) {
-    double t = 0.0;
-    for (int w = 0; w < kFitWG / 64; ++w) t += s_red[w][threadIdx.x];
-    partials[(int64_t)blockIdx.x * kMetricVals + threadIdx.x] = t;
-  }
+// The model's prediction (segment max) for a nonempty batch.
+__device__ __forceinline__ double predict(const FitModel& A, const BatchRegs& r) {
+  double X[5];
+  fit_features(A.S, r.n, r.P, r.C, r.Q, X);
+  const double tm = fit_eq1(A.th + (r.ph * 2 + 0) * 5, X);
+  const double tc = fit_eq1(A.th + (r.ph * 2 + 1) * 5, X);
+  return tc > tm ? tc : tm;
 }
 
-// Sums pass-1 partials (fixed order) into tot[8].
-__global__ __launch_bounds__(kMetricVals * kFitReduceParts) void k_fit_metrics_sum(
-    const double* __restrict__ partials, int grid, int ncols, double* __restrict__ tot) {
-  __shared__ double s_red[kFitReduceParts * kMetricVals];
-  __shared__ double s_tot[kMetricVals];
-  reduce_columns(partials, grid, ncols, s_red, s_tot);
-  if (threadIdx.x < ncols) tot[threadIdx.x] = s_tot[threadIdx.x];
-}
-
-// Pass 2: per phase (and all), sum (y - mean)^2 and sum (y - yhat)^2 with
-// the means of pass 1 (tot1[8]): partials[block][8] = (prefill tot, sse,
-// decode tot, sse, all tot, sse, -, -).  Means per group are taken from the
-// pass-1 sums.
-__global__ __launch_bounds__(kFitWG) void k_fit_metrics2(const int64_t* __restrict__ sums,
-                                                         const uint8_t* __restrict__ phase,
-                                                         int64_t nB, const FitModel A,
-                                                         const double* __restrict__ y,
-                                                         const double* __restrict__ tot1,
-                                                         double* __restrict__ partials) {
+// The workgroup's sums of acc[kMetricVals] into partials[block][...].
+__device__ __forceinline__ void block_partials(const double acc[kMetricVals],
+                                               double* __restrict__ partials) {
   __shared__ double s_red[kFitWG / 64][kMetricVals];
-  const double n0 = tot1[0], n1 = tot1[4];
-  const double mean[3] = {n0 > 0 ? tot1[1] / n0 : 0.0, n1 > 0 ? tot1[5] / n1 : 0.0,
-                          n0 + n1 > 0 ? (tot1[1] + tot1[5]) / (n0 + n1) : 0.0};
-  double acc[kMetricVals] = {0, 0, 0, 0, 0, 0, 0, 0};
-  const int64_t stride = (int64_t)gridDim.x * kFitWG;
-  for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
-    if (sums[b] == 0) continue;
-    double X[5];
-    fit_features(A.S, sums, nB, b, X);
-    const int ph = phase[b] == 0 ? 0 : 1;
-    const double tm = fit_eq1(A.th + (ph * 2 + 0) * 5, X), tc = fit_eq1(A.th + (ph * 2 + 1) * 5, X);
-    const double yhat = tc > tm ? tc : tm, yb = y[b];
-    const double r = yb - yhat;
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const double dv = yb - mean[q];
-      acc[q * 2 + 0] += ph == q ? dv * dv : 0.0;
-      acc[q * 2 + 1] += ph == q ? r * r : 0.0;
-    }
-    const double da = yb - mean[2];
-    acc[4] += da * da;
-    acc[5] += r * r;
-  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
   for (int i = 0; i < kMetricVals; ++i) {
@@ -339,15 +339,139 @@ __global__ __launch_bounds__(kFitWG) void k_fit_metrics2(const int64_t* __restri
 
 // Radix select state of one selection: the bits chosen so far (prefix, the
 // top 8*pass bits) and the rank still to find inside the prefix bucket
-// (1-based; 0 = no values).
+// (1-based; 0 = no values).  Selection s: group s / 2 (0 prefill, 1 decode,
+// 2 all), p90 for even s, p99 for odd s.
 struct SelState {
   unsigned int prefix;
   unsigned int rank;
 };
 
-// One radix pass: hist[sel][digit] counts the relative errors of the
-// selection's group whose top 8*pass bits equal its prefix, by the next 8
-// bits.  Selection s: group s / 2 (0 prefill, 1 decode, 2 all).
+// Selections whose histogram has to be counted.  Two selections of one
+// group with the same prefix have the same histogram (p99 reuses p90's);
+// an "all" selection whose prefix equals both phase selections' of its
+// percentile has the sum of theirs.  In pass 0 every prefix is empty, so
+// only the prefill and decode p90 histograms are counted.
+__device__ __forceinline__ unsigned int counted_selections(const unsigned int pre[kSelections]) {
+  unsigned int m = 0;
+#pragma unroll
+  for (int s = 0; s < kSelections; ++s) {
+    const bool same_group = (s & 1) && pre[s] == pre[s - 1];
+    const bool both_phases = s >= 4 && pre[s] == pre[s - 4] && pre[s] == pre[s - 2];
+    if (!same_group && !both_phases) m |= 1u << s;
+  }
+  return m;
+}
+
+// Adds one relative error (group grp, or -1 for none) to the LDS histograms
+// of the counted selections whose prefix it matches.
+__device__ __forceinline__ void select_add(unsigned int* s_hist, float e, int grp, int pass,
+                                           const unsigned int pre[kSelections],
+                                           unsigned int counted) {
+  if (grp < 0) return;
+  const unsigned int u = __float_as_uint(e);
+  const int shift = 24 - 8 * pass;
+  const unsigned int digit = (u >> shift) & 255u;
+  const unsigned int top = pass == 0 ? 0u : (u >> (shift + 8));
+#pragma unroll
+  for (int s = 0; s < kSelections; ++s) {
+    const int sg = s / 2;
+    if (((counted >> s) & 1u) && (sg == grp || sg == 2) && top == pre[s])
+      atomicAdd(&s_hist[s * 256 + digit], 1u);
+  }
+}
+
+// Adds a workgroup's LDS histograms into the global ones.
+__device__ __forceinline__ void flush_hist(const unsigned int* s_hist, unsigned int counted,
+                                           unsigned int* __restrict__ hist) {
+  for (int i = threadIdx.x; i < kSelections * 256; i += blockDim.x)
+    if (((counted >> (i / 256)) & 1u) && s_hist[i]) atomicAdd(&hist[i], s_hist[i]);
+}
+
+// Pass 1: prediction and relative error of every batch (NaN for an empty
+// batch or y <= 0) and, per phase, the batch count, sum y and the count of
+// relative errors: partials[block][8] = (n, sum y, m, -) for prefill, then
+// decode.  Also the first radix pass of the percentile selection (the top 8
+// bits of every error; hist must be zero on entry).
+__global__ __launch_bounds__(kFitWG) void k_fit_metrics1(const int64_t* __restrict__ sums,
+                                                         const uint8_t* __restrict__ phase,
+                                                         int64_t nB, const FitModel A,
+                                                         const double* __restrict__ y,
+                                                         float* __restrict__ rel_err,
+                                                         double* __restrict__ partials,
+                                                         unsigned int* __restrict__ hist) {
+  __shared__ unsigned int s_hist[kSelections * 256];
+  for (int i = threadIdx.x; i < kSelections * 256; i += kFitWG) s_hist[i] = 0u;
+  __syncthreads();
+  const unsigned int pre0[kSelections] = {0, 0, 0, 0, 0, 0};
+  const unsigned int counted = counted_selections(pre0);
+  double acc[kMetricVals] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int64_t stride = (int64_t)gridDim.x * kFitWG;
+  for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
+    const BatchRegs r = load_batch(sums, phase, y, nB, b);
+    float e = __builtin_nanf("");
+    if (r.ph >= 0) {
+      const double yhat = predict(A, r);
+      if (r.y > 0) e = (float)(fabs(yhat - r.y) / r.y);
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        acc[q * 4 + 0] += r.ph == q ? 1.0 : 0.0;
+        acc[q * 4 + 1] += r.ph == q ? r.y : 0.0;
+        acc[q * 4 + 2] += (r.ph == q && r.y > 0) ? 1.0 : 0.0;
+      }
+    }
+    rel_err[b] = e;
+    select_add(s_hist, e, (r.ph >= 0 && r.y > 0) ? r.ph : -1, 0, pre0, counted);
+  }
+  block_partials(acc, partials);  // synchronises the workgroup
+  flush_hist(s_hist, counted, hist);
+}
+
+// Sums a pass's partials (fixed order) into tot[8].
+__global__ __launch_bounds__(kReduceWG) void k_fit_metrics_sum(const double* __restrict__ partials,
+                                                               int grid,
+                                                               double* __restrict__ tot) {
+  __shared__ double s_red[kReduceWG];
+  __shared__ double s_tot[kMetricVals];
+  reduce_columns<kMetricVals>(partials, grid, s_red, s_tot);
+  if (threadIdx.x < kMetricVals) tot[threadIdx.x] = s_tot[threadIdx.x];
+}
+
+// Pass 2: per phase (and all), sum (y - mean)^2 and sum (y - yhat)^2 with
+// the means of the pass-1 sums tot1[8]: partials[block][8] = (prefill
+// sst, sse, decode sst, sse, all sst, sse, -, -).
+__global__ __launch_bounds__(kFitWG) void k_fit_metrics2(const int64_t* __restrict__ sums,
+                                                         const uint8_t* __restrict__ phase,
+                                                         int64_t nB, const FitModel A,
+                                                         const double* __restrict__ y,
+                                                         const double* __restrict__ tot1,
+                                                         double* __restrict__ partials) {
+  const double n0 = tot1[0], n1 = tot1[4];
+  const double mean[3] = {n0 > 0 ? tot1[1] / n0 : 0.0, n1 > 0 ? tot1[5] / n1 : 0.0,
+                          n0 + n1 > 0 ? (tot1[1] + tot1[5]) / (n0 + n1) : 0.0};
+  double acc[kMetricVals] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int64_t stride = (int64_t)gridDim.x * kFitWG;
+  for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
+    const BatchRegs r = load_batch(sums, phase, y, nB, b);
+    if (r.ph < 0) continue;
+    const double res = r.y - predict(A, r);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const double dv = r.y - mean[q];
+      acc[q * 2 + 0] += r.ph == q ? dv * dv : 0.0;
+      acc[q * 2 + 1] += r.ph == q ? res * res : 0.0;
+    }
+    const double da = r.y - mean[2];
+    acc[4] += da * da;
+    acc[5] += res * res;
+  }
+  block_partials(acc, partials);
+}
+
+// One later radix pass (pass 1..3): hist[sel][digit] counts the relative
+// errors of the selection's group whose top 8*pass bits equal its prefix, by
+// the next 8 bits (counted selections only).  Four errors per thread per
+// iteration, their loads issued together.
+constexpr int kSelUnroll = 4;
 __global__ __launch_bounds__(kFitWG) void k_select_hist(const float* __restrict__ rel_err,
                                                         const uint8_t* __restrict__ phase,
                                                         int64_t nB, int pass,
@@ -355,65 +479,103 @@ __global__ __launch_bounds__(kFitWG) void k_select_hist(const float* __restrict_
                                                         unsigned int* __restrict__ hist) {
   __shared__ unsigned int s_hist[kSelections * 256];
   for (int i = threadIdx.x; i < kSelections * 256; i += kFitWG) s_hist[i] = 0u;
-  __syncthreads();
   unsigned int pre[kSelections];
 #pragma unroll
   for (int s = 0; s < kSelections; ++s) pre[s] = st[s].prefix;
-  const int shift = 24 - 8 * pass;
-  const int64_t stride = (int64_t)gridDim.x * kFitWG;
-  for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
-    const float e = rel_err[b];
-    if (!(e >= 0.0f)) continue;  // NaN: empty batch or y <= 0
-    const unsigned int u = __float_as_uint(e);
-    const int grp = phase[b] == 0 ? 0 : 1;
-    const unsigned int digit = (u >> shift) & 255u;
-    const unsigned int top = pass == 0 ? 0u : (u >> (shift + 8));
+  const unsigned int counted = counted_selections(pre);
+  __syncthreads();
+  const int64_t step = (int64_t)kFitWG * kSelUnroll;
+  const int64_t stride = (int64_t)gridDim.x * step;
+  for (int64_t b0 = (int64_t)blockIdx.x * step + threadIdx.x; b0 < nB; b0 += stride) {
+    float e[kSelUnroll];
+    int ph[kSelUnroll];
+#pragma unroll
+    for (int u = 0; u < kSelUnroll; ++u) {
+      const int64_t b = b0 + (int64_t)u * kFitWG;
+      e[u] = b < nB ? rel_err[b] : __builtin_nanf("");
+      ph[u] = b < nB ? (int)phase[b] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kSelUnroll; ++u)
+      select_add(s_hist, e[u], e[u] >= 0.0f ? (ph[u] == 0 ? 0 : 1) : -1, pass, pre, counted);
+  }
+  __syncthreads();
+  flush_hist(s_hist, counted, hist);
+}
+
+// After a radix pass: each selection moves into the bucket holding its rank
+// (thread t owns digit t of every selection; an inclusive scan over the 256
+// counts finds the bucket), and the histogram is cleared for the next pass.
+// A selection that was not counted takes the histogram it equals (see
+// counted_selections).  After the first pass (tot1 != NULL) the ranks come
+// from the pass-1 counts m (tot1[2], tot1[6]): ceil(9m/10) and
+// ceil(99m/100), 0 when m = 0.
+__global__ __launch_bounds__(256) void k_select_pick(SelState* __restrict__ st,
+                                                     unsigned int* __restrict__ hist,
+                                                     const double* __restrict__ tot1) {
+  __shared__ unsigned int s_wave[kSelections][4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  SelState cur[kSelections];
+  unsigned int pre[kSelections];
+#pragma unroll
+  for (int s = 0; s < kSelections; ++s) {
+    cur[s] = st[s];
+    pre[s] = cur[s].prefix;
+  }
+  if (tot1) {
+    const unsigned long long m0 = (unsigned long long)tot1[2], m1 = (unsigned long long)tot1[6];
 #pragma unroll
     for (int s = 0; s < kSelections; ++s) {
-      const int sg = s / 2;
-      if ((sg == grp || sg == 2) && top == pre[s]) atomicAdd(&s_hist[s * 256 + digit], 1u);
+      const int g = s / 2;
+      const unsigned long long m = g == 0 ? m0 : (g == 1 ? m1 : m0 + m1);
+      const unsigned long long num = (s & 1) ? 99 : 9, den = (s & 1) ? 100 : 10;
+      cur[s].rank = (unsigned int)((num * m + den - 1) / den);
     }
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < kSelections * 256; i += kFitWG)
-    if (s_hist[i]) atomicAdd(&hist[i], s_hist[i]);
-}
-
-// After a radix pass: each selection moves into the bucket holding its rank;
-// the histogram is cleared for the next pass.  One workgroup of 64 threads.
-__global__ __launch_bounds__(64) void k_select_pick(SelState* __restrict__ st,
-                                                    unsigned int* __restrict__ hist) {
-  const int s = threadIdx.x;
-  if (s < kSelections && st[s].rank > 0) {
-    unsigned int below = 0, digit = 0;
-    for (; digit < 256; ++digit) {
-      const unsigned int h = hist[s * 256 + digit];
-      if (below + h >= st[s].rank) break;
-      below += h;
+  const unsigned int counted = counted_selections(pre);
+  unsigned int v[kSelections], incl[kSelections];
+#pragma unroll
+  for (int s = 0; s < kSelections; ++s) {
+    if ((counted >> s) & 1u) {
+      v[s] = hist[s * 256 + t];
+      hist[s * 256 + t] = 0u;
+    } else if ((s & 1) && pre[s] == pre[s - 1]) {
+      v[s] = v[s - 1];
+    } else {
+      v[s] = v[s - 4] + v[s - 2];
     }
-    st[s].prefix = (st[s].prefix << 8) | (digit & 255u);
-    st[s].rank -= below;
+    unsigned int x = v[s];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const unsigned int up = __shfl_up(x, off, 64);
+      if (lane >= off) x += up;
+    }
+    incl[s] = x;
+    if (lane == 63) s_wave[s][w] = x;
   }
-  __syncthreads();
-  for (int i = threadIdx.x; i < kSelections * 256; i += 64) hist[i] = 0u;
+  __syncthreads();  // every thread has read st[] before one of them rewrites it
+#pragma unroll
+  for (int s = 0; s < kSelections; ++s) {
+    unsigned int before = 0;
+    for (int k = 0; k < w; ++k) before += s_wave[s][k];
+    const unsigned int hi = before + incl[s], lo = hi - v[s];
+    const unsigned int rank = cur[s].rank;
+    if (rank > 0 && lo < rank && rank <= hi) {
+      st[s].prefix = (cur[s].prefix << 8) | (unsigned int)t;
+      st[s].rank = rank - lo;
+    } else if (t == 0 && rank == 0) {
+      st[s].rank = 0;
+    }
+  }
 }
 
-// The selections' starting ranks from the pass-1 counts (tot1: m at [2] and
-// [6]): ceil(m * 9/10) and ceil(m * 99/100), 0 when m = 0.  Also clears the
-// histogram.
-__global__ __launch_bounds__(64) void k_select_init(const double* __restrict__ tot1,
-                                                    SelState* __restrict__ st,
-                                                    unsigned int* __restrict__ hist) {
-  const int s = threadIdx.x;
-  if (s < kSelections) {
-    const int g = s / 2;
-    const unsigned long long m0 = (unsigned long long)tot1[2], m1 = (unsigned long long)tot1[6];
-    const unsigned long long m = g == 0 ? m0 : (g == 1 ? m1 : m0 + m1);
-    const unsigned long long num = (s & 1) ? 99 : 9, den = (s & 1) ? 100 : 10;
-    st[s].prefix = 0u;
-    st[s].rank = (unsigned int)((num * m + den - 1) / den);
-  }
-  for (int i = threadIdx.x; i < kSelections * 256; i += 64) hist[i] = 0u;
+// Clears the selection state (empty prefixes, no ranks) and the histogram
+// before the first radix pass.
+__global__ __launch_bounds__(256) void k_select_init(SelState* __restrict__ st,
+                                                     unsigned int* __restrict__ hist) {
+  const int t = threadIdx.x;
+  if (t < kSelections) st[t] = SelState{0u, 0u};
+  for (int i = t; i < kSelections * 256; i += 256) hist[i] = 0u;
 }
 
 // The metrics from the pass sums and the selected percentiles:
