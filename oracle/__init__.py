@@ -104,8 +104,12 @@ class Oracle:
         lib.orc_tenant_sums.argtypes = [P, P, i64, i32, P]
         lib.orc_batch_sums.argtypes = [i64, i64, P, P, P, P, P]
         lib.orc_admit.argtypes = [i64, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
+        lib.orc_shape_constants_ext.argtypes = [P, P]
+        lib.orc_attribute_ext.argtypes = [i64, i64, P, P, P, P, P, P, i32,
+                                          P, P, P, P, P, P, P, P]
         for f in ("orc_shape_constants", "orc_validate", "orc_features",
-                  "orc_attribute", "orc_tenant_sums", "orc_batch_sums", "orc_admit"):
+                  "orc_attribute", "orc_tenant_sums", "orc_batch_sums", "orc_admit",
+                  "orc_shape_constants_ext", "orc_attribute_ext"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
         self.path = so_path
@@ -136,14 +140,23 @@ class Oracle:
         del keep
         return xr, xb
 
+    def shape_constants_ext(self, shape=None) -> np.ndarray:
+        """(S0, S1, S2, S3, S5, S6) of the extended model."""
+        S = np.zeros(6, np.float64)
+        keep, sp = _shape_ptr(shape)
+        _check(self.lib.orc_shape_constants_ext(sp, _ptr(S)), "shape_constants_ext")
+        del keep
+        return S
+
     def attribute(self, offsets, p, c, tenant, shape, coeffs, n_tenants,
-                  outputs=ALL_OUTPUTS) -> dict:
-        """Runs the oracle; returns a dict with the requested outputs."""
+                  outputs=ALL_OUTPUTS, ext=False) -> dict:
+        """Runs the oracle; returns a dict with the requested outputs.  With
+        ext=True, the extended model (28 coefficients)."""
         off = _arr(offsets, np.int64)
         p, c, t = _arr(p, np.int32), _arr(c, np.int32), _arr(tenant, np.int32)
         co = _arr(coeffs, np.float32)
-        if co.shape != (20,):
-            raise ValueError("coeffs must hold 20 fp32 values")
+        if co.shape != ((28,) if ext else (20,)):
+            raise ValueError("coeffs must hold 28 (extended) or 20 fp32 values")
         nB, N = len(off) - 1, len(p)
         out = {}
         for name, n, dt in (("T", nB, np.float64), ("TM", nB, np.float64),
@@ -156,7 +169,8 @@ class Oracle:
             out["tenant_sums"] = np.zeros(int(n_tenants), np.float64)
         keep, sp = _shape_ptr(shape)
         g = out.get
-        rc = self.lib.orc_attribute(
+        fn = self.lib.orc_attribute_ext if ext else self.lib.orc_attribute
+        rc = fn(
             nB, N, _ptr(off), _ptr(p), _ptr(c), _ptr(t), sp, _ptr(co), int(n_tenants),
             _ptr(g("T")), _ptr(g("TM")), _ptr(g("TC")), _ptr(g("phase")),
             _ptr(g("regime")), _ptr(g("share")), _ptr(g("share_alt")),
@@ -230,6 +244,15 @@ def features(offsets, p, c, shape=None):
 
 def attribute(offsets, p, c, tenant, shape, coeffs, n_tenants, outputs=ALL_OUTPUTS):
     return default().attribute(offsets, p, c, tenant, shape, coeffs, n_tenants, outputs)
+
+
+def shape_constants_ext(shape=None):
+    return default().shape_constants_ext(shape)
+
+
+def attribute_ext(offsets, p, c, tenant, shape, coeffs, n_tenants, outputs=ALL_OUTPUTS):
+    """The extended model: coeffs [28], index (phase*2 + segment)*7 + k."""
+    return default().attribute(offsets, p, c, tenant, shape, coeffs, n_tenants, outputs, ext=True)
 
 
 def tenant_sums(tenant, share, n_tenants):

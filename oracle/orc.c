@@ -13,6 +13,7 @@
  */
 #include "orc.h"
 
+#include <stdint.h>
 #include <stdlib.h>
 
 #include <stddef.h>
@@ -232,6 +233,108 @@ int orc_attribute(int64_t nB, int64_t N, const int64_t *off, const int32_t *p,
         if (share_alt) share_alt[i] = dot5(th[ph][1 - seg], x);
         /* L_u accumulates in request order (batches in order, requests in
          * order inside a batch). */
+        if (tenant_sums) tenant_sums[tenant[i]] += f;
+      }
+    }
+  }
+  return ORC_OK;
+}
+
+int orc_shape_constants_ext(const orc_shape *sh, double S[6]) {
+  if (!S) return ORC_EINVAL;
+  double S4[4];
+  const int rc = orc_shape_constants(sh, S4);
+  if (rc != ORC_OK) return rc;
+  for (int k = 0; k < 4; ++k) S[k] = S4[k];
+  if (!sh) {
+    S[4] = S[5] = 1.0;
+    return ORC_OK;
+  }
+  const int64_t L = sh->n_layers, h = sh->hidden, hq = sh->n_q_heads, d = sh->head_dim,
+                V = sh->vocab;
+  /* S5: a processed token attending to one cached key costs, per layer and
+   * query head, a head_dim-long dot product for the score and a head_dim-long
+   * multiply-add into the output: 4*head_dim FLOPs. */
+  const int64_t s5 = 4 * L * hq * d;
+  /* S6: the logits of one position: a (vocab x hidden) matrix times a
+   * vector, 2*vocab*hidden FLOPs per request. */
+  const int64_t s6 = 2 * V * h;
+  if (s5 >= ORC_EXACT_LIMIT || s6 >= ORC_EXACT_LIMIT) return ORC_EINVAL;
+  S[4] = (double)s5;
+  S[5] = (double)s6;
+  return ORC_OK;
+}
+
+/* theta . x with the terms added in order k = 0..6. */
+static double dot7(const double th[7], const double x[7]) {
+  double acc = th[0] * x[0];
+  for (int k = 1; k < 7; ++k) acc = acc + th[k] * x[k];
+  return acc;
+}
+
+int orc_attribute_ext(int64_t nB, int64_t N, const int64_t *off, const int32_t *p,
+                      const int32_t *c, const int32_t *tenant, const orc_shape *shape,
+                      const float coeffs[28], int32_t n_tenants, double *T, double *TM,
+                      double *TC, uint8_t *phase_out, uint8_t *regime, double *share,
+                      double *share_alt, double *tenant_sums) {
+  double S[6];
+  if (!coeffs) return ORC_EINVAL;
+  if (tenant_sums && !tenant) return ORC_EINVAL;
+  int rc = orc_shape_constants_ext(shape, S);
+  if (rc != ORC_OK) return rc;
+  rc = orc_validate(nB, N, off, p, c, tenant_sums ? tenant : NULL, n_tenants);
+  if (rc != ORC_OK) return rc;
+
+  double th[2][2][7];
+  for (int ph = 0; ph < 2; ++ph)
+    for (int s = 0; s < 2; ++s)
+      for (int k = 0; k < 7; ++k) th[ph][s][k] = (double)coeffs[(ph * 2 + s) * 7 + k];
+
+  if (tenant_sums)
+    for (int32_t u = 0; u < n_tenants; ++u) tenant_sums[u] = 0.0;
+
+  for (int64_t b = 0; b < nB; ++b) {
+    const int64_t lo = off[b], hi = off[b + 1], n = hi - lo;
+    if (n == 0) {
+      if (T) T[b] = 0.0;
+      if (TM) TM[b] = 0.0;
+      if (TC) TC[b] = 0.0;
+      if (phase_out) phase_out[b] = ORC_REGIME_EMPTY;
+      if (regime) regime[b] = ORC_REGIME_EMPTY;
+      continue;
+    }
+    int64_t P, C, Q;
+    int ph;
+    batch_sums(lo, hi, p, c, &P, &C, &Q, &ph);
+    /* sum of p_i*c_i, exact: each product is below 2^51; the sum is checked
+     * against 2^63 as it grows */
+    int64_t R = 0;
+    for (int64_t i = lo; i < hi; ++i) {
+      const int64_t pc = (int64_t)p[i] * (int64_t)c[i];
+      if (R > INT64_MAX - pc) return ORC_ERANGE;
+      R += pc;
+    }
+    const double X[7] = {S[0], S[1] * (double)P, S[2] * (double)C, S[3] * (double)Q,
+                         (double)n * (double)n, S[4] * (double)R, S[5] * (double)n};
+    const double tm = dot7(th[ph][ORC_MEM], X);
+    const double tc = dot7(th[ph][ORC_COMP], X);
+    /* The segment rule of orc_attribute: compute-bound when strictly larger. */
+    const int seg = (tc > tm) ? ORC_COMP : ORC_MEM;
+    if (T) T[b] = seg == ORC_COMP ? tc : tm;
+    if (TM) TM[b] = tm;
+    if (TC) TC[b] = tc;
+    if (phase_out) phase_out[b] = (uint8_t)ph;
+    if (regime) regime[b] = (uint8_t)(2 * ph + seg);
+    if (share || share_alt || tenant_sums) {
+      for (int64_t i = lo; i < hi; ++i) {
+        const int64_t p2 = (int64_t)p[i] * (int64_t)p[i];
+        const int64_t pc = (int64_t)p[i] * (int64_t)c[i];
+        /* the request's own terms: summed over the batch they give X */
+        const double x[7] = {S[0] / (double)n, S[1] * (double)p[i], S[2] * (double)c[i],
+                             S[3] * (double)p2, (double)n, S[4] * (double)pc, S[5]};
+        const double f = dot7(th[ph][seg], x);
+        if (share) share[i] = f;
+        if (share_alt) share_alt[i] = dot7(th[ph][1 - seg], x);
         if (tenant_sums) tenant_sums[tenant[i]] += f;
       }
     }

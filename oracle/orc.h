@@ -102,6 +102,33 @@ int orc_attribute(int64_t n_batches, int64_t n_requests, const int64_t *offsets,
                   uint8_t *phase, uint8_t *regime, double *share,
                   double *share_alt, double *tenant_sums);
 
+/* Extended model (feature variants the paper leaves open; Sec. 2.1 defines
+ * Eq. 1 only).  Two more features per batch, each with its own coefficient:
+ *   a5 * S5 * sum_i p_i*c_i  attention of the processed tokens over the
+ *                            cached context (chunked prefill with a prefix);
+ *   a6 * S6 * |B|            per-request output projection (logits of one
+ *                            position per request); with the unit shape this
+ *                            is the other reading of Eq. 1's a4 term, a4*|B|
+ *                            per batch.
+ * S[0..5] = (S0, S1, S2, S3, S5, S6):
+ *   S5 = 4*L*Hq*head_dim   FLOPs per (processed token, cached key) pair
+ *   S6 = 2*vocab*hidden    output-projection FLOPs per request
+ * shape == NULL gives all ones. */
+int orc_shape_constants_ext(const orc_shape *shape, double S[6]);
+
+/* Attribution under the extended model.  coeffs[28] holds
+ * theta[phase][segment][k] at index (phase*2 + segment)*7 + k,
+ * k = (beta, a1, a2, a3, a4, a5, a6).  Per request the features are
+ *   x_i = (S0/|B|, S1*p_i, S2*c_i, S3*p_i^2, |B|, S5*p_i*c_i, S6),
+ * per batch their sums; terms are added in order k = 0..6.  Phase, segment
+ * and empty-batch rules, outputs and ownership as orc_attribute.  ORC_ERANGE
+ * also when a batch's sum of p_i*c_i reaches 2^63. */
+int orc_attribute_ext(int64_t n_batches, int64_t n_requests, const int64_t *offsets,
+                      const int32_t *p, const int32_t *c, const int32_t *tenant,
+                      const orc_shape *shape, const float coeffs[28], int32_t n_tenants,
+                      double *T, double *TM, double *TC, uint8_t *phase, uint8_t *regime,
+                      double *share, double *share_alt, double *tenant_sums);
+
 /* Exact per-batch sums of Eq. 1 and the batch phase (Sec. 2.1):
  *   sums[4][nB] = (|B|, sum p, sum c, sum p^2), zeros for an empty batch;
  *   phase[nB]   ORC_PREFILL / ORC_DECODE, 255 for an empty batch.

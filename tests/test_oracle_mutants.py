@@ -27,7 +27,7 @@ MUTANTS = [
     ("a2 sign flipped", "acc = acc + th[2] * x[2];", "acc = acc - th[2] * x[2];"),
     ("a4 batch term n not n^2", "S[3] * (double)Q, (double)n * (double)n};\n    const double tm",
      "S[3] * (double)Q, (double)n};\n    const double tm"),
-    ("tie goes to COMP", "const int seg = (tc > tm)", "const int seg = (tc >= tm)"),
+    ("tie goes to COMP", "const int seg = (tc > tm)", "const int seg = (tc >= tm)", 1),
     ("share uses other segment", "const double f = dot5(th[ph][seg], x);",
      "const double f = dot5(th[ph][1 - seg], x);"),
     ("phase rule and/or", "if (p[i] > 1 || c[i] == 0) prefill = 1;",
@@ -44,16 +44,42 @@ MUTANTS = [
      "th[ph][s][k] = (double)coeffs[(s * 2 + ph) * 5 + k];"),
     ("Q sums p not p^2", "sq += (int64_t)p[i] * (int64_t)p[i];", "sq += p[i];"),
     ("output projection twice", "wb * (L * p_layer + V * h)", "wb * (L * p_layer + 2 * V * h)"),
-    ("empty regime 0", "if (regime) regime[b] = ORC_REGIME_EMPTY;", "if (regime) regime[b] = 0;"),
+    ("empty regime 0", "if (regime) regime[b] = ORC_REGIME_EMPTY;", "if (regime) regime[b] = 0;", 1),
     ("tenant sums of other segment", "if (tenant_sums) tenant_sums[tenant[i]] += f;",
-     "if (tenant_sums) tenant_sums[tenant[i]] += dot5(th[ph][1 - seg], x);"),
+     "if (tenant_sums) tenant_sums[tenant[i]] += dot5(th[ph][1 - seg], x);", 1),
     ("per-request p^2 uses p", "x[3] = S[3] * (double)p2;", "x[3] = S[3] * (double)p;"),
     ("admission delta sign", "if (delta) *delta = T1 - T0;", "if (delta) *delta = T0 - T1;"),
     ("admission share of the first request", "if (share) *share = f1[n];",
      "if (share) *share = f1[0];"),
     ("admission drops the candidate's context", "c1[n] = cc;", "c1[n] = 0;"),
     ("admission batch not grown", "off1[2] = {0, n + 1};", "off1[2] = {0, n > 0 ? n : 1};"),
+    # the extended model (orc_attribute_ext, orc_shape_constants_ext)
+    ("ext tie goes to COMP", "const int seg = (tc > tm)", "const int seg = (tc >= tm)", 2),
+    ("ext empty regime 0", "if (regime) regime[b] = ORC_REGIME_EMPTY;",
+     "if (regime) regime[b] = 0;", 2),
+    ("ext tenant sums of other segment", "if (tenant_sums) tenant_sums[tenant[i]] += f;",
+     "if (tenant_sums) tenant_sums[tenant[i]] += dot7(th[ph][1 - seg], x);", 2),
+    ("ext cross term reads sum c", "S[4] * (double)R,", "S[4] * (double)C,"),
+    ("ext per-request term split over the batch", "S[4] * (double)pc, S[5]};",
+     "S[4] * (double)pc, S[5] / (double)n};"),
+    ("ext batch term n^2", "S[5] * (double)n};", "S[5] * (double)n * (double)n};"),
+    ("ext pair FLOPs halved", "const int64_t s5 = 4 * L * hq * d;",
+     "const int64_t s5 = 2 * L * hq * d;"),
+    ("ext logits FLOPs halved", "const int64_t s6 = 2 * V * h;", "const int64_t s6 = V * h;"),
+    ("ext coefficient stride 5", "(double)coeffs[(ph * 2 + s) * 7 + k];",
+     "(double)coeffs[(ph * 2 + s) * 5 + k];"),
+    ("ext last term dropped", "for (int k = 1; k < 7; ++k)", "for (int k = 1; k < 6; ++k)"),
 ]
+EXT = json.load(open(os.path.join(ROOT, "tests", "golden", "ext_examples.json")))
+EXT_SETS = ("prefill_mem", "prefill_comp", "decode_mem", "decode_comp")
+
+
+def ext_coeffs(sets):
+    th = np.zeros(28, np.float32)
+    for g, name in enumerate(EXT_SETS):
+        if name in sets:
+            th[g * 7:(g + 1) * 7] = sets[name]
+    return th
 
 
 def coeff_vec(d):
@@ -104,6 +130,37 @@ def battery(orc: oracle.Oracle):
     pairs2 = 3  # (q0,k0), (q1,k0), (q1,k1)
     per_pair = sh["n_layers"] * sh["n_q_heads"] * 4 * sh["head_dim"]
     assert S[3] == (pairs2 * per_pair - 2 * 1 * per_pair) / 2
+    # extended model: hand-worked batches, constants, and Eq. 1 when a5 = a6 = 0
+    for ex in EXT["unit_shape_examples"]:
+        off = np.array([0, len(ex["p"])], np.int64)
+        r = orc.attribute(off, ex["p"], ex["c"], None, None, ext_coeffs(ex["sets"]), 0,
+                          ("T", "regime", "share"), ext=True)
+        assert r["T"][0] == ex["T"] and r["regime"][0] == ex["regime"]
+        assert list(r["share"]) == ex["shares"]
+    xs = EXT["shaped"]
+    assert list(orc.shape_constants_ext(xs["shape"])) == xs["S"]
+    for ex in xs["examples"]:
+        off = np.array([0, len(ex["p"])], np.int64)
+        r = orc.attribute(off, ex["p"], ex["c"], None, xs["shape"], ext_coeffs(xs["sets"]), 0,
+                          ("T", "regime", "share"), ext=True)
+        assert r["T"][0] == ex["T"] and list(r["share"]) == ex["shares"]
+    Sx = orc.shape_constants_ext(sh)
+    assert Sx[4] == EXT["llama3_1_8b"]["S5"] and Sx[5] == EXT["llama3_1_8b"]["S6"]
+    tr = tracegen.config_trace("tiny-mixed")
+    co = tracegen.config_coeffs("tiny-mixed")
+    wide = np.zeros(28, np.float32)
+    for g in range(4):
+        wide[g * 7:g * 7 + 5] = co[g * 5:(g + 1) * 5]
+    outs = ("T", "regime", "share", "tenant_sums")
+    a = orc.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co, tr.n_tenants, outs)
+    b = orc.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, wide, tr.n_tenants, outs,
+                      ext=True)
+    for k in outs:
+        assert np.array_equal(a[k], b[k]), k
+    # an empty batch inside a trace: regime 255 under both models
+    tr = tracegen.from_batches([([2], [0]), ([], []), ([1], [3])], None, 1)
+    r = orc.attribute(tr.offsets, tr.p, tr.c, None, None, wide, 0, ("T", "regime"), ext=True)
+    assert r["regime"][1] == 255 and r["T"][1] == 0.0
 
 
 def _build(tmp_path, text, tag):
@@ -119,10 +176,25 @@ def test_battery_passes_on_real_source(tmp_path):
     battery(_build(tmp_path, open(SRC).read(), "orig"))
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_mutant_is_caught(tmp_path, name, old, new):
+def mutate(text, old, new, occurrence):
+    """text with the given occurrence (1-based) of old replaced; occurrence 0
+    asks for a unique anchor."""
+    n = text.count(old)
+    if occurrence == 0:
+        assert n == 1, f"mutation anchor must be unique ({n} found)"
+        return text.replace(old, new)
+    assert n >= occurrence, f"anchor has {n} occurrences"
+    at = -1
+    for _ in range(occurrence):
+        at = text.index(old, at + 1)
+    return text[:at] + new + text[at + len(old):]
+
+
+@pytest.mark.parametrize("mut", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, mut):
+    name, old, new = mut[:3]
+    occurrence = mut[3] if len(mut) > 3 else 0
     text = open(SRC).read()
-    assert text.count(old) == 1, f"mutation anchor for '{name}' must be unique"
-    orc = _build(tmp_path, text.replace(old, new), "mut")
+    orc = _build(tmp_path, mutate(text, old, new, occurrence), "mut")
     with pytest.raises((AssertionError, oracle.OracleError)):
         battery(orc)
