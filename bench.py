@@ -317,6 +317,69 @@ def bench_fit(hip, stream, dt, tr, lat, with_oracle):
     return res
 
 
+def bench_ext(hip, stream, dt, tr, bufs, ws, steps, with_oracle):
+    """The extended model (Eq. 1 plus the cross term sum p*c and the
+    per-request term) on the same trace and outputs: llmv_attribute_ext
+    steps between HIP events, the tile kernel on its own, and the oracle's
+    extended model on sampled batches and every tenant."""
+    import numpy as np
+    import torch
+    import tracegen
+    from paper_2608_08382_amd import llmv
+
+    lat, reg, share, tsum = bufs
+    co = tracegen.ext_coeffs(100 + tracegen.CONFIG_SEED.get(tr.name, 0))
+
+    def step():
+        llmv.llmv_attribute_ext(dt, tr.shape, co, lat, reg, share, tr.n_tenants, tsum, ws)
+
+    step()
+    torch.cuda.synchronize()
+    evs = [(hip.create(), hip.create()) for _ in range(steps)]
+    start, stop = hip.create(), hip.create()
+    hip.record(start, stream)
+    for i in range(steps):
+        llmv.llmv_set_kernel_events(*evs[i])
+        step()
+    llmv.llmv_set_kernel_events(None, None)
+    hip.record(stop, stream)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(start, stop) / steps
+    k_ms = sum(hip.elapsed_ms(a, b) for a, b in evs) / steps
+    nbytes = algorithmic_bytes(tr.n_requests, tr.n_batches)
+    gbps = nbytes / (k_ms / 1e3) / 1e9
+    res = {"metric": "attributed requests/sec, extended model", "value": tr.n_requests / (ms / 1e3),
+           "unit": "requests/s", "ms_per_step": ms, "kernel_ms": k_ms, "achieved_gbps": gbps,
+           "frac": gbps / PEAK_HBM_GBPS, "steps": steps}
+    log(f"[bench] extended model: {ms:.4f} ms/step, tile kernel {k_ms:.4f} ms, {gbps:.0f} GB/s")
+    if with_oracle:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import parity
+        t0 = time.perf_counter()
+        ref_all = oracle.attribute_ext(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co,
+                                       tr.n_tenants, ("T", "TM", "TC", "phase", "regime",
+                                                      "tenant_sums"))
+        dt_o = time.perf_counter() - t0
+        st = parity.compare(ref_all, tr.offsets, lat.cpu().numpy(), reg.cpu().numpy(), None,
+                            tsum.cpu().numpy())
+        rng = np.random.default_rng(23)
+        bids = np.unique(rng.integers(0, tr.n_batches, 500))
+        off, p, c, t = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
+        ref = oracle.attribute_ext(off, p, c, t, tr.shape, co, tr.n_tenants,
+                                   ("T", "TM", "TC", "phase", "regime", "share", "share_alt"))
+        idx = np.concatenate([np.arange(tr.offsets[b], tr.offsets[b + 1]) for b in bids])
+        g_share = np.zeros(tr.n_requests, np.float32)
+        g_share[idx] = share[torch.from_numpy(idx).to(share.device)].cpu().numpy()
+        st["sampled"] = parity.compare(ref, tr.offsets, lat.cpu().numpy(), reg.cpu().numpy(),
+                                       g_share, None, batch_ids=bids)
+        res["cpu_baseline"] = {"value": tr.n_requests / dt_o, "unit": "requests/s", "cores": 1,
+                               "kind": "oracle", "sample": "full trace, batch outputs and "
+                                                           "tenant sums"}
+        res["parity"] = st
+    return res
+
+
 def tracegen_single_batch(n):
     """One decode batch of n requests (context U[128, 8192]), 16 tenants."""
     import numpy as np
@@ -339,6 +402,8 @@ def main():
                     help="also time the step with subsets of the outputs (stderr)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the what-if sweep measurement (4 shapes x 256 coefficient vectors)")
+    ap.add_argument("--no-ext", action="store_true",
+                    help="skip the extended-model measurement")
     ap.add_argument("--no-fit", action="store_true",
                     help="skip the fitting and metrics measurement")
     ap.add_argument("--no-admission", action="store_true",
@@ -471,6 +536,11 @@ def main():
         result["cpu_baseline"] = cb
         result["parity"] = {k: v for k, v in stats.items()}
         log(f"[bench] oracle {cb['value']:.3e} req/s on {cb['cores']} core; parity {stats}")
+    if not args.no_ext:
+        result["extended_model"] = bench_ext(hip, stream, dt, tr, (lat, reg, share, tsum), ws,
+                                             max(5, args.steps // 2), not args.no_cpu_baseline)
+        step()  # the Eq. 1 outputs again, for the blocks below
+        torch.cuda.synchronize()
     if not args.no_admission:
         del share
         torch.cuda.empty_cache()

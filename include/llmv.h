@@ -128,6 +128,37 @@ int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
                    float *share, int32_t n_tenants, double *tenant_sums,
                    void *ws, size_t ws_bytes, void *stream);
 
+/* Extended model (feature variants the paper leaves open; Sec. 2.1 defines
+ * Eq. 1 only).  Two more features per batch, each with its own coefficient
+ * in every (phase, segment) set:
+ *   a5 * S5 * sum_i p_i*c_i   the processed tokens attending to the cached
+ *                             context (a prefill chunk with a prefix);
+ *   a6 * S6 * |B|             a per-request term: one position's logits
+ *                             (with the unit shape, the other reading of
+ *                             Eq. 1's a4 term, a4*|B| per batch).
+ * Per request the features are
+ *   x_i = (S0/|B|, S1*p_i, S2*c_i, S3*p_i^2, |B|, S5*p_i*c_i, S6),
+ * so shares stay additive.  Phase, segment and empty-batch rules are those
+ * of llmv_attribute. */
+
+/* Host only.  S[0..3] as llmv_shape_constants; S[4] = S5 =
+ * 4*L*Hq*head_dim (FLOPs per processed token and cached key: score and
+ * value mix, every layer and query head), S[5] = S6 = 2*vocab*hidden
+ * (output-projection FLOPs per request).  shape == NULL gives all ones. */
+int llmv_shape_constants_ext(const llmv_shape *shape, double S[6]);
+
+/* llmv_attribute under the extended model.
+ *   coeffs  host, 28 finite fp32: theta[phase][segment][k] at index
+ *           (phase*2 + segment)*7 + k, k = (beta, a1, a2, a3, a4, a5, a6).
+ * Other arguments, outputs, precision and workspace as llmv_attribute.  The
+ * batch sum of p_i*c_i is exact in uint64 and must stay below 2^63 (not
+ * checked).  With a5 = a6 = 0 in every set the results are bit-identical
+ * to llmv_attribute with the first five coefficients of each set. */
+int llmv_attribute_ext(const llmv_trace *trace, const llmv_shape *shape,
+                       const float coeffs[28], float *latency, uint8_t *regime,
+                       float *share, int32_t n_tenants, double *tenant_sums,
+                       void *ws, size_t ws_bytes, void *stream);
+
 /* What-if sweep (Sec. 1: fast "what-if" planning over alternative model
  * and coefficient settings; Eq. 1 and Sec. 2 Problem formulation for each):
  * the tenant sums of one trace under every pair (shape s, coefficient vector

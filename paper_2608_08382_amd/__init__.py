@@ -4,9 +4,10 @@ The computation lives in libllmv.so (HIP kernels for gfx950, C ABI in
 include/llmv.h); ``llmv`` is its ctypes binding.
 """
 from . import llmv  # noqa: F401
-from .llmv import (DeviceTrace, LlmvError, admit, attribute, attribute_sweep,  # noqa: F401
-                   batch_sums, features, fit, fit_metrics, fit_workspace, llmv_admit,
-                   llmv_attribute, llmv_attribute_sweep, llmv_batch_sums, llmv_features,
+from .llmv import (DeviceTrace, LlmvError, admit, attribute, attribute_ext,  # noqa: F401
+                   attribute_sweep, batch_sums, features, fit, fit_metrics, fit_workspace, llmv_admit,
+                   llmv_attribute, llmv_attribute_ext, llmv_attribute_sweep, llmv_batch_sums,
+                   llmv_features, llmv_shape_constants_ext,
                    llmv_fit, llmv_fit_metrics, llmv_fit_workspace_size, llmv_last_error,
                    llmv_shape_constants, llmv_tenant_sums, llmv_validate, llmv_workspace_size,
                    tenant_sums, workspace)

@@ -169,9 +169,27 @@ TileKernel pick_tiles(int mode, int hist, bool share) {
   return share ? k_tiles<MODE_ATTR, HIST_GLOBAL, true, 1> : k_tiles<MODE_ATTR, HIST_GLOBAL, false, 1>;
 }
 
+// The tile kernel for a mode and its second argument's type.
+template <typename VT> struct TilePick;
+template <> struct TilePick<NoVars> {
+  static TileKernel get(int mode, int hist, bool share) { return pick_tiles(mode, hist, share); }
+};
+template <> struct TilePick<ExtModel> {
+  typedef void (*K)(const Params, const ExtModel);
+  static K get(int, int hist, bool share) {
+    if (hist == HIST_NONE)
+      return share ? k_tiles<MODE_EXT, HIST_NONE, true, 1> : k_tiles<MODE_EXT, HIST_NONE, false, 1>;
+    if (hist == HIST_LDS)
+      return share ? k_tiles<MODE_EXT, HIST_LDS, true, 1> : k_tiles<MODE_EXT, HIST_LDS, false, 1>;
+    return share ? k_tiles<MODE_EXT, HIST_GLOBAL, true, 1> : k_tiles<MODE_EXT, HIST_GLOBAL, false, 1>;
+  }
+};
+
 // Partition + tiles (+ tenant reduction) shared by attribute and features.
-int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_tenant,
-              bool want_share, void* ws, size_t ws_bytes, hipStream_t stream) {
+// V: the kernel's second argument (the extended model, or nothing).
+template <typename VT>
+int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
+              bool want_tenant, bool want_share, void* ws, size_t ws_bytes, hipStream_t stream) {
   int cus = 0;
   int rc = device_cus(&cus);
   if (rc) return rc;
@@ -182,7 +200,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
   const int rep = hist == HIST_LDS ? hist_replicas(T) : 1;
   const size_t dyn = hist == HIST_LDS ? (size_t)rep * (size_t)T * sizeof(double) : 0;
-  const TileKernel kern = pick_tiles(mode, hist, want_share);
+  const auto kern = TilePick<VT>::get(mode, hist, want_share);
   P.hist_rep = rep;
 
   if (tr->n_requests <= kSmallN && hist != HIST_GLOBAL) {
@@ -195,7 +213,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
     P.claims = nullptr;
     P.partials = hist == HIST_LDS ? P.tenant_sums : nullptr;
     if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
-    hipLaunchKernelGGL(kern, dim3(1), dim3(kWG), dyn, stream, P, NoVars{});
+    hipLaunchKernelGGL(kern, dim3(1), dim3(kWG), dyn, stream, P, V);
     HIP_TRY(hipGetLastError(), "k_tiles launch");
     if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
     return LLMV_OK;
@@ -223,7 +241,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
   }
 
   if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, stream, P, NoVars{});
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, stream, P, V);
   HIP_TRY(hipGetLastError(), "k_tiles launch");
   if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
 
@@ -232,6 +250,36 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, int32_t T, bool want_te
                        (const double*)P.partials, (int)grid, (int)T, P.tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
   }
+  return LLMV_OK;
+}
+
+// Checks and kernel parameters shared by llmv_attribute (20 coefficients)
+// and llmv_attribute_ext (28).
+int attribute_params(const llmv_trace* trace, const llmv_shape* shape, const float* coeffs,
+                     int n_coeffs, float* latency, uint8_t* regime, float* share,
+                     int32_t n_tenants, double* tenant_sums, Params& P) {
+  const bool want_tenant = tenant_sums != nullptr;
+  int rc = check_trace(trace, want_tenant);
+  if (rc) return rc;
+  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
+  for (int i = 0; i < n_coeffs; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
+  if (want_tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
+  if (share && ((uintptr_t)share & 15u)) return fail(LLMV_EINVAL, "share must be 16-byte aligned");
+  rc = shape_constants(shape, P.S);
+  if (rc) return rc;
+  P.off = trace->offsets;
+  P.p = trace->p;
+  P.c = trace->c;
+  P.tenant = want_tenant ? trace->tenant : nullptr;
+  P.nB = trace->n_batches;
+  P.N = trace->n_requests;
+  P.latency = latency;
+  P.regime = regime;
+  P.share = share;
+  P.tenant_sums = tenant_sums;
+  P.n_tenants = want_tenant ? n_tenants : 0;
   return LLMV_OK;
 }
 
@@ -263,33 +311,38 @@ size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tena
 int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[20],
                    float* latency, uint8_t* regime, float* share, int32_t n_tenants,
                    double* tenant_sums, void* ws, size_t ws_bytes, void* stream) {
-  const bool want_tenant = tenant_sums != nullptr;
-  int rc = check_trace(trace, want_tenant);
-  if (rc) return rc;
-  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
-  for (int i = 0; i < 20; ++i)
-    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
-  if (want_tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
-    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
-  if (share && ((uintptr_t)share & 15u)) return fail(LLMV_EINVAL, "share must be 16-byte aligned");
   Params P{};
-  rc = shape_constants(shape, P.S);
+  int rc = attribute_params(trace, shape, coeffs, 20, latency, regime, share, n_tenants,
+                            tenant_sums, P);
   if (rc) return rc;
   for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[i];
-  P.off = trace->offsets;
-  P.p = trace->p;
-  P.c = trace->c;
-  P.tenant = want_tenant ? trace->tenant : nullptr;
-  P.nB = trace->n_batches;
-  P.N = trace->n_requests;
-  P.latency = latency;
-  P.regime = regime;
-  P.share = share;
-  P.tenant_sums = tenant_sums;
-  P.n_tenants = want_tenant ? n_tenants : 0;
-  if (!latency && !regime && !share && !want_tenant) return LLMV_OK;  // nothing requested
-  return run_tiles(MODE_ATTR, trace, P, n_tenants, want_tenant, share != nullptr, ws, ws_bytes,
-                   (hipStream_t)stream);
+  if (!latency && !regime && !share && !tenant_sums) return LLMV_OK;  // nothing requested
+  return run_tiles(MODE_ATTR, trace, P, NoVars{}, n_tenants, tenant_sums != nullptr,
+                   share != nullptr, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int llmv_shape_constants_ext(const llmv_shape* shape, double S[6]) {
+  if (!S) return fail(LLMV_EINVAL, "S is NULL");
+  return shape_constants_ext(shape, S);
+}
+
+int llmv_attribute_ext(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[28],
+                       float* latency, uint8_t* regime, float* share, int32_t n_tenants,
+                       double* tenant_sums, void* ws, size_t ws_bytes, void* stream) {
+  Params P{};
+  int rc = attribute_params(trace, shape, coeffs, 28, latency, regime, share, n_tenants,
+                            tenant_sums, P);
+  if (rc) return rc;
+  double S[6];
+  rc = shape_constants_ext(shape, S);
+  if (rc) return rc;
+  ExtModel E{};
+  E.S5 = S[4];
+  E.S6 = S[5];
+  for (int i = 0; i < 28; ++i) E.th[i] = (double)coeffs[i];
+  if (!latency && !regime && !share && !tenant_sums) return LLMV_OK;  // nothing requested
+  return run_tiles(MODE_EXT, trace, P, E, n_tenants, tenant_sums != nullptr, share != nullptr,
+                   ws, ws_bytes, (hipStream_t)stream);
 }
 
 int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shapes,
@@ -400,7 +453,8 @@ int llmv_batch_sums(const llmv_trace* trace, int64_t* sums, uint8_t* phase, void
   P.bsums = sums;
   P.bphase = phase;
   if (!sums && !phase) return LLMV_OK;
-  return run_tiles(MODE_FEAT, trace, P, 0, false, false, ws, ws_bytes, (hipStream_t)stream);
+  return run_tiles(MODE_FEAT, trace, P, NoVars{}, 0, false, false, ws, ws_bytes,
+                   (hipStream_t)stream);
 }
 
 int llmv_admit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
@@ -445,7 +499,8 @@ int llmv_features(const llmv_trace* trace, const llmv_shape* shape, float* x_req
   P.x_req = x_req;
   P.x_batch = x_batch;
   if (!x_req && !x_batch) return LLMV_OK;
-  return run_tiles(MODE_FEAT, trace, P, 0, false, false, ws, ws_bytes, (hipStream_t)stream);
+  return run_tiles(MODE_FEAT, trace, P, NoVars{}, 0, false, false, ws, ws_bytes,
+                   (hipStream_t)stream);
 }
 
 int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32_t n_tenants,

@@ -89,6 +89,26 @@ inline int shape_constants(const llmv_shape* sh, double S[4]) {
   return LLMV_OK;
 }
 
+// Constants of the extended model's two extra features: S[0..3] as
+// shape_constants, S[4] = 4*L*Hq*head_dim (FLOPs per processed token and
+// cached key), S[5] = 2*vocab*hidden (output-projection FLOPs per request);
+// all ones for the unit shape.
+inline int shape_constants_ext(const llmv_shape* sh, double S[6]) {
+  int rc = shape_constants(sh, S);
+  if (rc) return rc;
+  if (!sh) {
+    S[4] = S[5] = 1.0;
+    return LLMV_OK;
+  }
+  const int64_t s5 = 4 * (int64_t)sh->n_layers * sh->n_q_heads * sh->head_dim;
+  const int64_t s6 = 2 * (int64_t)sh->vocab * sh->hidden;
+  const int64_t lim = (int64_t)1 << 53;
+  if (s5 >= lim || s6 >= lim) return fail(LLMV_EINVAL, "shape constants exceed 2^53");
+  S[4] = (double)s5;
+  S[5] = (double)s6;
+  return LLMV_OK;
+}
+
 inline int check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (need == 0) return LLMV_OK;
   if (!ws) return fail(LLMV_EWORKSPACE, "workspace is NULL (%zu bytes needed)", need);

@@ -66,8 +66,11 @@ struct ChunkMap {
 
 // MODE_ATTR: latency, regime, share, tenant sums of one (shape, theta).
 // MODE_FEAT: the feature rows.  MODE_SWEEP: tenant sums of up to kSweepG
-// variants (shape, theta) per pass over the trace.
-enum { MODE_ATTR = 0, MODE_FEAT = 1, MODE_SWEEP = 2 };
+// variants (shape, theta) per pass over the trace.  MODE_EXT: the outputs
+// of MODE_ATTR under the extended model (Eq. 1 plus a cross term
+// a5*S5*sum p*c and a per-request term a6*S6*|B|).
+enum { MODE_ATTR = 0, MODE_FEAT = 1, MODE_SWEEP = 2, MODE_EXT = 3 };
+template <int MODE> constexpr bool kAttrMode = MODE == MODE_ATTR || MODE == MODE_EXT;
 
 // Native vectors: 16-byte global loads / stores (dwordx4).
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
@@ -122,8 +125,15 @@ struct VarTable {
   float K[kSweepG][4][4];   // [variant][regime][k1, k2, k3, unused]
 };
 struct NoVars {};
+// The extended model of a MODE_EXT launch: the two extra shape constants
+// and the coefficients theta[phase][segment][k], k = 0..6 (beta, a1..a6).
+struct ExtModel {
+  double S5, S6;
+  double th[28];
+};
 template <int MODE> struct VarsOf { using type = NoVars; };
 template <> struct VarsOf<MODE_SWEEP> { using type = VarTable; };
+template <> struct VarsOf<MODE_EXT> { using type = ExtModel; };
 
 // ---------------------------------------------------------------- wave ops
 
@@ -219,6 +229,40 @@ __device__ __forceinline__ void batch_model(const Params& P, int64_t bg, int64_t
   k[3] = th[3] * P.S[3];
 }
 
+// Eq. 1 plus the two extra terms, added in order k = 0..6.
+__device__ __forceinline__ double eq7(const double* th, const double X[7]) {
+  double acc = th[0] * X[0];
+#pragma unroll
+  for (int k = 1; k < 7; ++k) acc = acc + th[k] * X[k];
+  return acc;
+}
+
+// batch_model under the extended model: Rsum = sum p*c.  The share
+// constants gain k0 += theta_a6*S6 and k4 = theta_a5*S5 (the coefficient of
+// p*c):  share_i = k0 + k1*p_i + k2*c_i + k3*p_i^2 + k4*p_i*c_i.
+__device__ __forceinline__ void ext_model(const Params& P, const ExtModel& E, int64_t bg,
+                                          int64_t n, uint64_t Psum, uint64_t Csum, uint64_t Qsum,
+                                          uint64_t Rsum, bool prefill, double* k, double* k4) {
+  const double X[7] = {P.S[0], P.S[1] * (double)Psum, P.S[2] * (double)Csum,
+                       P.S[3] * (double)Qsum, (double)n * (double)n, E.S5 * (double)Rsum,
+                       E.S6 * (double)n};
+  const int phase = prefill ? 0 : 1;
+  const double* thm = E.th + (phase * 2 + 0) * 7;
+  const double* thc = E.th + (phase * 2 + 1) * 7;
+  const double tm = eq7(thm, X);
+  const double tc = eq7(thc, X);
+  // Roofline max of the two segments; ties stay memory-bound.
+  const int seg = (tc > tm) ? 1 : 0;
+  if (P.latency) P.latency[bg] = (float)(seg ? tc : tm);
+  if (P.regime) P.regime[bg] = (uint8_t)(2 * phase + seg);
+  const double* th = seg ? thc : thm;
+  k[0] = th[0] * (P.S[0] / (double)n) + th[4] * (double)n + th[6] * E.S6;
+  k[1] = th[1] * P.S[1];
+  k[2] = th[2] * P.S[2];
+  k[3] = th[3] * P.S[3];
+  *k4 = th[5] * E.S5;
+}
+
 // Share constants of one batch under variant g of a sweep (the same
 // arithmetic as batch_model in MODE_ATTR, without batch outputs).
 __device__ __forceinline__ void sweep_model(const VarTable& V, int g, int64_t n, uint64_t Psum,
@@ -283,8 +327,9 @@ __device__ __forceinline__ void empty_batch(const Params& P, int64_t bg) {
 }
 
 // Per-request epilogue: the share (+ tenant histogram) or the feature row.
-// Shares: k0 + k1*p + k2*c + k3*p^2 in fp32 from the batch's constants
-// (themselves evaluated in fp64), relative error a few fp32 ulp.
+// Shares: k0 + k1*p + k2*c + k3*p^2 (+ k4*p*c under the extended model, k[4])
+// in fp32 from the batch's constants (themselves evaluated in fp64),
+// relative error a few fp32 ulp.
 template <int MODE, int HIST, bool SHARE>
 __device__ __forceinline__ float request_out(const Params& P, const float* k, const double* kd,
                                              int32_t p, int32_t c, double* s_hist, int32_t t,
@@ -301,7 +346,8 @@ __device__ __forceinline__ float request_out(const Params& P, const float* k, co
     }
     return 0.0f;
   }
-  const float s = share_of(k, p, c);
+  float s = share_of(k, p, c);
+  if constexpr (MODE == MODE_EXT) s = fmaf(k[4], (float)p * (float)c, s);
   if (HIST == HIST_LDS) atomicAdd(s_hist + t, (double)s);
   if (HIST == HIST_GLOBAL) unsafeAtomicAdd(P.tenant_sums + t, (double)s);
   return s;
@@ -465,10 +511,11 @@ __device__ __forceinline__ void store_round(const Params& P, float* stage, int64
 // whole wave (the second pass mostly hits in L2).
 template <int MODE, int HIST, bool SHARE, int NV>
 __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V, WaveLds& W,
-                          float* stage, int64_t bg, int64_t rs, int64_t re, double* s_hist) {
+                          double* wk4, float* stage, int64_t bg, int64_t rs, int64_t re,
+                          double* s_hist) {
   const int lane = threadIdx.x & 63;
   const int64_t ra = rs & ~(int64_t)3;
-  uint64_t sp = 0, scz = 0, sq = 0;
+  uint64_t sp = 0, scz = 0, sq = 0, sr = 0;
   int32_t pv[kVec], cv[kVec], tv[kVec];
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
@@ -480,12 +527,14 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
         sp += p;
         scz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
         sq += (uint64_t)p * p;
+        if constexpr (MODE == MODE_EXT) sr += (uint64_t)p * c;
       }
     }
   }
   sp = wave_sum(sp);
   scz = wave_sum(scz);
   sq = wave_sum(sq);
+  if constexpr (MODE == MODE_EXT) sr = wave_sum(sr);
   const int64_t n = re - rs;
   if constexpr (MODE == MODE_SWEEP) {
     // every lane holds the sums: per variant, the constants and one pass
@@ -508,11 +557,15 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
   }
   if (lane == 0) {
     const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
-    batch_model<MODE>(P, bg, n, sp, scz & kCMask, sq, prefill, W.k[0]);
+    if constexpr (MODE == MODE_EXT)
+      ext_model(P, V, bg, n, sp, scz & kCMask, sq, sr, prefill, W.k[0], wk4);
+    else
+      batch_model<MODE>(P, bg, n, sp, scz & kCMask, sq, prefill, W.k[0]);
   }
   wave_lds_sync();
   const double kd[4] = {W.k[0][0], W.k[0][1], W.k[0][2], W.k[0][3]};
-  const float k[4] = {(float)kd[0], (float)kd[1], (float)kd[2], (float)kd[3]};
+  const float k[5] = {(float)kd[0], (float)kd[1], (float)kd[2], (float)kd[3],
+                      MODE == MODE_EXT ? (float)wk4[0] : 0.0f};
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
     load_slots<HIST != HIST_NONE>(P, x, pv, cv, tv);
@@ -526,10 +579,10 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
         if (x + q >= rs && x + q < re)
           sv[qq] = request_out<MODE, HIST, SHARE>(P, k, kd, pv[q], cv[q], s_hist, tv[q], x + q);
       }
-      if (MODE == MODE_ATTR && SHARE)
+      if (kAttrMode<MODE> && SHARE)
         *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
     }
-    if (MODE == MODE_ATTR && SHARE)
+    if (kAttrMode<MODE> && SHARE)
       store_round(P, stage, ra, (int32_t)(base - ra), (int32_t)(rs - ra), (int32_t)(re - ra));
   }
   wave_lds_sync();
@@ -551,13 +604,19 @@ template <int MODE, int HIST, bool SHARE, int NV>
 __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename VarsOf<MODE>::type V) {
   extern __shared__ double s_hist[];  // [variants][n_tenants] when HIST_LDS
   __shared__ WaveLds s_wave[kWaves];
-  constexpr bool STAGE = MODE == MODE_ATTR && SHARE;
+  constexpr bool STAGE = kAttrMode<MODE> && SHARE;
+  constexpr bool EXT = MODE == MODE_EXT;
+  // extended model, per wave: sum p*c and the share constant k4 of each batch
+  __shared__ uint64_t s_rsum[EXT ? kWaves * kTileBatches : 1];
+  __shared__ double s_k4[EXT ? kWaves * kTileBatches : 1];
   __shared__ float s_stage[STAGE ? kWaves * 64 * kStagePitch : 1];  // shares, per wave
   constexpr bool TEN = HIST != HIST_NONE;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   WaveLds& W = s_wave[tid >> 6];
+  uint64_t* W_r = s_rsum + (EXT ? (tid >> 6) * kTileBatches : 0);
+  double* W_k4 = s_k4 + (EXT ? (tid >> 6) * kTileBatches : 0);
   float* stage = s_stage + (STAGE ? (tid >> 6) * 64 * kStagePitch : 0);
   const int32_t x0 = lane * kVec;  // first slot of this lane in a round
   const int32_t n_hist = hist_len<MODE, NV>(P);
@@ -613,7 +672,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
       }
 
       if (count == 0) {
-        big_batch<MODE, HIST, SHARE, NV>(P, V, W, stage, b, r0, r1,
+        big_batch<MODE, HIST, SHARE, NV>(P, V, W, W_k4, stage, b, r0, r1,
                                          MODE == MODE_SWEEP ? s_hist : s_hist_lane);
       } else {
         const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
@@ -638,6 +697,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
         // ---- batch-start bitmask, accumulators
         if (lane < kTileMaskWords + 2) W.mask[lane] = 0u;
         if (lane < count) W.acc[lane] = BatchAcc{0, 0, 0};
+        if (EXT && lane < count) W_r[lane] = 0ull;
         wave_lds_sync();
         if (ne) atomicOr(&W.mask[lo >> 5], 1u << (lo & 31));
         wave_lds_sync();
@@ -667,7 +727,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
           const uint32_t ends =
               ((bits[r] >> 1) | (1u << (kVec - 1)) | (valid[r] & ~(valid[r] >> 1))) & valid[r];
           uint32_t rp = 0;
-          uint64_t rcz = 0, rq = 0;
+          uint64_t rcz = 0, rq = 0, rr = 0;
 #pragma unroll
           for (int q = 0; q < kVec; ++q) {
             if ((valid[r] >> q) & 1u) {
@@ -675,14 +735,17 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
               rp += p;
               rcz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
               rq += (uint64_t)p * p;
+              if constexpr (EXT) rr += (uint64_t)p * c;
               if ((ends >> q) & 1u) {
                 const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
                 atomicAdd((unsigned long long*)&W.acc[k].p, (unsigned long long)rp);
                 atomicAdd((unsigned long long*)&W.acc[k].cz, (unsigned long long)rcz);
                 atomicAdd((unsigned long long*)&W.acc[k].q, (unsigned long long)rq);
+                if constexpr (EXT) atomicAdd((unsigned long long*)&W_r[k], (unsigned long long)rr);
                 rp = 0;
                 rcz = 0;
                 rq = 0;
+                rr = 0;
               }
             }
           }
@@ -754,7 +817,10 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
               const int64_t n = (int64_t)lo_next - lo;
               // decode iff every request processes one token over a nonzero context
               const bool prefill = (a.p != (uint64_t)n) || ((a.cz >> 48) != 0);
-              batch_model<MODE>(P, bg, n, a.p, a.cz & kCMask, a.q, prefill, W.k[k]);
+              if constexpr (EXT)
+                ext_model(P, V, bg, n, a.p, a.cz & kCMask, a.q, W_r[k], prefill, W.k[k], &W_k4[k]);
+              else
+                batch_model<MODE>(P, bg, n, a.p, a.cz & kCMask, a.q, prefill, W.k[k]);
             }
           }
           wave_lds_sync();
@@ -765,7 +831,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
             if (r * kRoundSlots >= L) break;  // wave-uniform
             const int64_t pos = ra + r * kRoundSlots + x0;
             uint32_t kcur = 0xffffffffu;
-            float kk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            float kk[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
             double kd[4] = {0.0, 0.0, 0.0, 0.0};
   #pragma unroll
             for (int g = 0; g < kVec / 4; ++g) {
@@ -780,15 +846,16 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
                     kcur = k;
                     kd[0] = W.k[k][0]; kd[1] = W.k[k][1]; kd[2] = W.k[k][2]; kd[3] = W.k[k][3];
                     kk[0] = (float)kd[0]; kk[1] = (float)kd[1]; kk[2] = (float)kd[2]; kk[3] = (float)kd[3];
+                    if constexpr (EXT) kk[4] = (float)W_k4[k];
                   }
                   sv[qq] = request_out<MODE, HIST, SHARE>(P, kk, kd, pv[r][q], cv[r][q], s_hist_lane,
                                                           tv[r][q], pos + q);
                 }
               }
-              if (MODE == MODE_ATTR && SHARE)
+              if (kAttrMode<MODE> && SHARE)
                 *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
             }
-            if (MODE == MODE_ATTR && SHARE) store_round(P, stage, ra, r * kRoundSlots, xf, L);
+            if (kAttrMode<MODE> && SHARE) store_round(P, stage, ra, r * kRoundSlots, xf, L);
           }
         }
         wave_lds_sync();

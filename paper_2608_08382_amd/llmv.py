@@ -27,7 +27,8 @@ LLMV_TENANTS_MAX = 1 << 24
 EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute",
            "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
            "llmv_batch_sums", "llmv_admit", "llmv_fit_workspace_size", "llmv_fit",
-           "llmv_fit_metrics", "llmv_last_error", "llmv_set_kernel_events")
+           "llmv_fit_metrics", "llmv_shape_constants_ext", "llmv_attribute_ext",
+           "llmv_last_error", "llmv_set_kernel_events")
 
 
 class LlmvError(RuntimeError):
@@ -72,6 +73,8 @@ def load(path: str = LIB_PATH):
             lib.llmv_batch_sums.argtypes = [P, P, P, P, sz, P]
             lib.llmv_admit.argtypes = [P, P, i64, P, P, P, P, P, i64, P, P, P, P, P]
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
+            lib.llmv_shape_constants_ext.argtypes = [P, P]
+            lib.llmv_attribute_ext.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
             lib.llmv_fit_workspace_size.argtypes = [i64]
             lib.llmv_fit_workspace_size.restype = sz
             lib.llmv_fit.argtypes = [P, P, i64, P, P, P, i32, P, P, P, sz, P]
@@ -82,7 +85,8 @@ def load(path: str = LIB_PATH):
             lib.llmv_set_kernel_events.restype = ctypes.c_int
             for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
                       "llmv_features", "llmv_tenant_sums", "llmv_validate", "llmv_batch_sums",
-                      "llmv_admit", "llmv_fit", "llmv_fit_metrics"):
+                      "llmv_admit", "llmv_fit", "llmv_fit_metrics", "llmv_shape_constants_ext",
+                      "llmv_attribute_ext"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -204,6 +208,33 @@ def llmv_admit(sums, phase, n_batches: int, shape, coeffs, cand_batch, cand_p, c
                              _ptr(cand_batch), _ptr(cand_p), _ptr(cand_c), m, _ptr(t_after),
                              _ptr(delta), _ptr(share), _ptr(regime), _stream(stream)),
            "llmv_admit")
+
+
+def llmv_shape_constants_ext(shape=None):
+    """(S0, S1, S2, S3, S5, S6) of the extended model (host only)."""
+    S = (ctypes.c_double * 6)()
+    sh = make_shape(shape)
+    _check(load().llmv_shape_constants_ext(_shape_ref(sh), S), "llmv_shape_constants_ext")
+    return list(S)
+
+
+def llmv_attribute_ext(trace: DeviceTrace, shape, coeffs, latency=None, regime=None, share=None,
+                       n_tenants: int = 0, tenant_sums=None, ws=None, stream=None):
+    """llmv_attribute under the extended model: coeffs holds 28 numbers,
+    index (phase*2 + segment)*7 + k, k = (beta, a1, ..., a6)."""
+    vals = [float(v) for v in coeffs]
+    if len(vals) != 28:
+        raise ValueError("the extended model takes 28 coefficients")
+    co = (ctypes.c_float * 28)(*vals)
+    sh = make_shape(shape)
+    if ws is None:
+        ws = workspace(trace.n_batches, trace.n_requests, n_tenants, trace.p.device)
+    tr = trace.struct(with_tenant=tenant_sums is not None)
+    nbytes = ws.numel() * ws.element_size()
+    _check(load().llmv_attribute_ext(ctypes.byref(tr), _shape_ref(sh), co, _ptr(latency),
+                                     _ptr(regime), _ptr(share), int(n_tenants), _ptr(tenant_sums),
+                                     _ptr(ws), nbytes, _stream(stream)),
+           "llmv_attribute_ext")
 
 
 def llmv_fit_workspace_size(n_batches: int) -> int:
@@ -391,3 +422,21 @@ def fit_metrics(sums, phase, shape, coeffs, y, ws=None, rel_err=False):
     if rel_err:
         res["rel_err"] = err
     return res
+
+
+def attribute_ext(trace: DeviceTrace, shape, coeffs, n_tenants: int = 0,
+                  outputs=("latency", "regime", "share", "tenant_sums"), ws=None):
+    """Allocates the requested outputs and runs llmv_attribute_ext."""
+    dev = trace.p.device
+    out = {}
+    if "latency" in outputs:
+        out["latency"] = torch.empty(trace.n_batches, dtype=torch.float32, device=dev)
+    if "regime" in outputs:
+        out["regime"] = torch.empty(trace.n_batches, dtype=torch.uint8, device=dev)
+    if "share" in outputs:
+        out["share"] = torch.empty(trace.n_requests, dtype=torch.float32, device=dev)
+    if "tenant_sums" in outputs:
+        out["tenant_sums"] = torch.empty(n_tenants, dtype=torch.float64, device=dev)
+    llmv_attribute_ext(trace, shape, coeffs, out.get("latency"), out.get("regime"),
+                       out.get("share"), n_tenants, out.get("tenant_sums"), ws)
+    return out

@@ -205,6 +205,36 @@ def test_fit_argument_errors(llmv):
     assert met(FAKE, FAKE, 8, None, co, FAKE, None, FAKE, FAKE, need - 1, None) == EW
 
 
+@pytest.mark.parametrize("name", sorted(tracegen.SHAPES))
+def test_shape_constants_ext_match_oracle(llmv, name):
+    sh = tracegen.SHAPES[name]
+    assert llmv.llmv_shape_constants_ext(sh) == list(oracle.shape_constants_ext(sh))
+    assert llmv.llmv_shape_constants_ext(None) == [1.0] * 6
+
+
+def test_attribute_ext_argument_errors(llmv):
+    """Host-side checks of llmv_attribute_ext; every call fails before any
+    launch."""
+    lib = llmv.load()
+    E = llmv.LLMV_EINVAL
+    co = (ctypes.c_float * 28)(*([1.0] * 28))
+    tr = ctypes.byref(_trace(llmv))
+    out = FAKE
+    ext = lib.llmv_attribute_ext
+    assert ext(None, None, co, out, None, None, 0, None, None, 0, None) == E
+    assert ext(tr, None, None, out, None, None, 0, None, None, 0, None) == E
+    co[27] = float("nan")
+    assert ext(tr, None, co, out, None, None, 0, None, None, 0, None) == E
+    co[27] = 1.0
+    assert ext(tr, None, co, None, None, None, 0, FAKE, None, 0, None) == E  # n_tenants 0
+    assert ext(tr, None, co, None, None, FAKE + 4, 0, None, None, 0, None) == E  # share misaligned
+    bad = llmv.llmv_shape(n_layers=0)
+    assert ext(tr, ctypes.byref(bad), co, out, None, None, 0, None, None, 0, None) == E
+    S = (ctypes.c_double * 6)()
+    assert lib.llmv_shape_constants_ext(ctypes.byref(bad), S) == E
+    assert lib.llmv_shape_constants_ext(None, None) == E
+
+
 def test_fit_workspace_size(llmv):
     """Fixed part plus 4 bytes per batch (the relative errors), 256-aligned."""
     lib = llmv.load()

@@ -130,6 +130,29 @@ def base_coeffs(seed: int) -> np.ndarray:
     return out.astype(np.float32)
 
 
+# Extended model: a5 (per processed-token/cached-key pair, attention FLOPs)
+# and a6 (per request, output-projection FLOPs), anchored like a3 and a1.
+_EXT_MEM_ANCHOR = (0.5 / _FL, 0.1 / _FL)
+_EXT_COMP_ANCHOR = (1 / _FL, 1 / _FL)
+_EXT_SIGMA = (0.2, 0.2)
+STREAM_EXT = 13
+
+
+def ext_coeffs(seed: int) -> np.ndarray:
+    """28 positive fp32 coefficients, index (phase*2+segment)*7+k: k < 5 are
+    base_coeffs(seed); a5, a6 are anchor * exp(sigma * Z), Z ~ N(0,1) drawn
+    per (phase, segment, k) from their own stream."""
+    base = base_coeffs(seed)
+    z = normal(seed, STREAM_EXT, 0, 8)
+    out = np.empty(28, np.float64)
+    for g in range(4):
+        anchor = _EXT_MEM_ANCHOR if g % 2 == 0 else _EXT_COMP_ANCHOR
+        out[g * 7:g * 7 + 5] = base[g * 5:(g + 1) * 5]
+        for j in range(2):
+            out[g * 7 + 5 + j] = anchor[j] * np.exp(_EXT_SIGMA[j] * z[g * 2 + j])
+    return out.astype(np.float32)
+
+
 def perturbed_coeffs(base: np.ndarray, seed: int) -> np.ndarray:
     """Each of the 20 coefficients times U[0.8, 1.2]."""
     u = uniform(seed, STREAM_PERTURB, 0, 20)
