@@ -334,6 +334,18 @@ def test_metrics_edge_cases(L):
     assert mg["prefill"]["p90"] == mg["prefill"]["p99"] == mo["prefill"]["p90"]
 
 
+def test_metrics_no_batches(L):
+    """No batches at all: every r^2 and percentile NaN, no batches counted."""
+    import torch
+    sums = torch.zeros((4, 0), dtype=torch.int64, device="cuda")
+    phase = torch.zeros(0, dtype=torch.uint8, device="cuda")
+    y = torch.zeros(0, dtype=torch.float64, device="cuda")
+    m = L.fit_metrics(sums, phase, None, tracegen.config_coeffs("tiny-mixed"), y)
+    for g in ("prefill", "decode", "all"):
+        assert m[g]["n"] == 0
+        assert np.isnan(m[g]["r2"]) and np.isnan(m[g]["p90"]) and np.isnan(m[g]["p99"])
+
+
 # -------------------------------------------------------- full-size workload
 
 
