@@ -19,6 +19,7 @@ the two fp64 predictions differ in the last place); per-batch relative
 errors within 1e-6, NaN exactly where the oracle has none; batch counts
 exact.
 """
+import os
 import sys
 
 import numpy as np
@@ -186,6 +187,31 @@ def test_fit_planted_recovery(L):
     for g in (2, 3):
         want[g * 5 + 3] = theta0[g * 5 + 3]
         want[g * 5 + 1] = truth[g * 5 + 1] + truth[g * 5 + 3] - theta0[g * 5 + 3]
+    assert np.max(np.abs(theta - want) / np.abs(want)) < 1e-6
+
+
+def test_fit_planted_recovery_model_shape(L):
+    """Planted recovery under the Llama3.1-8B shape (raw feature columns
+    spanning ~12 orders of magnitude, thousands of batches per set): the
+    column-scaled solve must recover every identifiable coefficient, as the
+    oracle pin with the same trace does."""
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from test_oracle_fit import model_shape_trace
+    tr = model_shape_trace(12)
+    co = tracegen.config_coeffs("heavy-tailed")
+    T = oracle.attribute(tr.offsets, tr.p, tr.c, None, tr.shape, co, 0, ("T", "regime"))
+    counts_true = np.bincount(T["regime"][T["regime"] != 255], minlength=4)
+    truth = co.astype(np.float64)
+    theta0 = truth * np.random.default_rng(6).uniform(0.9, 1.1, 20)
+    theta, counts = gpu_fit(L, tr, T["T"], theta0, 6)
+    assert np.array_equal(counts, counts_true)
+    want = truth.copy()
+    for g in (0, 1):
+        want[g * 5 + 2] = theta0[g * 5 + 2]
+    S = oracle.shape_constants(tr.shape)
+    for g in (2, 3):
+        want[g * 5 + 3] = theta0[g * 5 + 3]
+        want[g * 5 + 1] = truth[g * 5 + 1] + (truth[g * 5 + 3] - theta0[g * 5 + 3]) * S[3] / S[1]
     assert np.max(np.abs(theta - want) / np.abs(want)) < 1e-6
 
 
