@@ -380,6 +380,55 @@ def bench_ext(hip, stream, dt, tr, bufs, ws, steps, with_oracle):
     return res
 
 
+def bench_many_tenants(hip, stream, dt, tr, coeffs, bufs, with_oracle, n_tenants=1 << 20):
+    """The same trace with 2^20 tenants (Zipf(1.2) ids from the generator):
+    tenant sums through the LDS tenant cache and global atomics instead of
+    an LDS histogram.  Five llmv_attribute steps between HIP events."""
+    import numpy as np
+    import torch
+    import tracegen
+    from paper_2608_08382_amd import llmv
+
+    lat, reg, share = bufs
+    big = tracegen.generate(tracegen.KIND_HEAVY_TAILED, tr.n_batches,
+                            tracegen.CONFIG_SEED.get(tr.name, 4), n_tenants, tr.shape, "many")
+    assert np.array_equal(big.offsets, tr.offsets)
+    ten = torch.as_tensor(big.tenant, device=dt.p.device)
+    saved = dt.tenant
+    dt.tenant = ten
+    tsum = torch.empty(n_tenants, dtype=torch.float64, device=dt.p.device)
+    ws = llmv.workspace(tr.n_batches, tr.n_requests, n_tenants)
+
+    def step():
+        llmv.llmv_attribute(dt, tr.shape, coeffs, lat, reg, share, n_tenants, tsum, ws)
+
+    step()
+    torch.cuda.synchronize()
+    evs = [(hip.create(), hip.create()) for _ in range(5)]
+    for a, b in evs:
+        hip.record(a, stream)
+        step()
+        hip.record(b, stream)
+    torch.cuda.synchronize()
+    ms = sorted(hip.elapsed_ms(a, b) for a, b in evs)[2]
+    res = {"metric": "attributed requests/sec, 2^20 tenants", "value": tr.n_requests / (ms / 1e3),
+           "unit": "requests/s", "ms_per_step": ms, "n_tenants": n_tenants,
+           "tenants_with_requests": int(np.count_nonzero(np.bincount(big.tenant,
+                                                                     minlength=n_tenants)))}
+    log(f"[bench] {n_tenants} tenants: {ms:.3f} ms/step")
+    if with_oracle:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import parity
+        ref = oracle.attribute(tr.offsets, tr.p, tr.c, big.tenant, tr.shape, coeffs, n_tenants,
+                               ("T", "TM", "TC", "phase", "regime", "tenant_sums"))
+        res["parity"] = parity.compare(ref, tr.offsets, lat.cpu().numpy(), reg.cpu().numpy(), None,
+                                       tsum.cpu().numpy())
+    dt.tenant = saved
+    del ten, tsum, ws
+    return res
+
+
 def tracegen_single_batch(n):
     """One decode batch of n requests (context U[128, 8192]), 16 tenants."""
     import numpy as np
@@ -402,6 +451,8 @@ def main():
                     help="also time the step with subsets of the outputs (stderr)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the what-if sweep measurement (4 shapes x 256 coefficient vectors)")
+    ap.add_argument("--no-tenants", action="store_true",
+                    help="skip the 2^20-tenant measurement")
     ap.add_argument("--no-ext", action="store_true",
                     help="skip the extended-model measurement")
     ap.add_argument("--no-fit", action="store_true",
@@ -539,6 +590,11 @@ def main():
     if not args.no_ext:
         result["extended_model"] = bench_ext(hip, stream, dt, tr, (lat, reg, share, tsum), ws,
                                              max(5, args.steps // 2), not args.no_cpu_baseline)
+        step()  # the Eq. 1 outputs again, for the blocks below
+        torch.cuda.synchronize()
+    if not args.no_tenants:
+        result["many_tenants"] = bench_many_tenants(hip, stream, dt, tr, coeffs, (lat, reg, share),
+                                                    not args.no_cpu_baseline)
         step()  # the Eq. 1 outputs again, for the blocks below
         torch.cuda.synchronize()
     if not args.no_admission:

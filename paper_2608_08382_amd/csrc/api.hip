@@ -199,7 +199,8 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   if (rc) return rc;
   const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
   const int rep = hist == HIST_LDS ? hist_replicas(T) : 1;
-  const size_t dyn = hist == HIST_LDS ? (size_t)rep * (size_t)T * sizeof(double) : 0;
+  const size_t dyn = hist == HIST_LDS ? (size_t)rep * (size_t)T * sizeof(double)
+                     : (hist == HIST_GLOBAL ? kCacheLds : 0);
   const auto kern = TilePick<VT>::get(mode, hist, want_share);
   P.hist_rep = rep;
 
@@ -522,7 +523,7 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
   const bool lds = lds_hist(n_tenants);
   const int64_t grid =
       lds ? grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_LDS>, (size_t)n_tenants * sizeof(double)))
-          : grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_GLOBAL>, 0));
+          : grid_for(n, cus, blocks_per_cu(k_tenant_hist<HIST_GLOBAL>, kCacheLds));
   if (!lds) {
     // the atomics path accumulates into the output: clear it first
     hipLaunchKernelGGL(k_zero_f64, dim3(16), dim3(kWG), 0, s, tenant_sums, (int64_t)n_tenants);
@@ -538,7 +539,7 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
                        (const double*)partials, (int)grid, (int)n_tenants, tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
   } else {
-    hipLaunchKernelGGL(k_tenant_hist<HIST_GLOBAL>, dim3((unsigned)grid), dim3(kWG), 0, s, tenant,
+    hipLaunchKernelGGL(k_tenant_hist<HIST_GLOBAL>, dim3((unsigned)grid), dim3(kWG), kCacheLds, s, tenant,
                        share, n, n_tenants, (double*)nullptr, tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_hist launch");
   }

@@ -93,7 +93,7 @@ struct Params {
   uint8_t* regime;          // [nB] or null
   float* share;             // [N] or null
   double* partials;         // [grid][n_tenants] (HIST_LDS)
-  double* tenant_sums;      // [n_tenants] (HIST_GLOBAL: atomics target)
+  double* tenant_sums;      // [n_tenants] (HIST_GLOBAL: the tenant cache's output)
   float* x_req;             // [5][N] (MODE_FEAT) or null
   double* x_batch;          // [5][nB] (MODE_FEAT) or null
   int64_t* bsums;           // [4][nB] (|B|, sum p, sum c, sum p^2) (MODE_FEAT) or null
@@ -326,6 +326,82 @@ __device__ __forceinline__ void empty_batch(const Params& P, int64_t bg) {
   }
 }
 
+// ---------------------------------------------------------- tenant cache
+//
+// Tenant sums for more tenants than an LDS histogram holds (HIST_GLOBAL):
+// each workgroup keeps a 4-way set-associative table of kCacheSlots (tenant,
+// fp64 sum) slots in LDS.  A tenant's bucket is a hash of its id; one 16-byte
+// LDS read gives the bucket's four tags.  A tenant claims a free way of its
+// bucket (compare-and-swap of the tag: tags only ever change from empty to a
+// tenant, so a stale read is harmless) on its second sight in the workgroup,
+// which a 64K-bit filter of hashed tenant ids records, so that tenants seen
+// once do not take the ways frequent tenants need; one that finds its bucket
+// full, or is seen for the first time, adds into the output with a global
+// atomic.
+// At the end each workgroup adds its slots into the output (cleared before
+// the launch).  Under a skewed tenant mix the frequent tenants are seen first
+// and stay in LDS, so the global atomics go to rare tenants and seldom
+// collide.
+constexpr int kCacheLog2 = 11;
+constexpr int kCacheSlots = 1 << kCacheLog2;
+constexpr int kSeenWords = 2048;  // 64K bits
+constexpr size_t kCacheLds =
+    kCacheSlots * (sizeof(double) + sizeof(int32_t)) + kSeenWords * sizeof(uint32_t);
+
+__device__ __forceinline__ int32_t* cache_tags(double* base) {
+  return (int32_t*)(base + kCacheSlots);
+}
+
+__device__ __forceinline__ uint32_t* cache_seen(double* base) {
+  return (uint32_t*)(cache_tags(base) + kCacheSlots);
+}
+
+__device__ __forceinline__ void cache_init(double* base) {
+  int32_t* tag = cache_tags(base);
+  uint32_t* seen = cache_seen(base);
+  for (int i = threadIdx.x; i < kCacheSlots; i += blockDim.x) {
+    base[i] = 0.0;
+    tag[i] = -1;
+  }
+  for (int i = threadIdx.x; i < kSeenWords; i += blockDim.x) seen[i] = 0u;
+}
+
+__device__ __forceinline__ void cache_add(double* base, int32_t t, double v, double* out) {
+  int32_t* tag = cache_tags(base);
+  const uint32_t bk = ((uint32_t)t * 2654435761u) >> (32 - (kCacheLog2 - 2));
+  int32_t* tb = tag + 4 * bk;
+  const v4i tg = *(const v4i*)tb;
+  int w = tg.x == t ? 0 : (tg.y == t ? 1 : (tg.z == t ? 2 : (tg.w == t ? 3 : -1)));
+  if (w < 0 && (tg.x < 0 || tg.y < 0 || tg.z < 0 || tg.w < 0)) {
+    // a free way: claim it on the tenant's second sight
+    const uint32_t hs = ((uint32_t)t * 0x85ebca6bu) >> 16;
+    const uint32_t bit = 1u << (hs & 31u);
+    if (atomicOr(cache_seen(base) + (hs >> 5), bit) & bit) {
+      const int32_t ways[4] = {tg.x, tg.y, tg.z, tg.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (w < 0 && ways[j] < 0) {
+          const int32_t old = atomicCAS(tb + j, -1, t);
+          if (old < 0 || old == t) w = j;
+        }
+      }
+    }
+  }
+  if (w >= 0)
+    atomicAdd(base + 4 * bk + w, v);
+  else
+    unsafeAtomicAdd(out + t, v);
+}
+
+// After the workgroup's last add (the caller synchronises first).
+__device__ __forceinline__ void cache_flush(double* base, double* out) {
+  const int32_t* tag = cache_tags(base);
+  for (int i = threadIdx.x; i < kCacheSlots; i += blockDim.x) {
+    const int32_t t = tag[i];
+    if (t >= 0) unsafeAtomicAdd(out + t, base[i]);
+  }
+}
+
 // Per-request epilogue: the share (+ tenant histogram) or the feature row.
 // Shares: k0 + k1*p + k2*c + k3*p^2 (+ k4*p*c under the extended model, k[4])
 // in fp32 from the batch's constants (themselves evaluated in fp64),
@@ -349,7 +425,7 @@ __device__ __forceinline__ float request_out(const Params& P, const float* k, co
   float s = share_of(k, p, c);
   if constexpr (MODE == MODE_EXT) s = fmaf(k[4], (float)p * (float)c, s);
   if (HIST == HIST_LDS) atomicAdd(s_hist + t, (double)s);
-  if (HIST == HIST_GLOBAL) unsafeAtomicAdd(P.tenant_sums + t, (double)s);
+  if (HIST == HIST_GLOBAL) cache_add(s_hist, t, (double)s, P.tenant_sums);
   return s;
 }
 
@@ -631,6 +707,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
 
   if (HIST == HIST_LDS)
     for (int u = tid; u < n_hist; u += kWG) s_hist[u] = 0.0;
+  if (HIST == HIST_GLOBAL) cache_init(s_hist);
   // this lane's replica of the histogram (MODE_ATTR, MODE_FEAT)
   double* s_hist_lane = s_hist;
   if constexpr (MODE != MODE_SWEEP)
@@ -896,6 +973,9 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename Va
       for (int r = 1; r < P.hist_rep; ++r) acc += s_hist[r * T + u];
       dst[u] = acc;
     }
+  } else if (HIST == HIST_GLOBAL) {
+    __syncthreads();
+    cache_flush(s_hist, P.tenant_sums);
   }
 }
 
@@ -1071,17 +1151,21 @@ __global__ __launch_bounds__(kWG) void k_tenant_hist(const int32_t* __restrict__
   extern __shared__ double s_hist[];
   if (HIST == HIST_LDS)
     for (int u = threadIdx.x; u < T; u += kWG) s_hist[u] = 0.0;
+  else
+    cache_init(s_hist);
   __syncthreads();
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
   const int64_t lo = per * blockIdx.x, hi = min(n, lo + per);
   for (int64_t i = lo + threadIdx.x; i < hi; i += kWG) {
     const double v = (double)share[i];
     if (HIST == HIST_LDS) atomicAdd(s_hist + tenant[i], v);
-    else unsafeAtomicAdd(out + tenant[i], v);
+    else cache_add(s_hist, tenant[i], v, out);
   }
+  __syncthreads();
   if (HIST == HIST_LDS) {
-    __syncthreads();
     for (int u = threadIdx.x; u < T; u += kWG) partials[(int64_t)blockIdx.x * T + u] = s_hist[u];
+  } else {
+    cache_flush(s_hist, out);
   }
 }
 

@@ -204,7 +204,7 @@ def test_single_launch_boundary(L, N):
 
 
 # 1..1024 tenants: 4 LDS histogram replicas, 2048: 2, 3000 and 4096: 1,
-# above 4096: global atomics
+# above 4096: the LDS tenant cache with global atomics for the rest
 @pytest.mark.parametrize("n_tenants", [1, 2, 1024, 2048, 3000, 4096, 4097, 100000])
 def test_tenant_counts(L, n_tenants):
     rng = np.random.default_rng(n_tenants)
@@ -214,6 +214,20 @@ def test_tenant_counts(L, n_tenants):
                             n_tenants, None)
     check(L, tr, tracegen.SHAPES["qwen2.5-32b"], tracegen.base_coeffs(34), n_tenants,
           f"T={n_tenants}")
+
+
+@pytest.mark.parametrize("n_tenants", [4097, 1 << 16, 1 << 20, 1 << 24])
+def test_tenant_cache_under_skew(L, n_tenants):
+    """More tenants than an LDS histogram holds, Zipf(1.2) ids (a few
+    tenants take most requests, most tenants are seen once): the tenant
+    cache keeps the frequent ones, the rest go to global atomics; every
+    tenant's sum against the oracle.  200k batches (~2.5e7 requests), so each
+    workgroup's cache fills and overflows."""
+    tr = tracegen.generate(tracegen.KIND_HEAVY_TAILED, 200_000, 41, n_tenants,
+                           tracegen.SHAPES["llama3.1-8b"], "skewed")
+    st, g, ref = check(L, tr, tr.shape, tracegen.base_coeffs(36), n_tenants, f"T={n_tenants}")
+    say(f"[tenant cache] T={n_tenants}: {st}, tenants with requests "
+        f"{np.count_nonzero(np.bincount(tr.tenant, minlength=n_tenants))}")
 
 
 def test_single_tenant_all_requests(L):
@@ -322,11 +336,14 @@ def test_features(L, name, nb):
 # --------------------------------------------------------- tenant sums API
 
 
-@pytest.mark.parametrize("n,T", [(0, 3), (1, 1), (12345, 16), (1_000_003, 1024), (200_000, 5000)])
+@pytest.mark.parametrize("n,T", [(0, 3), (1, 1), (12345, 16), (1_000_003, 1024), (200_000, 5000),
+                                 (3_000_000, 1 << 20)])
 def test_tenant_sums_standalone(L, n, T):
     import torch
     rng = np.random.default_rng(n + T)
     t = rng.integers(0, T, n).astype(np.int32)
+    if T > 4096:  # skewed ids: the tenant cache's frequent and rare tenants
+        t = (tracegen.zipf(n + T, 7, 0, n, T, 1.2)).astype(np.int32)
     s = (rng.random(n) * 100).astype(np.float32)
     out = L.tenant_sums(torch.from_numpy(t).cuda(), torch.from_numpy(s).cuda(), T)
     torch.cuda.synchronize()
