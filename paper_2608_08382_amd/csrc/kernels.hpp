@@ -675,9 +675,12 @@ __device__ __forceinline__ int32_t hist_len(const Params& P) {
 }
 
 // NV (MODE_SWEEP): histogram rows, i.e. variants per pass, >= V.n; 1
-// otherwise.  V: the variants of a sweep (an empty struct otherwise).
+// otherwise.  V: the variants of a sweep (an empty struct otherwise).  The
+// 4-variant sweep instance is held to two waves per SIMD (left alone it
+// takes a few more than 256 registers and runs one).
 template <int MODE, int HIST, bool SHARE, int NV>
-__global__ __launch_bounds__(kWG) void k_tiles(const Params P, const typename VarsOf<MODE>::type V) {
+__global__ __launch_bounds__(kWG, (MODE == MODE_SWEEP && NV == 4) ? 2 : 1) void k_tiles(
+    const Params P, const typename VarsOf<MODE>::type V) {
   extern __shared__ double s_hist[];  // [variants][n_tenants] when HIST_LDS
   __shared__ WaveLds s_wave[kWaves];
   constexpr bool STAGE = kAttrMode<MODE> && SHARE;
