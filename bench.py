@@ -112,7 +112,7 @@ def bench_sweep(hip, stream, with_oracle):
     shapes = [tracegen.SHAPES[k] for k in names]
     dt = llmv.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
     out = torch.empty((4, 256, tr.n_tenants), dtype=torch.float64, device=dt.p.device)
-    ws = llmv.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+    ws = llmv.sweep_workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
     llmv.llmv_attribute_sweep(dt, shapes, co, tr.n_tenants, out, ws)
     torch.cuda.synchronize()
     reps = 3

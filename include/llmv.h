@@ -104,8 +104,14 @@ typedef struct {
 int llmv_shape_constants(const llmv_shape *shape, double S[4]);
 
 /* Bytes of device workspace every call below needs for a trace of this
- * size (the what-if sweep's per-workgroup histograms included). */
+ * size, except llmv_attribute_sweep (llmv_sweep_workspace_size). */
 size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
+
+/* Bytes of device workspace llmv_attribute_sweep needs for a trace of this
+ * size: llmv_workspace_size's (with a histogram per setting of a pass)
+ * plus the (batch, tenant) groups: 20 bytes per request, 32 bytes per batch
+ * and a few KiB. */
+size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
 
 /* Batched attribution (Sec. 2 Problem formulation; Sec. 2.1, Eq. 1).
  *   trace     host struct, device arrays as above.
@@ -170,10 +176,13 @@ int llmv_attribute_ext(const llmv_trace *trace, const llmv_shape *shape,
  *   out      device [n_shapes][n_coeffs][n_tenants] fp64, overwritten:
  *            out[(s*n_coeffs + v)*n_tenants + u] = L_u under (s, v).
  * Equivalent to n_shapes*n_coeffs calls of llmv_attribute with only
- * tenant_sums requested (the same shares, summed in another order).  Each
- * pass over the trace evaluates 8 consecutive variants (4 above 1024 tenants,
- * 2 above 2048): every tile is loaded and its batch sums formed once per pass.
- * n_tenants must be <= 4096 here.  The workspace is llmv_workspace_size's. */
+ * tenant_sums requested, up to rounding: the shares of one tenant's requests
+ * in one batch are summed in closed form, k0*n + k1*sum p + k2*sum c +
+ * k3*sum p^2 with the batch's fp32 constants and the group's sums rounded to
+ * fp32, and added in fp64.  The (batch, tenant) groups are formed once per
+ * call; each pass over them evaluates 8 consecutive settings (4 above 1024
+ * tenants, 2 above 2048).  n_tenants must be <= 4096 here.  The workspace is
+ * llmv_sweep_workspace_size's. */
 int llmv_attribute_sweep(const llmv_trace *trace, const llmv_shape *shapes,
                          int32_t n_shapes, const float *coeffs, int32_t n_coeffs,
                          int32_t n_tenants, double *out, void *ws, size_t ws_bytes,

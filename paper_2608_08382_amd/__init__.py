@@ -9,5 +9,5 @@ from .llmv import (DeviceTrace, LlmvError, admit, attribute, attribute_ext,  # n
                    llmv_attribute, llmv_attribute_ext, llmv_attribute_sweep, llmv_batch_sums,
                    llmv_features, llmv_shape_constants_ext,
                    llmv_fit, llmv_fit_metrics, llmv_fit_workspace_size, llmv_last_error,
-                   llmv_shape_constants, llmv_tenant_sums, llmv_validate, llmv_workspace_size,
-                   tenant_sums, workspace)
+                   llmv_shape_constants, llmv_sweep_workspace_size, llmv_tenant_sums,
+                   llmv_validate, llmv_workspace_size, sweep_workspace, tenant_sums, workspace)

@@ -7,7 +7,7 @@ import subprocess
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SOURCES = [os.path.join(PKG, "csrc", "api.hip"), os.path.join(PKG, "csrc", "fit.hip")]
-DEPS = SOURCES + [os.path.join(PKG, "csrc", h) for h in ("kernels.hpp", "fit.hpp", "host.hpp")] + [
+DEPS = SOURCES + [os.path.join(PKG, "csrc", h) for h in ("kernels.hpp", "groups.hpp", "fit.hpp", "host.hpp")] + [
     os.path.join(ROOT, "include", "llmv.h")]
 OUT = os.path.join(PKG, "libllmv.so")
 

@@ -9,6 +9,7 @@
 #include <mutex>
 
 #include "host.hpp"
+#include "groups.hpp"
 #include "kernels.hpp"
 #include "llmv.h"
 
@@ -61,7 +62,7 @@ int hist_replicas(int32_t T) {
   return 1;
 }
 
-// Variants per what-if pass for T tenants (T <= kHistLdsMax): 8, 4 or 2
+// Settings per what-if pass for T tenants (T <= kHistLdsMax): 8, 4 or 2
 // fp64 histograms of T + hot-tenant replicas, at most 65 KiB of LDS, so that
 // with the kernel's own LDS two workgroups fit in a CU's 160 KiB.
 constexpr size_t kSweepHistLds = 65 * 1024;
@@ -72,11 +73,11 @@ int sweep_group(int32_t T) {
 }
 static_assert(2 * (kHistLdsMax + kHotSlots) * sizeof(double) <= kSweepHistLds, "sweep LDS");
 
-typedef void (*SweepKernel)(const Params, const VarTable);
+typedef void (*SweepKernel)(const GroupSweep, const VarTable);
 SweepKernel pick_sweep(int g) {
-  if (g >= 8) return k_tiles<MODE_SWEEP, HIST_LDS, false, 8>;
-  if (g >= 4) return k_tiles<MODE_SWEEP, HIST_LDS, false, 4>;
-  return k_tiles<MODE_SWEEP, HIST_LDS, false, 2>;
+  if (g >= 8) return k_sweep_groups<8>;
+  if (g >= 4) return k_sweep_groups<4>;
+  return k_sweep_groups<2>;
 }
 
 struct Layout {
@@ -112,16 +113,17 @@ ChunkMap chunk_map(int64_t n, int64_t workers) {
   return m;
 }
 
-// Workspace layout shared by every entry point.
-Layout layout(int64_t grid, int32_t T) {
+// Workspace layout shared by every entry point; rows = histograms per
+// workgroup (settings per pass in the what-if sweep, else 1).
+Layout layout(int64_t grid, int32_t T, int rows = 1) {
   Layout L{};
   size_t o = 0;
   L.wg_first = o;  // first batch of each chunk
   o += align_up((size_t)(grid * kWaves * (1 + kDynPerWorker) + 1) * sizeof(int64_t));
   L.claims = o;
   o += align_up(sizeof(unsigned long long));
-  L.partials = o;  // [grid][variants of a what-if pass][T]
-  if (lds_hist(T)) o += align_up((size_t)grid * (size_t)sweep_group(T) * (size_t)T * sizeof(double));
+  L.partials = o;  // [grid][rows][T]
+  if (lds_hist(T)) o += align_up((size_t)grid * (size_t)rows * (size_t)T * sizeof(double));
   L.counts = o;  // what-if sweep: requests per tenant, and the hot tenants
   if (lds_hist(T)) o += align_up((size_t)T * sizeof(unsigned long long));
   L.hot = o;
@@ -130,6 +132,37 @@ Layout layout(int64_t grid, int32_t T) {
   o += align_up(sizeof(int));
   L.total = o;
   return L;
+}
+
+// The what-if sweep's groups after a Layout ending at o: slice table, slice
+// group counts and offsets, batch group offsets, exact batch sums, scan tile
+// sums, and the groups (at most one per request, plus a tile of slack that
+// the sweep tiles read past the last group).
+struct GroupLayout {
+  size_t first, scnt, soff, gofs, bsum, tsum, gw, gf, total;
+};
+GroupLayout group_layout(size_t o, int64_t nB, int64_t N) {
+  GroupLayout G{};
+  const int64_t nS = (N + kSlice - 1) / kSlice;
+  const int64_t nt = (nS + kScanTile - 1) / kScanTile;
+  G.first = o;
+  o += align_up((size_t)(nS + 1) * sizeof(int64_t));
+  G.scnt = o;
+  o += align_up((size_t)(nS + 1) * sizeof(int64_t));
+  G.soff = o;
+  o += align_up((size_t)(nS + 1) * sizeof(int64_t));
+  G.gofs = o;
+  o += align_up((size_t)(nB + 1) * sizeof(int64_t));
+  G.bsum = o;
+  o += align_up((size_t)(3 * nB + 1) * sizeof(unsigned long long));
+  G.tsum = o;
+  o += align_up((size_t)(nt + 1) * sizeof(int64_t));
+  G.gw = o;
+  o += align_up((size_t)(N + kGT) * sizeof(uint32_t));
+  G.gf = o;
+  o += align_up((size_t)(N + kGT) * sizeof(v4f));
+  G.total = o;
+  return G;
 }
 
 int check_trace(const llmv_trace* tr, bool need_tenant) {
@@ -161,12 +194,12 @@ int partition(const llmv_trace* tr, const ChunkMap& cm, int64_t* wg_first,
 typedef void (*TileKernel)(const Params, const NoVars);
 
 TileKernel pick_tiles(int mode, int hist, bool share) {
-  if (mode == MODE_FEAT) return k_tiles<MODE_FEAT, HIST_NONE, false, 1>;
+  if (mode == MODE_FEAT) return k_tiles<MODE_FEAT, HIST_NONE, false>;
   if (hist == HIST_NONE)
-    return share ? k_tiles<MODE_ATTR, HIST_NONE, true, 1> : k_tiles<MODE_ATTR, HIST_NONE, false, 1>;
+    return share ? k_tiles<MODE_ATTR, HIST_NONE, true> : k_tiles<MODE_ATTR, HIST_NONE, false>;
   if (hist == HIST_LDS)
-    return share ? k_tiles<MODE_ATTR, HIST_LDS, true, 1> : k_tiles<MODE_ATTR, HIST_LDS, false, 1>;
-  return share ? k_tiles<MODE_ATTR, HIST_GLOBAL, true, 1> : k_tiles<MODE_ATTR, HIST_GLOBAL, false, 1>;
+    return share ? k_tiles<MODE_ATTR, HIST_LDS, true> : k_tiles<MODE_ATTR, HIST_LDS, false>;
+  return share ? k_tiles<MODE_ATTR, HIST_GLOBAL, true> : k_tiles<MODE_ATTR, HIST_GLOBAL, false>;
 }
 
 // The tile kernel for a mode and its second argument's type.
@@ -178,10 +211,10 @@ template <> struct TilePick<ExtModel> {
   typedef void (*K)(const Params, const ExtModel);
   static K get(int, int hist, bool share) {
     if (hist == HIST_NONE)
-      return share ? k_tiles<MODE_EXT, HIST_NONE, true, 1> : k_tiles<MODE_EXT, HIST_NONE, false, 1>;
+      return share ? k_tiles<MODE_EXT, HIST_NONE, true> : k_tiles<MODE_EXT, HIST_NONE, false>;
     if (hist == HIST_LDS)
-      return share ? k_tiles<MODE_EXT, HIST_LDS, true, 1> : k_tiles<MODE_EXT, HIST_LDS, false, 1>;
-    return share ? k_tiles<MODE_EXT, HIST_GLOBAL, true, 1> : k_tiles<MODE_EXT, HIST_GLOBAL, false, 1>;
+      return share ? k_tiles<MODE_EXT, HIST_LDS, true> : k_tiles<MODE_EXT, HIST_LDS, false>;
+    return share ? k_tiles<MODE_EXT, HIST_GLOBAL, true> : k_tiles<MODE_EXT, HIST_GLOBAL, false>;
   }
 };
 
@@ -309,6 +342,14 @@ size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tena
   return layout(grid_max_for(n), n_tenants > 0 ? n_tenants : 0).total;
 }
 
+size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
+  const int64_t nB = n_batches > 0 ? n_batches : 0;
+  const int64_t n = n_requests > 0 ? n_requests : 0;
+  const int32_t T = n_tenants > 0 ? n_tenants : 0;
+  const Layout L = layout(grid_max_for(n), T, lds_hist(T) ? sweep_group(T) : 1);
+  return group_layout(L.total, nB, n).total;
+}
+
 int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[20],
                    float* latency, uint8_t* regime, float* share, int32_t n_tenants,
                    double* tenant_sums, void* ws, size_t ws_bytes, void* stream) {
@@ -369,51 +410,107 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   int cus = 0;
   rc = device_cus(&cus);
   if (rc) return rc;
-  const Layout L = layout(grid_max_for(trace->n_requests), n_tenants);
-  rc = check_ws(ws, ws_bytes, L.total);
+  const int64_t nB = trace->n_batches, N = trace->n_requests;
+  // One pass over the groups per G consecutive settings (shape-major, as in
+  // out); each pass keeps G tenant histograms in LDS.
+  const int G = sweep_group(n_tenants);
+  const Layout L = layout(grid_max_for(N), n_tenants, G);
+  const GroupLayout GL = group_layout(L.total, nB, N);
+  rc = check_ws(ws, ws_bytes, GL.total);
   if (rc) return rc;
   char* base = (char*)ws;
-  // One pass over the trace per group of G consecutive variants (shape-major,
-  // as in out); each pass keeps G tenant histograms in LDS.
-  const int G = sweep_group(n_tenants);
+  const int64_t n_var = (int64_t)n_shapes * n_coeffs;
+  if (N == 0) {  // no requests: every tenant sum is zero
+    const int64_t n_out = n_var * n_tenants;
+    int64_t blocks = (n_out + kWG - 1) / kWG;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(k_zero_f64, dim3((unsigned)blocks), dim3(kWG), 0, st, out, n_out);
+    HIP_TRY(hipGetLastError(), "k_zero_f64 launch");
+    return LLMV_OK;
+  }
   const size_t dyn = (size_t)G * (size_t)(n_tenants + kHotSlots) * sizeof(double);
   const SweepKernel kern = pick_sweep(G);
-  const int64_t grid = grid_for(trace->n_requests, cus, blocks_per_cu(kern, dyn));
-  const ChunkMap cm = chunk_map(trace->n_requests, grid * kWaves);
-  Params P{};
-  P.off = trace->offsets;
-  P.p = trace->p;
-  P.c = trace->c;
-  P.tenant = trace->tenant;
-  P.nB = trace->n_batches;
-  P.N = trace->n_requests;
-  P.wg_first = (int64_t*)(base + L.wg_first);
-  P.claims = (unsigned long long*)(base + L.claims);
-  P.n_chunks = cm.n_chunks;
-  P.partials = (double*)(base + L.partials);
-  P.n_tenants = n_tenants;
-  P.hist_rep = 1;
-  {
-    // the most frequent tenants get replicated histogram entries
-    unsigned long long* counts = (unsigned long long*)(base + L.counts);
-    int32_t* hot = (int32_t*)(base + L.hot);
-    hipLaunchKernelGGL(k_zero_u64, dim3(16), dim3(kWG), 0, st, counts, (int64_t)n_tenants);
-    HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
-    int64_t blocks = (P.N + (int64_t)kWG * 64 - 1) / ((int64_t)kWG * 64);
-    blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
-    hipLaunchKernelGGL(k_tenant_count, dim3((unsigned)blocks), dim3(kWG),
-                       (size_t)n_tenants * sizeof(unsigned int), st, P.tenant, P.N, n_tenants, counts);
-    HIP_TRY(hipGetLastError(), "k_tenant_count launch");
-    hipLaunchKernelGGL(k_hot_tenants, dim3(1), dim3(kWG), 0, st, (const unsigned long long*)counts,
-                       n_tenants, hot);
-    HIP_TRY(hipGetLastError(), "k_hot_tenants launch");
-    P.hot = hot;
-  }
-  // every launch takes exactly n_chunks claims (one per chunk it runs, the
-  // static ones included), so launch i starts at claim i * n_chunks
-  rc = partition(trace, cm, (int64_t*)P.wg_first, P.claims, st);
+  const int64_t grid = grid_for(N, cus, blocks_per_cu(kern, dyn));
+  unsigned long long* claims = (unsigned long long*)(base + L.claims);
+
+  // the most frequent tenants get replicated histogram entries
+  unsigned long long* counts = (unsigned long long*)(base + L.counts);
+  int32_t* hot = (int32_t*)(base + L.hot);
+  hipLaunchKernelGGL(k_zero_u64, dim3(16), dim3(kWG), 0, st, counts, (int64_t)n_tenants);
+  HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
+  int64_t blocks = (N + (int64_t)kWG * 64 - 1) / ((int64_t)kWG * 64);
+  blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+  hipLaunchKernelGGL(k_tenant_count, dim3((unsigned)blocks), dim3(kWG),
+                     (size_t)n_tenants * sizeof(unsigned int), st, trace->tenant, N, n_tenants,
+                     counts);
+  HIP_TRY(hipGetLastError(), "k_tenant_count launch");
+  hipLaunchKernelGGL(k_hot_tenants, dim3(1), dim3(kWG), 0, st, (const unsigned long long*)counts,
+                     n_tenants, hot);
+  HIP_TRY(hipGetLastError(), "k_hot_tenants launch");
+
+  // the groups: counts and exact batch sums per slice, slice offsets, then
+  // the groups themselves
+  const int64_t nS = (N + kSlice - 1) / kSlice;
+  int64_t* first = (int64_t*)(base + GL.first);
+  int64_t* scnt = (int64_t*)(base + GL.scnt);
+  int64_t* soff = (int64_t*)(base + GL.soff);
+  int64_t* gofs = (int64_t*)(base + GL.gofs);
+  unsigned long long* bsum = (unsigned long long*)(base + GL.bsum);
+  int64_t* tsum = (int64_t*)(base + GL.tsum);
+  uint32_t* gw = (uint32_t*)(base + GL.gw);
+  v4f* gf = (v4f*)(base + GL.gf);
+  ChunkMap sm{};  // equal slices, none claimed
+  sm.s1 = kSlice;
+  sm.s2 = 1;
+  sm.n_static = nS;
+  sm.n_chunks = nS;
+  sm.F = nS * kSlice;
+  rc = partition(trace, sm, first, claims, st);
   if (rc) return rc;
-  const int64_t n_var = (int64_t)n_shapes * n_coeffs;
+  hipLaunchKernelGGL(k_zero_u64, dim3(256), dim3(kWG), 0, st, bsum, 3 * nB);
+  HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
+  int64_t bgrid = (nS + kWaves - 1) / kWaves;
+  const int64_t bcap = (int64_t)cus * blocks_per_cu(k_group_build<true>, 0);
+  if (bgrid > bcap) bgrid = bcap;
+  hipLaunchKernelGGL(k_group_build<false>, dim3((unsigned)bgrid), dim3(kWG), 0, st, trace->offsets,
+                     trace->p, trace->c, trace->tenant, nB, N, (const int64_t*)first, nS, scnt, bsum,
+                     (const int64_t*)nullptr, (int64_t*)nullptr, (uint32_t*)nullptr, (v4f*)nullptr);
+  HIP_TRY(hipGetLastError(), "k_group_build launch");
+  const int64_t nt = (nS + kScanTile - 1) / kScanTile;  // >= 1
+  hipLaunchKernelGGL(k_scan_tiles, dim3((unsigned)nt), dim3(kScanWG), 0, st, (const int64_t*)scnt, nS,
+                     tsum);
+  HIP_TRY(hipGetLastError(), "k_scan_tiles launch");
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanWG), 0, st, tsum, nt);
+  HIP_TRY(hipGetLastError(), "k_scan_top launch");
+  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nt), dim3(kScanWG), 0, st, (const int64_t*)scnt, nS,
+                     (const int64_t*)tsum, soff);
+  HIP_TRY(hipGetLastError(), "k_scan_apply launch");
+  hipLaunchKernelGGL(k_group_build<true>, dim3((unsigned)bgrid), dim3(kWG), 0, st, trace->offsets,
+                     trace->p, trace->c, trace->tenant, nB, N, (const int64_t*)first, nS,
+                     (int64_t*)nullptr, (unsigned long long*)nullptr, (const int64_t*)soff, gofs, gw,
+                     gf);
+  HIP_TRY(hipGetLastError(), "k_group_build launch");
+
+  // the passes: the chunks of k_tiles over the batches; every launch takes
+  // exactly n_chunks claims (one per chunk it runs, the static ones
+  // included), so launch i starts at claim i * n_chunks
+  const ChunkMap cm = chunk_map(N, grid * kWaves);
+  int64_t* wg_first = (int64_t*)(base + L.wg_first);
+  rc = partition(trace, cm, wg_first, claims, st);
+  if (rc) return rc;
+  GroupSweep Q{};
+  Q.off = trace->offsets;
+  Q.gofs = gofs;
+  Q.bsum = bsum;
+  Q.gw = gw;
+  Q.gf = gf;
+  Q.nB = nB;
+  Q.wg_first = wg_first;
+  Q.claims = claims;
+  Q.n_chunks = cm.n_chunks;
+  Q.partials = (double*)(base + L.partials);
+  Q.n_tenants = n_tenants;
+  Q.hot = hot;
   int64_t launch = 0;
   for (int64_t v0 = 0; v0 < n_var; v0 += G, ++launch) {
     VarTable V{};
@@ -427,12 +524,12 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
       for (int r = 0; r < 4; ++r)
         for (int k = 1; k < 4; ++k) V.K[g][r][k - 1] = (float)(V.th[g][r * 5 + k] * S[s][k]);
     }
-    P.claim_base = (uint64_t)launch * (uint64_t)cm.n_chunks;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, P, V);
-    HIP_TRY(hipGetLastError(), "k_tiles launch");
+    Q.claim_base = (uint64_t)launch * (uint64_t)cm.n_chunks;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, Q, V);
+    HIP_TRY(hipGetLastError(), "k_sweep_groups launch");
     const int n_hist = V.n * n_tenants;
     hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)((n_hist + kTenantChunk - 1) / kTenantChunk)),
-                       dim3(64 * kReduceWaves), 0, st, (const double*)P.partials, (int)grid, n_hist,
+                       dim3(64 * kReduceWaves), 0, st, (const double*)Q.partials, (int)grid, n_hist,
                        out + v0 * n_tenants);
     HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
   }

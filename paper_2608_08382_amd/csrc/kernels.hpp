@@ -22,6 +22,8 @@
 //  * Tenant sums accumulate in an fp64 LDS histogram per workgroup, flushed
 //    once to a [grid][n_tenants] partial array that k_tenant_reduce folds in
 //    a fixed order.
+// The what-if sweep (many coefficient settings over one trace) has kernels
+// of its own in groups.hpp.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -65,11 +67,10 @@ struct ChunkMap {
 };
 
 // MODE_ATTR: latency, regime, share, tenant sums of one (shape, theta).
-// MODE_FEAT: the feature rows.  MODE_SWEEP: tenant sums of up to kSweepG
-// variants (shape, theta) per pass over the trace.  MODE_EXT: the outputs
-// of MODE_ATTR under the extended model (Eq. 1 plus a cross term
-// a5*S5*sum p*c and a per-request term a6*S6*|B|).
-enum { MODE_ATTR = 0, MODE_FEAT = 1, MODE_SWEEP = 2, MODE_EXT = 3 };
+// MODE_FEAT: the feature rows.  MODE_EXT: the outputs of MODE_ATTR under the
+// extended model (Eq. 1 plus a cross term a5*S5*sum p*c and a per-request
+// term a6*S6*|B|).
+enum { MODE_ATTR = 0, MODE_FEAT = 1, MODE_EXT = 2 };
 template <int MODE> constexpr bool kAttrMode = MODE == MODE_ATTR || MODE == MODE_EXT;
 
 // Native vectors: 16-byte global loads / stores (dwordx4).
@@ -98,32 +99,12 @@ struct Params {
   double* x_batch;          // [5][nB] (MODE_FEAT) or null
   int64_t* bsums;           // [4][nB] (|B|, sum p, sum c, sum p^2) (MODE_FEAT) or null
   uint8_t* bphase;          // [nB] phase, 255 for an empty batch (MODE_FEAT) or null
-  const int32_t* hot;       // [kHot] most frequent tenants, -1 for none (MODE_SWEEP)
   int32_t n_tenants;
   int32_t hist_rep;         // MODE_ATTR, HIST_LDS: histogram replicas (1, 2 or 4)
   double S[4];              // shape constants
   double th[20];            // theta[phase][segment][k]
 };
 
-// The variants of one MODE_SWEEP launch: shape constants and Eq. 1
-// coefficients (theta[phase][segment][k], as in Params) of each, and the
-// batch-independent share constants k1..k3 = fp32(theta_a1*S1, theta_a2*S2,
-// theta_a3*S3) of each regime (2*phase + segment), rounded from the same fp64
-// products as in MODE_ATTR.
-constexpr int kSweepG = 8;
-// Under tenant skew many lanes of one LDS atomic hit the same histogram
-// entry and serialize.  A sweep gives each of its kHot most frequent tenants
-// kHotRep histogram entries (lane l adds into entry l % kHotRep), folded at
-// the end.
-constexpr int kHot = 4;
-constexpr int kHotRep = 4;
-constexpr int kHotSlots = kHot * kHotRep;
-struct VarTable {
-  int32_t n;                // variants in this launch, 1..kSweepG
-  double S[kSweepG][4];
-  double th[kSweepG][20];
-  float K[kSweepG][4][4];   // [variant][regime][k1, k2, k3, unused]
-};
 struct NoVars {};
 // The extended model of a MODE_EXT launch: the two extra shape constants
 // and the coefficients theta[phase][segment][k], k = 0..6 (beta, a1..a6).
@@ -132,7 +113,6 @@ struct ExtModel {
   double th[28];
 };
 template <int MODE> struct VarsOf { using type = NoVars; };
-template <> struct VarsOf<MODE_SWEEP> { using type = VarTable; };
 template <> struct VarsOf<MODE_EXT> { using type = ExtModel; };
 
 // ---------------------------------------------------------------- wave ops
@@ -261,49 +241,6 @@ __device__ __forceinline__ void ext_model(const Params& P, const ExtModel& E, in
   k[2] = th[2] * P.S[2];
   k[3] = th[3] * P.S[3];
   *k4 = th[5] * E.S5;
-}
-
-// Share constants of one batch under variant g of a sweep (the same
-// arithmetic as batch_model in MODE_ATTR, without batch outputs).
-__device__ __forceinline__ void sweep_model(const VarTable& V, int g, int64_t n, uint64_t Psum,
-                                            uint64_t Csum, uint64_t Qsum, bool prefill,
-                                            double* k) {
-  const double* S = V.S[g];
-  const double X[5] = {S[0], S[1] * (double)Psum, S[2] * (double)Csum, S[3] * (double)Qsum,
-                       (double)n * (double)n};
-  const int phase = prefill ? 0 : 1;
-  const double* thm = V.th[g] + (phase * 2 + 0) * 5;
-  const double* thc = V.th[g] + (phase * 2 + 1) * 5;
-  // Roofline max of the two segments; ties stay memory-bound.
-  const double* th = (eq1(thc, X) > eq1(thm, X)) ? thc : thm;
-  k[0] = th[0] * (S[0] / (double)n) + th[4] * (double)n;
-  k[1] = th[1] * S[1];
-  k[2] = th[2] * S[2];
-  k[3] = th[3] * S[3];
-}
-
-// One batch under every variant of a sweep: k0 of variant g (fp32, rounded
-// from the fp64 value of sweep_model) into k0[g]; returns the segments (bit
-// g) and the phase (bit 8, set for decode).
-template <int NV>
-__device__ __forceinline__ uint32_t sweep_batch(const VarTable& V, int64_t n, uint64_t Psum,
-                                                uint64_t Csum, uint64_t Qsum, bool prefill,
-                                                float* k0) {
-  const int phase = prefill ? 0 : 1;
-  uint32_t segs = (uint32_t)phase << 8;
-  for (int g = 0; g < NV; ++g) {
-    const double* S = V.S[g];
-    const double X[5] = {S[0], S[1] * (double)Psum, S[2] * (double)Csum, S[3] * (double)Qsum,
-                         (double)n * (double)n};
-    const double* thm = V.th[g] + (phase * 2 + 0) * 5;
-    const double* thc = V.th[g] + (phase * 2 + 1) * 5;
-    // Roofline max of the two segments; ties stay memory-bound.
-    const bool comp = eq1(thc, X) > eq1(thm, X);
-    const double* th = comp ? thc : thm;
-    segs |= (uint32_t)comp << g;
-    k0[g] = (float)(th[0] * (S[0] / (double)n) + th[4] * (double)n);
-  }
-  return segs;
 }
 
 // fp32 share of one request from fp32 batch constants (as request_out).
@@ -481,19 +418,10 @@ struct BatchAcc {
 
 // LDS private to one wave.
 struct WaveLds {
-  union {
-    uint32_t mask[kTileMaskWords + 2];  // bit x: a nonempty batch starts at slot x
-    uint16_t segs[kTileBatches + 1];    // sweep, after the batch sums: per nonempty
-                                        // batch, bit g = segment of variant g, bit 8 =
-                                        // decode phase
-  };
+  uint32_t mask[kTileMaskWords + 2];  // bit x: a nonempty batch starts at slot x
   BatchAcc acc[kTileBatches];         // per nonempty batch of the tile
-  union {
-    double k[kTileBatches][4];        // per nonempty batch: share / feature constants
-    float k0s[kTileBatches][kSweepG]; // sweep: k0 of each variant
-  };
+  double k[kTileBatches][4];          // per nonempty batch: share / feature constants
   static_assert(kVec % 4 == 0 && kVec <= 28, "lane slots: multiple of 4, bits fit a word pair");
-  static_assert(kSweepG <= 8, "segment bits of a sweep fit below the phase bit");
 };
 
 // Orders LDS accesses between the lanes of one wave (a wave's LDS accesses
@@ -585,7 +513,7 @@ __device__ __forceinline__ void store_round(const Params& P, float* stage, int64
 
 // One batch too large for a wave tile: two passes over its requests by the
 // whole wave (the second pass mostly hits in L2).
-template <int MODE, int HIST, bool SHARE, int NV>
+template <int MODE, int HIST, bool SHARE>
 __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V, WaveLds& W,
                           double* wk4, float* stage, int64_t bg, int64_t rs, int64_t re,
                           double* s_hist) {
@@ -612,25 +540,6 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
   sq = wave_sum(sq);
   if constexpr (MODE == MODE_EXT) sr = wave_sum(sr);
   const int64_t n = re - rs;
-  if constexpr (MODE == MODE_SWEEP) {
-    // every lane holds the sums: per variant, the constants and one pass
-    const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
-    for (int g = 0; g < V.n; ++g) {
-      double kd[4];
-      sweep_model(V, g, n, sp, scz & kCMask, sq, prefill, kd);
-      const float k[4] = {(float)kd[0], (float)kd[1], (float)kd[2], (float)kd[3]};
-      double* hg = s_hist + g * (P.n_tenants + kHotSlots);
-      for (int64_t base = ra; base < re; base += kRoundSlots) {
-        const int64_t x = base + lane * kVec;
-        load_slots<true>(P, x, pv, cv, tv);
-#pragma unroll
-        for (int q = 0; q < kVec; ++q)
-          if (x + q >= rs && x + q < re) atomicAdd(hg + tv[q], (double)share_of(k, pv[q], cv[q]));
-      }
-    }
-    wave_lds_sync();
-    return;
-  }
   if (lane == 0) {
     const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
     if constexpr (MODE == MODE_EXT)
@@ -664,24 +573,14 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
   wave_lds_sync();
 }
 
-// Entries of the LDS tenant histogram: hist_rep replicas of n_tenants
-// (lane l adds into replica l % hist_rep, so that lanes of one atomic that
-// share a frequent tenant spread over hist_rep entries), or in a sweep NV
-// rows of n_tenants + hot-tenant replicas.
-template <int MODE, int NV>
-__device__ __forceinline__ int32_t hist_len(const Params& P) {
-  if constexpr (MODE == MODE_SWEEP) return NV * (P.n_tenants + kHotSlots);
-  else return P.hist_rep * P.n_tenants;
-}
-
-// NV (MODE_SWEEP): histogram rows, i.e. variants per pass, >= V.n; 1
-// otherwise.  V: the variants of a sweep (an empty struct otherwise).  The
-// 4-variant sweep instance is held to two waves per SIMD (left alone it
-// takes a few more than 256 registers and runs one).
-template <int MODE, int HIST, bool SHARE, int NV>
-__global__ __launch_bounds__(kWG, (MODE == MODE_SWEEP && NV == 4) ? 2 : 1) void k_tiles(
-    const Params P, const typename VarsOf<MODE>::type V) {
-  extern __shared__ double s_hist[];  // [variants][n_tenants] when HIST_LDS
+// V: the extended model (MODE_EXT), an empty struct otherwise.  The LDS
+// tenant histogram (HIST_LDS) holds hist_rep replicas of n_tenants entries:
+// lane l adds into replica l % hist_rep, so that lanes of one atomic that
+// share a frequent tenant spread over hist_rep entries.
+template <int MODE, int HIST, bool SHARE>
+__global__ __launch_bounds__(kWG) void k_tiles(const Params P,
+                                               const typename VarsOf<MODE>::type V) {
+  extern __shared__ double s_hist[];  // [hist_rep][n_tenants] when HIST_LDS
   __shared__ WaveLds s_wave[kWaves];
   constexpr bool STAGE = kAttrMode<MODE> && SHARE;
   constexpr bool EXT = MODE == MODE_EXT;
@@ -698,23 +597,14 @@ __global__ __launch_bounds__(kWG, (MODE == MODE_SWEEP && NV == 4) ? 2 : 1) void 
   double* W_k4 = s_k4 + (EXT ? (tid >> 6) * kTileBatches : 0);
   float* stage = s_stage + (STAGE ? (tid >> 6) * 64 * kStagePitch : 0);
   const int32_t x0 = lane * kVec;  // first slot of this lane in a round
-  const int32_t n_hist = hist_len<MODE, NV>(P);
-  static_assert(NV >= 1 && NV <= kSweepG, "variants per pass");
-  int32_t hot[kHot];  // sweep: the most frequent tenants
-#pragma unroll
-  for (int h = 0; h < kHot; ++h) hot[h] = MODE == MODE_SWEEP ? uni(P.hot[h]) : -1;
-  // sweep: the regime constants k1..k3 of every variant, indexed per lane
-  __shared__ float s_K[MODE == MODE_SWEEP ? NV * 4 * 3 : 1];  // [variant][regime][k1..k3]
-  if constexpr (MODE == MODE_SWEEP)
-    for (int i = tid; i < NV * 12; i += kWG) s_K[i] = V.K[i / 12][(i / 3) % 4][i % 3];
+  const int32_t n_hist = P.hist_rep * P.n_tenants;
 
   if (HIST == HIST_LDS)
     for (int u = tid; u < n_hist; u += kWG) s_hist[u] = 0.0;
   if (HIST == HIST_GLOBAL) cache_init(s_hist);
-  // this lane's replica of the histogram (MODE_ATTR, MODE_FEAT)
+  // this lane's replica of the histogram
   double* s_hist_lane = s_hist;
-  if constexpr (MODE != MODE_SWEEP)
-    if (HIST == HIST_LDS) s_hist_lane = s_hist + (lane & (P.hist_rep - 1)) * P.n_tenants;
+  if (HIST == HIST_LDS) s_hist_lane = s_hist + (lane & (P.hist_rep - 1)) * P.n_tenants;
   __syncthreads();
 
   // the first chunk of each wave is its static one; later ones are claimed
@@ -752,8 +642,7 @@ __global__ __launch_bounds__(kWG, (MODE == MODE_SWEEP && NV == 4) ? 2 : 1) void 
       }
 
       if (count == 0) {
-        big_batch<MODE, HIST, SHARE, NV>(P, V, W, W_k4, stage, b, r0, r1,
-                                         MODE == MODE_SWEEP ? s_hist : s_hist_lane);
+        big_batch<MODE, HIST, SHARE>(P, V, W, W_k4, stage, b, r0, r1, s_hist_lane);
       } else {
         const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
         const int32_t lo_next = __shfl_down(lo, 1, 64);
@@ -832,60 +721,7 @@ __global__ __launch_bounds__(kWG, (MODE == MODE_SWEEP && NV == 4) ? 2 : 1) void 
         }
         wave_lds_sync();
 
-        if constexpr (MODE == MODE_SWEEP) {
-          // ---- every variant at once: lane j evaluates batch b+j under each
-          // variant (k0 and the segment); then each request adds its share
-          // under each variant to that variant's tenant histogram
-          // per nonempty batch: k0 of each variant, and the segments and phase
-          // (over the batch-start mask, no longer read in this tile)
-          float(*k0s)[kSweepG] = W.k0s;
-          uint16_t* segs = W.segs;
-          if (lane < count && ne) {
-            const uint32_t kb = __builtin_popcountll(ne_ball & ((1ull << lane) - 1ull));
-            const BatchAcc a = W.acc[kb];
-            const int64_t n = (int64_t)lo_next - lo;
-            const bool prefill = (a.p != (uint64_t)n) || ((a.cz >> 48) != 0);
-            float k0[kSweepG];
-            segs[kb] = (uint16_t)sweep_batch<NV>(V, n, a.p, a.cz & kCMask, a.q, prefill, k0);
-            for (int g = 0; g < NV; ++g) k0s[kb][g] = k0[g];
-          }
-          wave_lds_sync();
-          const int32_t TS = P.n_tenants + kHotSlots;  // histogram stride per variant
-          uint32_t kcur = 0xffffffffu;
-          float K[NV][4];
-#pragma unroll
-          for (int q = 0; q < kVec; ++q) {
-            if ((valid[0] >> q) & 1u) {
-              const uint32_t k = ord0[0] + __builtin_popcount(bits[0] & ((2u << q) - 1u)) - 1u;
-              if (k != kcur) {
-                kcur = k;
-                const uint32_t sg = segs[k];
-                const int ph = (int)(sg >> 8);
-#pragma unroll
-                for (int g = 0; g < NV; ++g) {
-                  const int r = 2 * ph + (int)((sg >> g) & 1u);
-                  const float* kr = &s_K[(g * 4 + r) * 3];
-                  K[g][0] = k0s[k][g];
-                  K[g][1] = kr[0];
-                  K[g][2] = kr[1];
-                  K[g][3] = kr[2];
-                }
-              }
-              const float pf = (float)pv[0][q], cf = (float)cv[0][q], pp = pf * pf;
-              int32_t e = tv[0][q];
-#pragma unroll
-              for (int h = 0; h < kHot; ++h)
-                if (tv[0][q] == hot[h]) e = P.n_tenants + h * kHotRep + (lane & (kHotRep - 1));
-              double* ht = s_hist + e;
-              // all NV rows: rows past V.n are scratch, never flushed
-#pragma unroll
-              for (int g = 0; g < NV; ++g)
-                atomicAdd(ht + g * TS,
-                          (double)fmaf(K[g][3], pp, fmaf(K[g][2], cf, fmaf(K[g][1], pf, K[g][0]))));
-            }
-          }
-          wave_lds_sync();
-        } else {
+        {
           // ---- per batch (lane j holds batch b+j): the model
           if (lane < count) {
             const int64_t bg = b + lane;
@@ -950,23 +786,7 @@ __global__ __launch_bounds__(kWG, (MODE == MODE_SWEEP && NV == 4) ? 2 : 1) void 
     chunk = k < (uint64_t)(P.n_chunks - workers) ? workers + (int64_t)k : P.n_chunks;
   }
 
-  if constexpr (MODE == MODE_SWEEP) {
-    // fold the hot tenants' replicas (fixed order), then flush n_tenants
-    // entries per variant
-    __syncthreads();
-    const int32_t T = P.n_tenants, TS = T + kHotSlots;
-    for (int i = tid; i < V.n * kHot; i += kWG) {
-      const int g = i / kHot, h = i % kHot;
-      if (hot[h] >= 0) {
-        double acc = s_hist[g * TS + hot[h]];
-        for (int r = 0; r < kHotRep; ++r) acc += s_hist[g * TS + T + h * kHotRep + r];
-        s_hist[g * TS + hot[h]] = acc;
-      }
-    }
-    __syncthreads();
-    double* dst = P.partials + (int64_t)blockIdx.x * V.n * T;
-    for (int i = tid; i < V.n * T; i += kWG) dst[i] = s_hist[(i / T) * TS + i % T];
-  } else if (HIST == HIST_LDS) {
+  if (HIST == HIST_LDS) {
     // fold the replicas in a fixed order
     __syncthreads();
     const int32_t T = P.n_tenants;
@@ -1049,57 +869,6 @@ __global__ __launch_bounds__(kWG) void k_admit(const int64_t* __restrict__ sums,
   if (delta) delta[j] = (float)(t1 - t0);
   if (share) share[j] = (float)f;
   if (regime) regime[j] = (uint8_t)(2 * ph1 + seg);
-}
-
-// ------------------------------------------------------ hot tenants
-
-// counts[u] += number of requests of tenant u (counts cleared beforehand);
-// a per-workgroup LDS histogram, then one global atomic per tenant.
-__global__ __launch_bounds__(kWG) void k_tenant_count(const int32_t* __restrict__ tenant,
-                                                      int64_t n, int32_t T,
-                                                      unsigned long long* __restrict__ counts) {
-  extern __shared__ unsigned int s_cnt[];
-  for (int u = threadIdx.x; u < T; u += kWG) s_cnt[u] = 0u;
-  __syncthreads();
-  const int64_t stride = (int64_t)gridDim.x * kWG;
-  for (int64_t i = (int64_t)blockIdx.x * kWG + threadIdx.x; i < n; i += stride)
-    atomicAdd(&s_cnt[tenant[i]], 1u);
-  __syncthreads();
-  for (int u = threadIdx.x; u < T; u += kWG)
-    if (s_cnt[u]) atomicAdd(&counts[u], (unsigned long long)s_cnt[u]);
-}
-
-// hot[0..kHot) = the most frequent tenants in decreasing count (ties: the
-// smaller id first); -1 where fewer tenants have requests.  One workgroup.
-__global__ __launch_bounds__(kWG) void k_hot_tenants(const unsigned long long* __restrict__ counts,
-                                                     int32_t T, int32_t* __restrict__ hot) {
-  __shared__ unsigned long long s_best[kWG / 64];
-  __shared__ int32_t s_hot[kHot];
-  const int tid = threadIdx.x, lane = tid & 63;
-  for (int h = 0; h < kHot; ++h) {
-    // key: count (saturated to 32 bits) above the complement of the id
-    unsigned long long best = 0;
-    for (int u = tid; u < T; u += kWG) {
-      bool taken = false;
-      for (int j = 0; j < h; ++j) taken |= (s_hot[j] == u);
-      const unsigned long long c = counts[u] < 0xffffffffull ? counts[u] : 0xffffffffull;
-      const unsigned long long key = (c << 32) | (unsigned long long)(0xffffffffu - (uint32_t)u);
-      if (!taken && c > 0 && key > best) best = key;
-    }
-    for (int m = 32; m >= 1; m >>= 1) {
-      const unsigned long long o = __shfl_xor(best, m, 64);
-      best = o > best ? o : best;
-    }
-    if (lane == 0) s_best[tid >> 6] = best;
-    __syncthreads();
-    if (tid == 0) {
-      unsigned long long b = 0;
-      for (int w = 0; w < kWG / 64; ++w) b = s_best[w] > b ? s_best[w] : b;
-      s_hot[h] = b ? (int32_t)(0xffffffffu - (uint32_t)(b & 0xffffffffull)) : -1;
-    }
-    __syncthreads();
-  }
-  if (tid < kHot) hot[tid] = s_hot[tid];
 }
 
 __global__ void k_zero_u64(unsigned long long* __restrict__ x, int64_t n) {

@@ -24,8 +24,8 @@ LLMV_P_MAX = 1 << 20
 LLMV_BATCH_MAX = 1 << 22
 LLMV_TENANTS_MAX = 1 << 24
 
-EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_attribute",
-           "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
+EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_sweep_workspace_size",
+           "llmv_attribute", "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
            "llmv_batch_sums", "llmv_admit", "llmv_fit_workspace_size", "llmv_fit",
            "llmv_fit_metrics", "llmv_shape_constants_ext", "llmv_attribute_ext",
            "llmv_last_error", "llmv_set_kernel_events")
@@ -66,6 +66,8 @@ def load(path: str = LIB_PATH):
             lib.llmv_shape_constants.argtypes = [P, P]
             lib.llmv_workspace_size.argtypes = [i64, i64, i32]
             lib.llmv_workspace_size.restype = sz
+            lib.llmv_sweep_workspace_size.argtypes = [i64, i64, i32]
+            lib.llmv_sweep_workspace_size.restype = sz
             lib.llmv_attribute.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
             lib.llmv_attribute_sweep.argtypes = [P, P, i32, P, i32, i32, P, P, sz, P]
             lib.llmv_features.argtypes = [P, P, P, P, P, sz, P]
@@ -157,6 +159,10 @@ def llmv_shape_constants(shape=None):
 
 def llmv_workspace_size(n_batches: int, n_requests: int, n_tenants: int) -> int:
     return int(load().llmv_workspace_size(n_batches, n_requests, n_tenants))
+
+
+def llmv_sweep_workspace_size(n_batches: int, n_requests: int, n_tenants: int) -> int:
+    return int(load().llmv_sweep_workspace_size(n_batches, n_requests, n_tenants))
 
 
 def llmv_attribute(trace: DeviceTrace, shape, coeffs, latency=None, regime=None, share=None,
@@ -313,6 +319,12 @@ def workspace(n_batches: int, n_requests: int, n_tenants: int, device="cuda"):
     return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
 
 
+def sweep_workspace(n_batches: int, n_requests: int, n_tenants: int, device="cuda"):
+    """A device workspace tensor of llmv_sweep_workspace_size bytes."""
+    n = llmv_sweep_workspace_size(n_batches, n_requests, n_tenants)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+
+
 def attribute(trace: DeviceTrace, shape, coeffs, n_tenants: int = 0,
               outputs=("latency", "regime", "share", "tenant_sums"), ws=None):
     """Allocates the requested outputs and runs llmv_attribute."""
@@ -340,7 +352,7 @@ def attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, ws=None)
     n_co = int(np.asarray(coeffs).reshape(-1, 20).shape[0])
     out = torch.empty((n_sh, n_co, n_tenants), dtype=torch.float64, device=trace.p.device)
     if ws is None:
-        ws = workspace(trace.n_batches, trace.n_requests, n_tenants, trace.p.device)
+        ws = sweep_workspace(trace.n_batches, trace.n_requests, n_tenants, trace.p.device)
     llmv_attribute_sweep(trace, shapes if shapes is not None else [None], coeffs, n_tenants,
                          out, ws)
     return out

@@ -459,12 +459,16 @@ def test_sweep_small(L):
                                    ("tenant_sums",))["tenant_sums"]
             e = parity.rel_err(out[s, v], ref)
             assert e.max() <= parity.RTOL, (s, v, e.max())
-    # the same numbers as single attribution calls
+    # single attribution calls give the same sums up to fp32 rounding: there
+    # each share is 4 fp32 operations (<= 4 ulp) before the fp64 sum; the sweep
+    # rounds a group's sums to fp32 (1 ulp) and evaluates k0*n + k1*P + k2*C +
+    # k3*Q in 4 fp32 operations (<= 4 ulp); with nonnegative terms both stay
+    # within 5 * 2^-24 of the exact sum over the same fp32 constants
     import torch
     dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
     one = L.attribute(dt, shapes[1], co[3], tr.n_tenants, ("tenant_sums",))["tenant_sums"]
     torch.cuda.synchronize()
-    np.testing.assert_allclose(out[1, 3], one.cpu().numpy(), rtol=1e-12)
+    np.testing.assert_allclose(out[1, 3], one.cpu().numpy(), rtol=10 * 2.0**-24)
 
 
 def skewed_tenants(rng, N, T, s=1.2):
@@ -515,6 +519,61 @@ def test_sweep_unit_shape_and_hand_coeffs(L):
     th = coeff_vec(HAND["base_coeffs"])
     out = run_sweep(L, tr, None, np.stack([th, th]))
     assert list(out[0, 0]) == tt["tenant_sums"] and list(out[0, 1]) == tt["tenant_sums"]
+
+
+def sweep_edge_trace(case):
+    """Traces for the sweep's (batch, tenant) groups: batches split by the
+    2048-request build slices (a 300000-request one among them), slices
+    that end exactly on a batch end, empty batches at both ends, no
+    requests at all, and batches with more distinct tenants than the
+    per-wave hash table holds."""
+    rng = np.random.default_rng(sum(map(ord, case)) + 11)
+    if case == "split-batches-skewed":
+        sizes = np.array([0, 0, 2048, 0, 4095, 1, 300000, 0, 0]
+                         + list(rng.integers(0, 400, 500)) + [0, 0, 0])
+        tr = random_fill(rng, sizes, n_tenants=1024)
+        return tracegen.Trace(tr.offsets, tr.p, tr.c, skewed_tenants(rng, tr.n_requests, 1024),
+                              1024, None)
+    if case == "slice-aligned":
+        return random_fill(rng, np.array([2048, 1024, 1024, 0, 2048, 0, 0]), n_tenants=7)
+    if case == "no-requests":
+        return random_fill(rng, np.zeros(40, np.int64), n_tenants=5)
+    if case == "many-tenants-per-batch":
+        return random_fill(rng, np.array([5000] * 40), n_tenants=4096)
+    raise KeyError(case)
+
+
+@pytest.mark.parametrize("case", ["split-batches-skewed", "slice-aligned", "no-requests",
+                                  "many-tenants-per-batch"])
+def test_sweep_group_edges(L, case):
+    tr = sweep_edge_trace(case)
+    co = tracegen.sweep_coeffs(tracegen.base_coeffs(78), 5)
+    shapes = [tracegen.SHAPES["qwen2.5-32b"]]
+    say(f"[sweep edge] {case}: nB={tr.n_batches} N={tr.n_requests} T={tr.n_tenants}")
+    out = run_sweep(L, tr, shapes, co)
+    for v in range(5):
+        ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shapes[0], co[v], tr.n_tenants,
+                               ("tenant_sums",))["tenant_sums"]
+        assert np.array_equal(out[0, v][ref == 0], ref[ref == 0]), (case, v)
+        if tr.n_requests:
+            e = parity.rel_err(out[0, v], ref)
+            assert e.max() <= parity.RTOL, (case, v, e.max())
+
+
+def test_sweep_refuses_a_small_workspace(L):
+    """llmv_workspace_size's bytes do not hold the groups: EWORKSPACE, and
+    the output is left alone."""
+    import torch
+    tr = tracegen.config_trace("whatif-sweep", 300)
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    co = tracegen.sweep_coeffs(tracegen.config_coeffs("whatif-sweep"), 2)
+    out = torch.full((1, 2, tr.n_tenants), -1.0, dtype=torch.float64, device="cuda")
+    ws = L.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+    with pytest.raises(L.LlmvError) as e:
+        L.llmv_attribute_sweep(dt, [tr.shape], co, tr.n_tenants, out, ws)
+    assert e.value.code == L.LLMV_EWORKSPACE
+    torch.cuda.synchronize()
+    assert bool((out == -1.0).all())
 
 
 def test_sweep_full_size_sampled(L):

@@ -244,6 +244,23 @@ def test_fit_workspace_size(llmv):
     assert lib.llmv_fit_workspace_size(1) == a + 256
 
 
+def test_sweep_workspace_size(llmv):
+    """The sweep's workspace: the common one (with a tenant histogram per
+    setting of a pass) plus 20 bytes per request for the (batch, tenant)
+    groups, 32 bytes per batch for their offsets and the exact batch sums."""
+    lib = llmv.load()
+    nB, N, T = 10_000, 1 << 24, 1024  # N large enough for the largest grid
+    base = lib.llmv_sweep_workspace_size(nB, N, T)
+    assert base % 256 == 0
+    assert base >= lib.llmv_workspace_size(nB, N, T) + 20 * N
+    dn = lib.llmv_sweep_workspace_size(nB, N + (1 << 20), T) - base
+    assert 20 << 20 <= dn <= (20 << 20) + 3 * 8 * ((1 << 20) // 2048) + 8 * 256
+    db = lib.llmv_sweep_workspace_size(nB + (1 << 16), N, T) - base
+    assert 32 << 16 <= db <= (32 << 16) + 3 * 256
+    assert lib.llmv_sweep_workspace_size(0, 0, 1) > 0
+    assert lib.llmv_sweep_workspace_size(-5, -5, -5) == lib.llmv_sweep_workspace_size(0, 0, 0)
+
+
 def test_python_binding_refuses_without_library(tmp_path):
     from paper_2608_08382_amd import llmv as mod
     saved = mod._lib
