@@ -85,12 +85,14 @@ struct Layout {
 };
 
 // Chunks for `workers` wave workers over n requests.  When a worker's share
-// is at least kMinDynShare requests: kStaticEighths/8 of the requests in one
-// static chunk per worker, the rest in up to kDynPerWorker claimed chunks
-// per worker of at least kMinChunk requests.  Otherwise one static chunk per
+// is at least kMinDynShare requests: kStaticEighths/8 of the requests in
+// static chunks, the rest in up to kDynPerWorker claimed chunks per worker of
+// at least kMinChunk requests.  The static part is one chunk per worker, or
+// with `pieces` chunks of kPiece requests dealt round-robin (neighbouring
+// waves then stream neighbouring memory).  Otherwise one static chunk per
 // worker and no claims (a claim is a device-wide atomic on one counter;
 // thousands of them cost more than a short launch can win back).
-ChunkMap chunk_map(int64_t n, int64_t workers) {
+ChunkMap chunk_map(int64_t n, int64_t workers, bool pieces) {
   ChunkMap m{};
   m.n_static = workers;
   m.s2 = 1;
@@ -101,25 +103,32 @@ ChunkMap chunk_map(int64_t n, int64_t workers) {
     m.n_chunks = workers;
     return m;
   }
-  m.s1 = n / 8 * kStaticEighths / workers;
-  m.F = m.s1 * workers;
+  const int64_t n_static = n / 8 * kStaticEighths / kPiece;
+  if (pieces && n_static >= workers) {
+    m.n_static = n_static;
+    m.s1 = kPiece;
+  } else {
+    m.s1 = n / 8 * kStaticEighths / workers;
+  }
+  m.F = m.s1 * m.n_static;
   const int64_t rest = n - m.F;
   int64_t dyn = (int64_t)kDynPerWorker * workers;
   if (dyn > rest / kMinChunk) dyn = rest / kMinChunk;
   if (dyn < 1) dyn = 1;
   m.s2 = (rest + dyn - 1) / dyn;
   if (m.s2 < 1) m.s2 = 1;
-  m.n_chunks = workers + dyn;
+  m.n_chunks = m.n_static + dyn;
   return m;
 }
 
-// Workspace layout shared by every entry point; rows = histograms per
-// workgroup (settings per pass in the what-if sweep, else 1).
-Layout layout(int64_t grid, int32_t T, int rows = 1) {
+// Workspace layout shared by every entry point for n requests; rows =
+// histograms per workgroup (settings per pass in the what-if sweep, else 1).
+Layout layout(int64_t n, int32_t T, int rows = 1) {
   Layout L{};
   size_t o = 0;
-  L.wg_first = o;  // first batch of each chunk
-  o += align_up((size_t)(grid * kWaves * (1 + kDynPerWorker) + 1) * sizeof(int64_t));
+  const int64_t grid = grid_max_for(n);
+  L.wg_first = o;  // first batch of each chunk (chunk_map's n_chunks + 1 at most)
+  o += align_up((size_t)(n / kPiece + grid * kWaves * (1 + kDynPerWorker) + 1) * sizeof(int64_t));
   L.claims = o;
   o += align_up(sizeof(unsigned long long));
   L.partials = o;  // [grid][rows][T]
@@ -227,7 +236,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   int rc = device_cus(&cus);
   if (rc) return rc;
   const int32_t Tl = want_tenant ? T : 0;
-  const Layout L = layout(grid_max_for(tr->n_requests), Tl);
+  const Layout L = layout(tr->n_requests, Tl);
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
   const int hist = !want_tenant ? HIST_NONE : (lds_hist(T) ? HIST_LDS : HIST_GLOBAL);
@@ -243,6 +252,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
     // workgroup's tenant histogram is the result (no reduction).
     P.split_by_count = 1;
     P.n_chunks = kWaves;
+    P.n_static = kWaves;
     P.wg_first = nullptr;
     P.claims = nullptr;
     P.partials = hist == HIST_LDS ? P.tenant_sums : nullptr;
@@ -258,12 +268,13 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   const int n_chunks = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
-  const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves);
+  const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves, true);
   P.wg_first = wg_first;
   P.split_by_count = 0;
   P.claims = (unsigned long long*)(base + L.claims);
   P.claim_base = 0;
   P.n_chunks = cm.n_chunks;
+  P.n_static = cm.n_static;
   P.partials = hist == HIST_LDS ? (double*)(base + L.partials) : nullptr;
 
   rc = partition(tr, cm, wg_first, P.claims, stream);
@@ -339,14 +350,14 @@ int llmv_shape_constants(const llmv_shape* shape, double S[4]) {
 size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
   (void)n_batches;
   const int64_t n = n_requests > 0 ? n_requests : 0;
-  return layout(grid_max_for(n), n_tenants > 0 ? n_tenants : 0).total;
+  return layout(n, n_tenants > 0 ? n_tenants : 0).total;
 }
 
 size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
   const int64_t nB = n_batches > 0 ? n_batches : 0;
   const int64_t n = n_requests > 0 ? n_requests : 0;
   const int32_t T = n_tenants > 0 ? n_tenants : 0;
-  const Layout L = layout(grid_max_for(n), T, lds_hist(T) ? sweep_group(T) : 1);
+  const Layout L = layout(n, T, lds_hist(T) ? sweep_group(T) : 1);
   return group_layout(L.total, nB, n).total;
 }
 
@@ -414,7 +425,7 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   // One pass over the groups per G consecutive settings (shape-major, as in
   // out); each pass keeps G tenant histograms in LDS.
   const int G = sweep_group(n_tenants);
-  const Layout L = layout(grid_max_for(N), n_tenants, G);
+  const Layout L = layout(N, n_tenants, G);
   const GroupLayout GL = group_layout(L.total, nB, N);
   rc = check_ws(ws, ws_bytes, GL.total);
   if (rc) return rc;
@@ -494,7 +505,7 @@ int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int3
   // the passes: the chunks of k_tiles over the batches; every launch takes
   // exactly n_chunks claims (one per chunk it runs, the static ones
   // included), so launch i starts at claim i * n_chunks
-  const ChunkMap cm = chunk_map(N, grid * kWaves);
+  const ChunkMap cm = chunk_map(N, grid * kWaves, false);  // one static chunk per wave
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   rc = partition(trace, cm, wg_first, claims, st);
   if (rc) return rc;
@@ -612,7 +623,7 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
   int cus = 0;
   int rc = device_cus(&cus);
   if (rc) return rc;
-  const Layout L = layout(grid_max_for(n), n_tenants);
+  const Layout L = layout(n, n_tenants);
   rc = check_ws(ws, ws_bytes, L.total);
   if (rc) return rc;
   char* base = (char*)ws;
@@ -650,7 +661,7 @@ int llmv_validate(const llmv_trace* trace, int32_t n_tenants, void* ws, size_t w
   if (trace->tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
     return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
   hipStream_t s = (hipStream_t)stream;
-  const Layout L = layout(grid_max_for(trace->n_requests), 0);
+  const Layout L = layout(trace->n_requests, 0);
   rc = check_ws(ws, ws_bytes, L.flag + sizeof(int));
   if (rc) return rc;
   int* flag = (int*)((char*)ws + L.flag);

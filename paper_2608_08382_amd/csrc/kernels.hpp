@@ -51,11 +51,13 @@ constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;  // requests in static chunk
 constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave worker, at most
 constexpr int64_t kMinChunk = 4 * kCap;              // requests per claimed chunk, at least
 constexpr int64_t kMinDynShare = 32 * kCap;          // requests per worker for claimed chunks
+constexpr int64_t kPiece = 16 * kCap;                // requests per static piece (tile kernel)
 
-// Chunks of the tile kernel's work.  Chunk w < n_static (one per wave
-// worker, taken statically) starts at request w*s1; chunk n_static + j
-// (claimed) starts at request F + j*s2, F = n_static*s1.  A chunk holds the
-// batches whose start offset lies in [its start, the next chunk's start).
+// Chunks of the tile kernel's work.  Chunk w < n_static (static) starts at
+// request w*s1; chunk n_static + j (claimed) starts at request F + j*s2,
+// F = n_static*s1.  A chunk holds the batches whose start offset lies in
+// [its start, the next chunk's start).  Wave worker w takes the static
+// chunks w, w + W, ... (W workers, n_static >= W), then claims.
 struct ChunkMap {
   int64_t s1, s2, F, n_static, n_chunks;
   // Number of chunks that start at or before request x (x >= 0).
@@ -88,6 +90,7 @@ struct Params {
   unsigned long long* claims;  // chunk claim counter
   uint64_t claim_base;      // counter value when this launch starts
   int64_t n_chunks;
+  int64_t n_static;         // chunks taken statically, round-robin (>= the wave workers)
   int32_t split_by_count;   // one workgroup, no chunk table: wave w takes batches
                             // [w*nB/4, (w+1)*nB/4) (small traces, one launch)
   float* latency;           // [nB] or null
@@ -501,7 +504,7 @@ __device__ __forceinline__ void store_round(const Params& P, float* stage, int64
     const int32_t x = s0 + e;              // slot within the tile
     const float* src = &stage[(e / kVec) * kStagePitch + (e % kVec)];
     if (x >= xf && x + 4 <= L) {
-      *(v4f*)(P.share + ra + x) = *(const v4f*)src;
+      __builtin_nontemporal_store(*(const v4f*)src, (v4f*)(P.share + ra + x));  // not re-read
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -607,19 +610,54 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
   if (HIST == HIST_LDS) s_hist_lane = s_hist + (lane & (P.hist_rep - 1)) * P.n_tenants;
   __syncthreads();
 
-  // the first chunk of each wave is its static one; later ones are claimed
+  // Wave w runs the static chunks w, w + W, ..., then claimed ones.  The
+  // next chunk's batch range and offsets window are loaded during the
+  // current chunk's first tiles: a static one is known at once, a claimed
+  // one once the claim issued at the start of the current chunk returns (a
+  // claim is issued for the last static chunk and every claimed chunk, so a
+  // launch takes W + n_chunks - n_static claims).
   const int64_t workers = (int64_t)gridDim.x * kWaves;
+  const bool dyn = P.n_chunks > P.n_static;
+  auto first_batch = [&](int64_t ch) {
+    return P.split_by_count ? P.nB * ch / workers : uni(P.wg_first[ch]);
+  };
+  // offsets window: lane j holds offsets[x0 + j] for j <= min(kTileBatches, x1 - x0)
+  auto window = [&](int64_t x0, int64_t x1) {
+    return (x0 < x1 && lane <= min((int64_t)kTileBatches, x1 - x0)) ? P.off[x0 + lane] : (int64_t)0;
+  };
+  // claim k of this launch names chunk n_static + k; past the last chunk, stop
+  auto claimed_chunk = [&](unsigned long long cl) {
+    const uint64_t k = readlane_u64((uint64_t)cl, 0) - P.claim_base;
+    return (dyn && k < (uint64_t)(P.n_chunks - P.n_static)) ? P.n_static + (int64_t)k : P.n_chunks;
+  };
+  auto claim_next = [&](int64_t ch) {
+    unsigned long long cl = ~0ull;
+    if (dyn && ch < P.n_chunks && ch + workers >= P.n_static && lane == 0)
+      cl = atomicAdd(P.claims, 1ull);
+    return cl;
+  };
   int64_t chunk = (int64_t)blockIdx.x * kWaves + (tid >> 6);
+  int64_t cb0 = 0, cb1 = 0, cwv = 0;  // the chunk's batch range and first window
+  if (chunk < P.n_chunks) {
+    cb0 = first_batch(chunk);
+    cb1 = first_batch(chunk + 1);
+    cwv = window(cb0, cb1);
+  }
+  unsigned long long claim = claim_next(chunk);
   while (chunk < P.n_chunks) {
-    // claim the next chunk now: the value is first read once this one is done
-    unsigned long long claim = ~0ull;
-    if (P.n_chunks > workers && lane == 0) claim = atomicAdd(P.claims, 1ull);
-    const int64_t bw0 = P.split_by_count ? P.nB * chunk / workers : uni(P.wg_first[chunk]);
-    const int64_t bw1 = P.split_by_count ? P.nB * (chunk + 1) / workers : uni(P.wg_first[chunk + 1]);
+    const int64_t bw0 = cb0, bw1 = cb1;
     int64_t b = bw0;
-    // offsets window: lane j holds offsets[b + j] for j <= min(kTileBatches, bw1 - b)
-    int64_t wv = (b < bw1 && lane <= min((int64_t)kTileBatches, bw1 - b)) ? P.off[b + lane] : 0;
+    int64_t wv = cwv;
     int64_t r0 = uni(readlane_i64(wv, 0));  // first request of batch b
+    // the next chunk: 0 = not known yet, 1 = its range loaded, 2 = its window too
+    int64_t next = P.n_chunks, nb0 = 0, nb1 = 0, nwin = 0;
+    int known = 0;
+    if (chunk + workers < P.n_static) {  // a static successor: known now
+      next = chunk + workers;
+      nb0 = first_batch(next);
+      nb1 = first_batch(next + 1);
+      known = 1;
+    }
 
     while (b < bw1) {
       // ---- tile: the longest run of whole batches from b within kTile slots
@@ -780,10 +818,33 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
       b = e;
       r0 = r1;
       wv = nwv;
+      // one step toward the next chunk per tile
+      if (known == 1) {
+        if (next < P.n_chunks) nwin = window(nb0, nb1);
+        known = 2;
+      } else if (known == 0) {
+        next = claimed_chunk(claim);
+        if (next < P.n_chunks) {
+          nb0 = first_batch(next);
+          nb1 = first_batch(next + 1);
+        }
+        known = 1;
+      }
     }
-    // claim k of this launch names chunk workers + k; past the last chunk, stop
-    const uint64_t k = readlane_u64((uint64_t)claim, 0) - P.claim_base;
-    chunk = k < (uint64_t)(P.n_chunks - workers) ? workers + (int64_t)k : P.n_chunks;
+    if (known == 0) {
+      next = claimed_chunk(claim);
+      if (next < P.n_chunks) {
+        nb0 = first_batch(next);
+        nb1 = first_batch(next + 1);
+      }
+      known = 1;
+    }
+    if (known == 1 && next < P.n_chunks) nwin = window(nb0, nb1);
+    chunk = next;
+    cb0 = nb0;
+    cb1 = nb1;
+    cwv = nwin;
+    claim = claim_next(chunk);
   }
 
   if (HIST == HIST_LDS) {
