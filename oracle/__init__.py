@@ -103,12 +103,14 @@ class Oracle:
                                       P, P, P, P, P, P, P, P]
         lib.orc_tenant_sums.argtypes = [P, P, i64, i32, P]
         lib.orc_batch_sums.argtypes = [i64, i64, P, P, P, P, P]
+        lib.orc_batch_sums_ext.argtypes = [i64, i64, P, P, P, P, P]
         lib.orc_admit.argtypes = [i64, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
         lib.orc_shape_constants_ext.argtypes = [P, P]
         lib.orc_attribute_ext.argtypes = [i64, i64, P, P, P, P, P, P, i32,
                                           P, P, P, P, P, P, P, P]
         for f in ("orc_shape_constants", "orc_validate", "orc_features",
-                  "orc_attribute", "orc_tenant_sums", "orc_batch_sums", "orc_admit",
+                  "orc_attribute", "orc_tenant_sums", "orc_batch_sums", "orc_batch_sums_ext",
+                  "orc_admit",
                   "orc_shape_constants_ext", "orc_attribute_ext"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
@@ -190,6 +192,18 @@ class Oracle:
                                        _ptr(phase)), "batch_sums")
         return sums, phase
 
+    def batch_sums_ext(self, offsets, p, c):
+        """Returns (sums [5, nB] int64 = (|B|, sum p, sum c, sum p^2, sum p*c),
+        phase [nB] uint8)."""
+        off = _arr(offsets, np.int64)
+        p, c = _arr(p, np.int32), _arr(c, np.int32)
+        nB, N = len(off) - 1, len(p)
+        sums = np.zeros((5, nB), np.int64)
+        phase = np.zeros(nB, np.uint8)
+        _check(self.lib.orc_batch_sums_ext(nB, N, _ptr(off), _ptr(p), _ptr(c), _ptr(sums),
+                                           _ptr(phase)), "batch_sums_ext")
+        return sums, phase
+
     def admit(self, p, c, cand_p, cand_c, shape, coeffs) -> dict:
         """Admission query for the batch of requests (p, c) and one candidate
         request (cand_p, cand_c): T_after, delta, share, share_alt, TM_after,
@@ -261,6 +275,10 @@ def tenant_sums(tenant, share, n_tenants):
 
 def batch_sums(offsets, p, c):
     return default().batch_sums(offsets, p, c)
+
+
+def batch_sums_ext(offsets, p, c):
+    return default().batch_sums_ext(offsets, p, c)
 
 
 def admit(p, c, cand_p, cand_c, shape, coeffs):

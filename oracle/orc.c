@@ -362,6 +362,24 @@ int orc_batch_sums(int64_t nB, int64_t N, const int64_t *off, const int32_t *p,
   return ORC_OK;
 }
 
+int orc_batch_sums_ext(int64_t nB, int64_t N, const int64_t *off, const int32_t *p,
+                       const int32_t *c, int64_t *sums, uint8_t *phase) {
+  int rc = orc_batch_sums(nB, N, off, p, c, sums, phase);
+  if (rc != ORC_OK || !sums) return rc;
+  for (int64_t b = 0; b < nB; ++b) {
+    /* sum of p_i*c_i, exact: each product is below 2^51; the sum is checked
+     * against 2^63 as it grows */
+    int64_t R = 0;
+    for (int64_t i = off[b]; i < off[b + 1]; ++i) {
+      const int64_t pc = (int64_t)p[i] * (int64_t)c[i];
+      if (R > INT64_MAX - pc) return ORC_ERANGE;
+      R += pc;
+    }
+    sums[4 * nB + b] = R;
+  }
+  return ORC_OK;
+}
+
 int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
               const orc_shape *shape, const float coeffs[20], double *T_after,
               double *delta, double *share, double *share_alt, double *TM_after,

@@ -136,6 +136,12 @@ int orc_attribute_ext(int64_t n_batches, int64_t n_requests, const int64_t *offs
 int orc_batch_sums(int64_t n_batches, int64_t n_requests, const int64_t *offsets,
                    const int32_t *p, const int32_t *c, int64_t *sums, uint8_t *phase);
 
+/* orc_batch_sums plus the extended model's cross sum (readings X1-X3):
+ *   sums[5][nB] = (|B|, sum p, sum c, sum p^2, sum p*c); ORC_ERANGE when a
+ *   batch's sum p*c reaches 2^63. */
+int orc_batch_sums_ext(int64_t n_batches, int64_t n_requests, const int64_t *offsets,
+                       const int32_t *p, const int32_t *c, int64_t *sums, uint8_t *phase);
+
 /* Admission query (Sec. 1: admission control that rejects or defers a
  * request whose share would exceed its budget; Sec. 2 Problem formulation).
  * B is the batch of the n requests (p, c) (n may be 0); B' is B with one more

@@ -11,6 +11,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "fit.py")
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
 import test_oracle_fit as pins  # noqa: E402
+import test_oracle_fit_ext as ext_pins  # noqa: E402
 
 MUTANTS = [
     ("ties go to COMP", "seg = np.where(tc > tm, 1, 0)", "seg = np.where(tc >= tm, 1, 0)"),
@@ -22,9 +23,17 @@ MUTANTS = [
     ("relative error over the prediction", "e = (np.abs(yh[pos] - ys[pos]) / ys[pos])",
      "e = (np.abs(yh[pos] - ys[pos]) / yh[pos])"),
     ("kept terms not subtracted",
-     "yf = y[idx] - X[idx][:, kept] @ theta[g * 5 + np.array(kept, int)] if kept else y[idx]",
+     "yf = y[idx] - X[idx][:, kept] @ theta[g * K + np.array(kept, int)] if kept else y[idx]",
      "yf = y[idx]"),
     ("rank judged on raw columns", "D = np.linalg.norm(Xf, axis=0)", "D = np.ones(Xf.shape[1])"),
+    # extended model (F5)
+    ("cross term kept only without contexts", "if ext and np.all(sums[4][idx] == sums[2][idx]):",
+     "if ext and np.all(sums[4][idx] == 0):"),
+    # (Q == P is the same test as P == |B|: both say every p is 1)
+    ("per-request term kept without contexts", "if ext and np.all(sums[1][idx] == sums[0][idx]):",
+     "if ext and np.all(sums[2][idx] == 0):"),
+    ("cross column from C", "S[4] * R", "S[4] * C"),
+    ("per-request column |B|^2", "S[5] * n]", "S[5] * n * n]"),
 ]
 
 
@@ -35,7 +44,22 @@ def load(path, name):
     return mod
 
 
+def ext_battery(F):
+    saved = ext_pins.F
+    try:
+        ext_pins.F = F
+        ext_pins.test_free_columns_by_hand()
+        ext_pins.test_planted_recovery()
+        ext_pins.test_planted_recovery_model_shape()
+        ext_pins.test_reduces_to_the_eq1_fit()
+        ext_pins.test_ols_normal_equations_hold(0)
+        ext_pins.test_metrics_of_the_exact_model()
+    finally:
+        ext_pins.F = saved
+
+
 def battery(F):
+    ext_battery(F)
     saved = pins.F
     try:
         pins.F = F
