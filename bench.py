@@ -302,6 +302,28 @@ def bench_fit(hip, stream, dt, tr, lat, with_oracle):
            "p99": {"prefill": o[0, 2], "decode": o[1, 2], "all": o[2, 2]}}
     log(f"[bench] fit: {rounds} rounds over {tr.n_batches} batches in {ms_fit:.3f} ms "
         f"({res['round_gbps']:.0f} GB/s per round); metrics {ms_met:.3f} ms; r2 {res['r2']}")
+    # the extended model: batch sums with sum p*c, fit of the 28 coefficients,
+    # metrics, on the same measured latencies
+    del sums
+    ws = llmv.workspace(tr.n_batches, tr.n_requests, 0, dev)
+    sums5 = torch.empty((5, tr.n_batches), dtype=torch.int64, device=dev)
+    ms_bs = timed(lambda: llmv.llmv_batch_sums_ext(dt, sums5, phase, ws), reps=3)
+    del ws
+    theta0x = tracegen.ext_coeffs(104).astype(np.float64) * \
+        np.random.default_rng(83).uniform(0.9, 1.1, 28)
+    thetax = torch.empty(28, dtype=torch.float64, device=dev)
+    ms_fx = timed(lambda: llmv.llmv_fit_ext(sums5, phase, tr.shape, y, theta0x, rounds, thetax,
+                                            counts, fws))
+    fittedx = thetax.cpu().numpy().astype(np.float32)
+    ms_mx = timed(lambda: llmv.llmv_fit_metrics_ext(sums5, phase, tr.shape, fittedx, y, out, err,
+                                                    fws))
+    ox = out.cpu().numpy()
+    res["extended"] = {"batch_sums_ms": ms_bs, "fit_ms": ms_fx, "round_ms": ms_fx / rounds,
+                       "round_gbps": 49 * tr.n_batches / (ms_fx / rounds / 1e3) / 1e9,
+                       "metrics_ms": ms_mx, "counts": counts.cpu().tolist(),
+                       "r2": {"prefill": ox[0, 0], "decode": ox[1, 0], "all": ox[2, 0]}}
+    log(f"[bench] fit (extended model): batch sums {ms_bs:.3f} ms; {rounds} rounds in "
+        f"{ms_fx:.3f} ms; metrics {ms_mx:.3f} ms; r2 {res['extended']['r2']}")
     if with_oracle:
         from oracle import fit as F
         nb = 200_000

@@ -199,6 +199,16 @@ int llmv_attribute_sweep(const llmv_trace *trace, const llmv_shape *shapes,
 int llmv_batch_sums(const llmv_trace *trace, int64_t *sums, uint8_t *phase, void *ws,
                     size_t ws_bytes, void *stream);
 
+/* llmv_batch_sums plus the extended model's cross sum (readings X1-X3), the
+ * state llmv_fit_ext and llmv_fit_metrics_ext start from:
+ *   sums    device [5][n_batches] int64: (|B|, sum p, sum c, sum p^2,
+ *           sum p*c); zeros for an empty batch.  sum p*c must stay below
+ *           2^63 (not checked).
+ *   phase   as llmv_batch_sums.
+ * Either output may be NULL.  Workspace as for llmv_attribute. */
+int llmv_batch_sums_ext(const llmv_trace *trace, int64_t *sums, uint8_t *phase, void *ws,
+                        size_t ws_bytes, void *stream);
+
 /* Admission query (Sec. 1: admission control that rejects or defers a
  * request whose share would exceed its budget; Sec. 2 Problem formulation;
  * Eq. 1).  Candidate j, a request (cand_p[j], cand_c[j]), is proposed for
@@ -284,6 +294,26 @@ int llmv_fit(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
 int llmv_fit_metrics(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
                      const llmv_shape *shape, const float coeffs[20], const double *y,
                      float *rel_err, double *out, void *ws, size_t ws_bytes, void *stream);
+
+/* llmv_fit and llmv_fit_metrics for the extended model (Eq. 1 plus a5*S5*
+ * sum p*c and a6*S6*|B|; the feature variants the paper leaves open), with
+ * the same rounds, identifiability rules, metrics and precision:
+ *   sums          device [5][n_batches] int64 as written by
+ *                 llmv_batch_sums_ext (the fifth row is sum p*c).
+ *   theta0, theta fp64 [28], coeffs fp32 [28]: index (phase*2 + segment)*7
+ *                 + k, k = (beta, a1, a2, a3, a4, a5, a6).
+ * Two more coefficients can keep their starting values: a5 when sum p*c ==
+ * sum c in every batch of a set (every request with a context processes one
+ * token: the cross term is the c term), a6 when sum p == |B| (every request
+ * processes one token: the per-request term is the p term).  Shape constants
+ * as llmv_shape_constants_ext.  Workspace: llmv_fit_workspace_size. */
+int llmv_fit_ext(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
+                 const llmv_shape *shape, const double *y, const double theta0[28],
+                 int32_t rounds, double *theta, int64_t *counts, void *ws, size_t ws_bytes,
+                 void *stream);
+int llmv_fit_metrics_ext(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
+                         const llmv_shape *shape, const float coeffs[28], const double *y,
+                         float *rel_err, double *out, void *ws, size_t ws_bytes, void *stream);
 
 /* Request and batch features (Sec. 2.1), structure of arrays:
  *   x_req   device [5][n_requests] fp32, element k of request i at

@@ -204,6 +204,7 @@ typedef void (*TileKernel)(const Params, const NoVars);
 
 TileKernel pick_tiles(int mode, int hist, bool share) {
   if (mode == MODE_FEAT) return k_tiles<MODE_FEAT, HIST_NONE, false>;
+  if (mode == MODE_SUMS) return k_tiles<MODE_SUMS, HIST_NONE, false>;
   if (hist == HIST_NONE)
     return share ? k_tiles<MODE_ATTR, HIST_NONE, true> : k_tiles<MODE_ATTR, HIST_NONE, false>;
   if (hist == HIST_LDS)
@@ -563,6 +564,25 @@ int llmv_batch_sums(const llmv_trace* trace, int64_t* sums, uint8_t* phase, void
   P.bphase = phase;
   if (!sums && !phase) return LLMV_OK;
   return run_tiles(MODE_FEAT, trace, P, NoVars{}, 0, false, false, ws, ws_bytes,
+                   (hipStream_t)stream);
+}
+
+int llmv_batch_sums_ext(const llmv_trace* trace, int64_t* sums, uint8_t* phase, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int rc = check_trace(trace, false);
+  if (rc) return rc;
+  Params P{};
+  rc = shape_constants(nullptr, P.S);
+  if (rc) return rc;
+  P.off = trace->offsets;
+  P.p = trace->p;
+  P.c = trace->c;
+  P.nB = trace->n_batches;
+  P.N = trace->n_requests;
+  P.bsums = sums;
+  P.bphase = phase;
+  if (!sums && !phase) return LLMV_OK;
+  return run_tiles(MODE_SUMS, trace, P, NoVars{}, 0, false, false, ws, ws_bytes,
                    (hipStream_t)stream);
 }
 

@@ -1,6 +1,7 @@
 // fit.hip -- host side of the fitting entry points of the libllmv C ABI
-// (llmv_fit, llmv_fit_metrics; include/llmv.h): argument checks, workspace
-// layout and the launches of the kernels in fit.hpp.
+// (llmv_fit, llmv_fit_metrics and their extended-model forms; include/llmv.h):
+// argument checks, workspace layout and the launches of the kernels in
+// fit.hpp.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -25,8 +26,8 @@ struct FitLayout {
 FitLayout fit_layout(int64_t nB) {
   FitLayout L{};
   size_t o = 0;
-  L.partials = o;  // per-workgroup sums: [grid][kFitVals], or [grid][kMetricVals]
-  o += align_up((size_t)kFitMaxGrid * kFitVals * sizeof(double));
+  L.partials = o;  // per-workgroup sums: [grid][FitCols::kVals], or [grid][kMetricVals]
+  o += align_up((size_t)kFitMaxGrid * kFitValsMax * sizeof(double));
   L.tot1 = o;
   o += align_up(kMetricVals * sizeof(double));
   L.tot2 = o;
@@ -65,25 +66,27 @@ int check_batches(const int64_t* sums, const uint8_t* phase, int64_t nB, const d
   return LLMV_OK;
 }
 
-}  // namespace
+// Shape constants of an NC-column model: S0..S3, and S5, S6 for NC = 7.
+template <int NC>
+int model_shape(const llmv_shape* shape, double S[6]) {
+  for (int k = 0; k < 6; ++k) S[k] = 0.0;
+  return NC == 7 ? shape_constants_ext(shape, S) : shape_constants(shape, S);
+}
 
-extern "C" {
-
-size_t llmv_fit_workspace_size(int64_t n_batches) { return fit_layout(n_batches).total; }
-
-int llmv_fit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
-             const llmv_shape* shape, const double* y, const double theta0[20], int32_t rounds,
-             double* theta, int64_t* counts, void* ws, size_t ws_bytes, void* stream) {
+template <int NC>
+int fit_run(const int64_t* sums, const uint8_t* phase, int64_t n_batches, const llmv_shape* shape,
+            const double* y, const double* theta0, int32_t rounds, double* theta, int64_t* counts,
+            void* ws, size_t ws_bytes, void* stream) {
   int rc = check_batches(sums, phase, n_batches, y);
   if (rc) return rc;
   if (rounds < 0 || rounds > kMaxRounds)
     return fail(LLMV_EINVAL, "rounds=%d outside [0, %d]", rounds, kMaxRounds);
   if (!theta0) return fail(LLMV_EINVAL, "theta0 is NULL");
   if (!theta) return fail(LLMV_EINVAL, "theta is NULL");
-  FitModel M{};
-  rc = shape_constants(shape, M.S);
+  FitModel<NC> M{};
+  rc = model_shape<NC>(shape, M.S);
   if (rc) return rc;
-  for (int i = 0; i < 20; ++i) {
+  for (int i = 0; i < 4 * NC; ++i) {
     if (!std::isfinite(theta0[i])) return fail(LLMV_EINVAL, "theta0[%d] is not finite", i);
     M.th[i] = theta0[i];
   }
@@ -95,33 +98,34 @@ int llmv_fit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
   long long* cnt = counts ? (long long*)counts : (long long*)(base + L.counts);
   hipStream_t s = (hipStream_t)stream;
 
-  hipLaunchKernelGGL(k_fit_init, dim3(1), dim3(64), 0, s, M, theta, cnt);
+  hipLaunchKernelGGL(k_fit_init<NC>, dim3(1), dim3(64), 0, s, M, theta, cnt);
   HIP_TRY(hipGetLastError(), "k_fit_init launch");
   FitShape F{};
-  for (int k = 0; k < 4; ++k) F.S[k] = M.S[k];
+  for (int k = 0; k < 6; ++k) F.S[k] = M.S[k];
   const int grid = fit_grid(n_batches);
   for (int r = 0; r < rounds; ++r) {
-    hipLaunchKernelGGL(k_fit_accum, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, F, y,
-                       (const double*)theta, partials);
+    hipLaunchKernelGGL(k_fit_accum<NC>, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, F,
+                       y, (const double*)theta, partials);
     HIP_TRY(hipGetLastError(), "k_fit_accum launch");
-    hipLaunchKernelGGL(k_fit_solve, dim3(1), dim3(kReduceWG), 0, s,
+    hipLaunchKernelGGL(k_fit_solve<NC>, dim3(1), dim3(kReduceWG), 0, s,
                        (const double*)partials, grid, theta, cnt);
     HIP_TRY(hipGetLastError(), "k_fit_solve launch");
   }
   return LLMV_OK;
 }
 
-int llmv_fit_metrics(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
-                     const llmv_shape* shape, const float coeffs[20], const double* y,
-                     float* rel_err, double* out, void* ws, size_t ws_bytes, void* stream) {
+template <int NC>
+int metrics_run(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+                const llmv_shape* shape, const float* coeffs, const double* y, float* rel_err,
+                double* out, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_batches(sums, phase, n_batches, y);
   if (rc) return rc;
   if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
   if (!out) return fail(LLMV_EINVAL, "out is NULL");
-  FitModel M{};
-  rc = shape_constants(shape, M.S);
+  FitModel<NC> M{};
+  rc = model_shape<NC>(shape, M.S);
   if (rc) return rc;
-  for (int i = 0; i < 20; ++i) {
+  for (int i = 0; i < 4 * NC; ++i) {
     if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
     M.th[i] = (double)coeffs[i];
   }
@@ -142,16 +146,16 @@ int llmv_fit_metrics(const int64_t* sums, const uint8_t* phase, int64_t n_batche
   // and the first pick; then pass 2 for r^2
   hipLaunchKernelGGL(k_select_init, dim3(1), dim3(256), 0, s, sel, hist);
   HIP_TRY(hipGetLastError(), "k_select_init launch");
-  hipLaunchKernelGGL(k_fit_metrics1, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, M, y,
-                     err, partials, hist);
+  hipLaunchKernelGGL(k_fit_metrics1<NC>, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches,
+                     M, y, err, partials, hist);
   HIP_TRY(hipGetLastError(), "k_fit_metrics1 launch");
   hipLaunchKernelGGL(k_fit_metrics_sum, dim3(1), dim3(kReduceWG), 0, s, (const double*)partials,
                      grid, tot1);
   HIP_TRY(hipGetLastError(), "k_fit_metrics_sum launch");
   hipLaunchKernelGGL(k_select_pick, dim3(1), dim3(256), 0, s, sel, hist, (const double*)tot1);
   HIP_TRY(hipGetLastError(), "k_select_pick launch");
-  hipLaunchKernelGGL(k_fit_metrics2, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches, M, y,
-                     (const double*)tot1, partials);
+  hipLaunchKernelGGL(k_fit_metrics2<NC>, dim3(grid), dim3(kFitWG), 0, s, sums, phase, n_batches,
+                     M, y, (const double*)tot1, partials);
   HIP_TRY(hipGetLastError(), "k_fit_metrics2 launch");
   hipLaunchKernelGGL(k_fit_metrics_sum, dim3(1), dim3(kReduceWG), 0, s, (const double*)partials,
                      grid, tot2);
@@ -169,6 +173,41 @@ int llmv_fit_metrics(const int64_t* sums, const uint8_t* phase, int64_t n_batche
                      (const double*)tot2, (const SelState*)sel, out);
   HIP_TRY(hipGetLastError(), "k_fit_metrics_final launch");
   return LLMV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t llmv_fit_workspace_size(int64_t n_batches) { return fit_layout(n_batches).total; }
+
+int llmv_fit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+             const llmv_shape* shape, const double* y, const double theta0[20], int32_t rounds,
+             double* theta, int64_t* counts, void* ws, size_t ws_bytes, void* stream) {
+  return fit_run<5>(sums, phase, n_batches, shape, y, theta0, rounds, theta, counts, ws, ws_bytes,
+                    stream);
+}
+
+int llmv_fit_ext(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+                 const llmv_shape* shape, const double* y, const double theta0[28],
+                 int32_t rounds, double* theta, int64_t* counts, void* ws, size_t ws_bytes,
+                 void* stream) {
+  return fit_run<7>(sums, phase, n_batches, shape, y, theta0, rounds, theta, counts, ws, ws_bytes,
+                    stream);
+}
+
+int llmv_fit_metrics(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+                     const llmv_shape* shape, const float coeffs[20], const double* y,
+                     float* rel_err, double* out, void* ws, size_t ws_bytes, void* stream) {
+  return metrics_run<5>(sums, phase, n_batches, shape, coeffs, y, rel_err, out, ws, ws_bytes,
+                        stream);
+}
+
+int llmv_fit_metrics_ext(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+                         const llmv_shape* shape, const float coeffs[28], const double* y,
+                         float* rel_err, double* out, void* ws, size_t ws_bytes, void* stream) {
+  return metrics_run<7>(sums, phase, n_batches, shape, coeffs, y, rel_err, out, ws, ws_bytes,
+                        stream);
 }
 
 }  // extern "C"

@@ -14,6 +14,9 @@
 //    does; the rest are fitted to y minus the kept terms; a set with fewer
 //    batches than free coefficients, or with (numerically) dependent free
 //    columns, keeps all its coefficients;
+//  * the extended model (Eq. 1 plus a5*S5*sum p*c and a6*S6*|B|) is fitted
+//    the same way with seven columns; a5 keeps its starting value when
+//    sum p*c == sum c in every batch of a set, a6 when sum p == |B|;
 //  * r^2 = 1 - SSE / sum (y - mean y)^2 over the nonempty batches of a phase;
 //  * relative error |yhat - y| / y over nonempty batches with y > 0, rounded
 //    to fp32; percentile p = the ceil(p n)-th smallest (nearest rank).
@@ -33,43 +36,59 @@
 
 namespace llmv {
 
-constexpr int kFitSet = 23;            // per set: X X^T upper triangle (15), X y (5),
-                                       // batches, batches with Q != P, batches with C != 0
-constexpr int kFitVals = 4 * kFitSet;  // the four (phase, segment) sets
+// Accumulators of one (phase, segment) set for NC columns (5: Eq. 1, 7: the
+// extended model): the upper triangle of X^T X, X^T y, the batch count and
+// the identifiability counts (batches with Q != P, C != 0, and for NC = 7
+// R != C, P != |B|).
+template <int NC>
+struct FitCols {
+  static_assert(NC == 5 || NC == 7, "Eq. 1 or the extended model");
+  static constexpr int kTri = NC * (NC + 1) / 2;
+  static constexpr int kFlags = NC == 5 ? 3 : 5;
+  static constexpr int kSet = kTri + NC + kFlags;
+  static constexpr int kVals = 4 * kSet;  // the four (phase, segment) sets
+};
+constexpr int kFitValsMax = FitCols<7>::kVals;
 constexpr int kFitWG = 256;
 constexpr int kReduceWG = 1024;        // threads of the fixed-order column reductions
 constexpr int kMetricVals = 8;         // per phase: n, sum y, m (y > 0), unused; x2 phases
 constexpr int kSelections = 6;         // (prefill, decode, all) x (p90, p99)
 
+// Shape constants: S0..S3, and for the extended model S5, S6.
 struct FitShape {
-  double S[4];
+  double S[6];
 };
 
 // Shape constants and one fp64 coefficient vector theta[phase][segment][k].
+template <int NC>
 struct FitModel {
-  double S[4];
-  double th[20];
+  double S[6];
+  double th[4 * NC];
 };
 
-// Eq. 1 under one coefficient set: the five terms added in order k = 0..4.
-__device__ __forceinline__ double fit_eq1(const double* th, const double X[5]) {
+// One coefficient set: the NC terms added in order k = 0, 1, ...
+template <int NC>
+__device__ __forceinline__ double fit_eq(const double* th, const double X[NC]) {
   double acc = th[0] * X[0];
-  acc = acc + th[1] * X[1];
-  acc = acc + th[2] * X[2];
-  acc = acc + th[3] * X[3];
-  acc = acc + th[4] * X[4];
+#pragma unroll
+  for (int k = 1; k < NC; ++k) acc = acc + th[k] * X[k];
   return acc;
 }
 
-// Eq. 1's feature vector of a batch from its exact sums (Sec. 2.1):
-// (S0, S1*P, S2*C, S3*Q, |B|^2).
+// The feature vector of a batch from its exact sums (Sec. 2.1):
+// (S0, S1*P, S2*C, S3*Q, |B|^2), and for the extended model (S5*R, S6*|B|).
+template <int NC>
 __device__ __forceinline__ void fit_features(const double* S, int64_t n, int64_t P, int64_t C,
-                                             int64_t Q, double X[5]) {
+                                             int64_t Q, int64_t R, double X[NC]) {
   X[0] = S[0];
   X[1] = S[1] * (double)P;
   X[2] = S[2] * (double)C;
   X[3] = S[3] * (double)Q;
   X[4] = (double)n * (double)n;
+  if constexpr (NC == 7) {
+    X[5] = S[4] * (double)R;
+    X[6] = S[5] * (double)n;
+  }
 }
 
 __device__ __forceinline__ double wave_sum_f64(double x) {
@@ -79,21 +98,24 @@ __device__ __forceinline__ double wave_sum_f64(double x) {
 
 // The state of one batch: exact sums, measured latency and phase.
 struct BatchRegs {
-  int64_t n, P, C, Q;
+  int64_t n, P, C, Q, R;
   double y;
   int ph;  // 0 prefill, 1 decode, -1 empty or past the end
 };
 
+// sums: [4][nB] (|B|, P, C, Q), for NC = 7 [5][nB] with R = sum p*c.
+template <int NC>
 __device__ __forceinline__ BatchRegs load_batch(const int64_t* __restrict__ sums,
                                                 const uint8_t* __restrict__ phase,
                                                 const double* __restrict__ y, int64_t nB,
                                                 int64_t b) {
-  BatchRegs r{0, 0, 0, 0, 0.0, -1};
+  BatchRegs r{0, 0, 0, 0, 0, 0.0, -1};
   if (b < nB) {
     r.n = sums[b];
     r.P = sums[nB + b];
     r.C = sums[2 * nB + b];
     r.Q = sums[3 * nB + b];
+    if constexpr (NC == 7) r.R = sums[4 * nB + b];
     r.y = y[b];
     r.ph = r.n == 0 ? -1 : (phase[b] == 0 ? 0 : 1);
   }
@@ -101,11 +123,12 @@ __device__ __forceinline__ BatchRegs load_batch(const int64_t* __restrict__ sums
 }
 
 // Per-workgroup sums of the normal equations of each set under the current
-// coefficients theta (device [20]): partials[block][set*kFitSet + k].
+// coefficients theta (device [4*NC]): partials[block][set*kSet + k].
 // A workgroup walks chunks of kFitWG batches: the chunk is loaded once,
 // coalesced (the next chunk's loads are issued before the current one is
 // processed) and staged in LDS; wave w then folds the chunk's batches of set
-// w (phase w/2, segment w%2) into 23 register accumulators per lane.
+// w (phase w/2, segment w%2) into kSet register accumulators per lane.
+template <int NC>
 __global__ __launch_bounds__(kFitWG) void k_fit_accum(const int64_t* __restrict__ sums,
                                                       const uint8_t* __restrict__ phase,
                                                       int64_t nB, const FitShape F,
@@ -113,58 +136,67 @@ __global__ __launch_bounds__(kFitWG) void k_fit_accum(const int64_t* __restrict_
                                                       const double* __restrict__ theta,
                                                       double* __restrict__ partials) {
   static_assert(kFitWG == 4 * 64, "one wave per (phase, segment) set");
+  using Cols = FitCols<NC>;
+  constexpr int kTri = Cols::kTri, kSet = Cols::kSet;
   __shared__ int64_t s_n[kFitWG], s_P[kFitWG], s_C[kFitWG], s_Q[kFitWG];
+  __shared__ int64_t s_R[NC == 7 ? kFitWG : 1];
   __shared__ double s_y[kFitWG];
   __shared__ int s_ph[kFitWG];
   const int tid = threadIdx.x, lane = tid & 63, set = tid >> 6;
   const int set_phase = set >> 1, set_seg = set & 1;
-  double th[10];  // the two segment sets of this wave's phase
+  double th[2 * NC];  // the two segment sets of this wave's phase
 #pragma unroll
-  for (int i = 0; i < 10; ++i) th[i] = theta[set_phase * 10 + i];
-  double acc[kFitSet];
+  for (int i = 0; i < 2 * NC; ++i) th[i] = theta[set_phase * 2 * NC + i];
+  double acc[kSet];
 #pragma unroll
-  for (int i = 0; i < kFitSet; ++i) acc[i] = 0.0;
+  for (int i = 0; i < kSet; ++i) acc[i] = 0.0;
 
   const int64_t stride = (int64_t)gridDim.x * kFitWG;
   int64_t base = (int64_t)blockIdx.x * kFitWG;
-  BatchRegs cur = load_batch(sums, phase, y, nB, base + tid);
+  BatchRegs cur = load_batch<NC>(sums, phase, y, nB, base + tid);
   for (; base < nB; base += stride) {
     s_n[tid] = cur.n;
     s_P[tid] = cur.P;
     s_C[tid] = cur.C;
     s_Q[tid] = cur.Q;
+    if constexpr (NC == 7) s_R[tid] = cur.R;
     s_y[tid] = cur.y;
     s_ph[tid] = cur.ph;
     __syncthreads();
-    cur = load_batch(sums, phase, y, nB, base + stride + tid);  // next chunk, in flight
+    cur = load_batch<NC>(sums, phase, y, nB, base + stride + tid);  // next chunk, in flight
 #pragma unroll
     for (int k = 0; k < kFitWG / 64; ++k) {
       const int i = k * 64 + lane;
       if (s_ph[i] != set_phase) continue;
-      const int64_t P = s_P[i], C = s_C[i], Q = s_Q[i];
-      double X[5];
-      fit_features(F.S, s_n[i], P, C, Q, X);
+      const int64_t n = s_n[i], P = s_P[i], C = s_C[i], Q = s_Q[i];
+      const int64_t R = NC == 7 ? s_R[i] : 0;
+      double X[NC];
+      fit_features<NC>(F.S, n, P, C, Q, R, X);
       // Roofline max of the two segments; ties stay memory-bound.
-      const int seg = fit_eq1(th + 5, X) > fit_eq1(th, X) ? 1 : 0;
+      const int seg = fit_eq<NC>(th + NC, X) > fit_eq<NC>(th, X) ? 1 : 0;
       if (seg != set_seg) continue;
       const double yb = s_y[i];
       int q = 0;
 #pragma unroll
-      for (int a = 0; a < 5; ++a)
+      for (int a = 0; a < NC; ++a)
 #pragma unroll
-        for (int c = a; c < 5; ++c) acc[q++] += X[a] * X[c];
+        for (int c = a; c < NC; ++c) acc[q++] += X[a] * X[c];
 #pragma unroll
-      for (int a = 0; a < 5; ++a) acc[15 + a] += X[a] * yb;
-      acc[20] += 1.0;
-      acc[21] += Q != P ? 1.0 : 0.0;
-      acc[22] += C != 0 ? 1.0 : 0.0;
+      for (int a = 0; a < NC; ++a) acc[kTri + a] += X[a] * yb;
+      acc[kTri + NC + 0] += 1.0;
+      acc[kTri + NC + 1] += Q != P ? 1.0 : 0.0;
+      acc[kTri + NC + 2] += C != 0 ? 1.0 : 0.0;
+      if constexpr (NC == 7) {
+        acc[kTri + NC + 3] += R != C ? 1.0 : 0.0;
+        acc[kTri + NC + 4] += P != n ? 1.0 : 0.0;
+      }
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < kFitSet; ++i) {
+  for (int i = 0; i < kSet; ++i) {
     const double t = wave_sum_f64(acc[i]);
-    if (lane == 0) partials[(int64_t)blockIdx.x * kFitVals + set * kFitSet + i] = t;
+    if (lane == 0) partials[(int64_t)blockIdx.x * Cols::kVals + set * kSet + i] = t;
   }
 }
 
@@ -195,33 +227,45 @@ __device__ __forceinline__ void reduce_columns(const double* __restrict__ partia
 }
 
 // Solves one set's normal equations over its free coefficients; returns
-// false when the set keeps its coefficients.  A15: the 15 upper-triangle
-// entries of X^T X, r: X^T y.  The free columns are scaled to unit diagonal
-// and factorised by Cholesky; a kept column becomes an identity row (its
-// term is moved to the right-hand side first), so the 5x5 code is fully
-// unrolled and stays in registers.  A pivot below 1e-12 (condition number of
-// the scaled columns beyond ~1e6) counts as dependent columns.
-__device__ inline bool solve_set(const double* A15, const double* r, double cnt, double npq,
-                                 double nc, double th[5]) {
-  const bool kept[5] = {false, false, nc == 0.0, npq == 0.0, false};
-  const int nf = 5 - (kept[2] ? 1 : 0) - (kept[3] ? 1 : 0);
-  if (cnt < (double)nf) return false;
-  double A[5][5];
+// false when the set keeps its coefficients.  A: the upper triangle of
+// X^T X, r: X^T y, f: the batch count and the identifiability counts
+// (FitCols).  The free columns are scaled to unit diagonal and factorised by
+// Cholesky; a kept column becomes an identity row (its term is moved to the
+// right-hand side first), so the code is fully unrolled.  A pivot below
+// 1e-12 (condition number of the scaled columns beyond ~1e6) counts as
+// dependent columns.
+template <int NC>
+__device__ inline bool solve_set(const double* At, const double* r, const double* f,
+                                 double th[NC]) {
+  bool kept[NC];
+#pragma unroll
+  for (int k = 0; k < NC; ++k) kept[k] = false;
+  kept[2] = f[2] == 0.0;  // sum c == 0 in every batch
+  kept[3] = f[1] == 0.0;  // sum p^2 == sum p in every batch
+  if constexpr (NC == 7) {
+    kept[5] = f[3] == 0.0;  // sum p*c == sum c in every batch
+    kept[6] = f[4] == 0.0;  // sum p == |B| in every batch
+  }
+  int nf = 0;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) nf += kept[k] ? 0 : 1;
+  if (f[0] < (double)nf) return false;
+  double A[NC][NC];
   int q = 0;
 #pragma unroll
-  for (int i = 0; i < 5; ++i)
+  for (int i = 0; i < NC; ++i)
 #pragma unroll
-    for (int j = i; j < 5; ++j) {
-      A[i][j] = A15[q];
-      A[j][i] = A15[q];
+    for (int j = i; j < NC; ++j) {
+      A[i][j] = At[q];
+      A[j][i] = At[q];
       ++q;
     }
-  double d[5], b[5];
+  double d[NC], b[NC];
 #pragma unroll
-  for (int i = 0; i < 5; ++i) {
+  for (int i = 0; i < NC; ++i) {
     double rhs = r[i];
 #pragma unroll
-    for (int j = 0; j < 5; ++j)
+    for (int j = 0; j < NC; ++j)
       if (kept[j]) rhs -= A[i][j] * th[j];
     if (kept[i]) {
       d[i] = 1.0;
@@ -232,90 +276,93 @@ __device__ inline bool solve_set(const double* A15, const double* r, double cnt,
       b[i] = rhs / d[i];
     }
   }
-  double M[5][5];
+  // scaled matrix, factorised in place (lower triangle)
 #pragma unroll
-  for (int i = 0; i < 5; ++i)
+  for (int i = 0; i < NC; ++i)
 #pragma unroll
-    for (int j = 0; j < 5; ++j)
-      M[i][j] = (kept[i] || kept[j]) ? (i == j ? 1.0 : 0.0) : A[i][j] / (d[i] * d[j]);
-  double L[5][5];
+    for (int j = 0; j < NC; ++j)
+      A[i][j] = (kept[i] || kept[j]) ? (i == j ? 1.0 : 0.0) : A[i][j] / (d[i] * d[j]);
 #pragma unroll
-  for (int j = 0; j < 5; ++j) {
-    double s = M[j][j];
+  for (int j = 0; j < NC; ++j) {
+    double s = A[j][j];
 #pragma unroll
-    for (int k = 0; k < j; ++k) s -= L[j][k] * L[j][k];
+    for (int k = 0; k < j; ++k) s -= A[j][k] * A[j][k];
     if (!(s > 1e-12)) return false;
-    L[j][j] = sqrt(s);
+    A[j][j] = sqrt(s);
 #pragma unroll
-    for (int i = j + 1; i < 5; ++i) {
-      double t = M[i][j];
+    for (int i = j + 1; i < NC; ++i) {
+      double t = A[i][j];
 #pragma unroll
-      for (int k = 0; k < j; ++k) t -= L[i][k] * L[j][k];
-      L[i][j] = t / L[j][j];
+      for (int k = 0; k < j; ++k) t -= A[i][k] * A[j][k];
+      A[i][j] = t / A[j][j];
     }
   }
-  double z[5], x[5];
+  double z[NC], x[NC];
 #pragma unroll
-  for (int i = 0; i < 5; ++i) {
+  for (int i = 0; i < NC; ++i) {
     double t = b[i];
 #pragma unroll
-    for (int k = 0; k < i; ++k) t -= L[i][k] * z[k];
-    z[i] = t / L[i][i];
+    for (int k = 0; k < i; ++k) t -= A[i][k] * z[k];
+    z[i] = t / A[i][i];
   }
 #pragma unroll
-  for (int i = 4; i >= 0; --i) {
+  for (int i = NC - 1; i >= 0; --i) {
     double t = z[i];
 #pragma unroll
-    for (int k = i + 1; k < 5; ++k) t -= L[k][i] * x[k];
-    x[i] = t / L[i][i];
+    for (int k = i + 1; k < NC; ++k) t -= A[k][i] * x[k];
+    x[i] = t / A[i][i];
   }
 #pragma unroll
-  for (int i = 0; i < 5; ++i)
+  for (int i = 0; i < NC; ++i)
     if (!kept[i]) th[i] = x[i] / d[i];
   return true;
 }
 
 // One workgroup: the normal equations of the four sets summed over the
 // per-workgroup partials in a fixed order, then each set solved; theta
-// (device [20]) is updated in place and counts[4] receives each set's batch
-// count.
+// (device [4*NC]) is updated in place and counts[4] receives each set's
+// batch count.
+template <int NC>
 __global__ __launch_bounds__(kReduceWG) void k_fit_solve(const double* __restrict__ partials,
                                                          int grid, double* __restrict__ theta,
                                                          long long* __restrict__ counts) {
+  using Cols = FitCols<NC>;
   __shared__ double s_red[kReduceWG];
-  __shared__ double s_tot[kFitVals];
-  reduce_columns<kFitVals>(partials, grid, s_red, s_tot);
+  __shared__ double s_tot[Cols::kVals];
+  reduce_columns<Cols::kVals>(partials, grid, s_red, s_tot);
   const int g = threadIdx.x;
   if (g < 4) {
-    const double* a = s_tot + g * kFitSet;
-    double th[5];
+    const double* a = s_tot + g * Cols::kSet;
+    double th[NC];
 #pragma unroll
-    for (int i = 0; i < 5; ++i) th[i] = theta[g * 5 + i];
-    if (solve_set(a, a + 15, a[20], a[21], a[22], th)) {
+    for (int i = 0; i < NC; ++i) th[i] = theta[g * NC + i];
+    if (solve_set<NC>(a, a + Cols::kTri, a + Cols::kTri + NC, th)) {
 #pragma unroll
-      for (int i = 0; i < 5; ++i) theta[g * 5 + i] = th[i];
+      for (int i = 0; i < NC; ++i) theta[g * NC + i] = th[i];
     }
-    counts[g] = (long long)a[20];
+    counts[g] = (long long)a[Cols::kTri + NC];
   }
 }
 
-// Fitting starts from theta0: copies it into theta (device [20]) and clears
-// the set counts.
-__global__ __launch_bounds__(64) void k_fit_init(const FitModel M, double* __restrict__ theta,
+// Fitting starts from theta0: copies it into theta (device [4*NC]) and
+// clears the set counts.
+template <int NC>
+__global__ __launch_bounds__(64) void k_fit_init(const FitModel<NC> M, double* __restrict__ theta,
                                                  long long* __restrict__ counts) {
   const int t = threadIdx.x;
-  if (t < 20) theta[t] = M.th[t];
+  if (t < 4 * NC) theta[t] = M.th[t];
   if (t < 4) counts[t] = 0;
 }
 
 // ------------------------------------------------------------ metrics
 
 // The model's prediction (segment max) for a nonempty batch.
-__device__ __forceinline__ double predict(const FitModel& A, const BatchRegs& r) {
-  double X[5];
-  fit_features(A.S, r.n, r.P, r.C, r.Q, X);
-  const double tm = fit_eq1(A.th + (r.ph * 2 + 0) * 5, X);
-  const double tc = fit_eq1(A.th + (r.ph * 2 + 1) * 5, X);
+template <int NC>
+__device__ __forceinline__ double predict(const FitModel<NC>& A, const BatchRegs& r) {
+  double X[NC];
+  fit_features<NC>(A.S, r.n, r.P, r.C, r.Q, r.R, X);
+  const double tm = fit_eq<NC>(A.th + (r.ph * 2 + 0) * NC, X);
+  const double tc = fit_eq<NC>(A.th + (r.ph * 2 + 1) * NC, X);
   return tc > tm ? tc : tm;
 }
 
@@ -392,9 +439,10 @@ __device__ __forceinline__ void flush_hist(const unsigned int* s_hist, unsigned 
 // relative errors: partials[block][8] = (n, sum y, m, -) for prefill, then
 // decode.  Also the first radix pass of the percentile selection (the top 8
 // bits of every error; hist must be zero on entry).
+template <int NC>
 __global__ __launch_bounds__(kFitWG) void k_fit_metrics1(const int64_t* __restrict__ sums,
                                                          const uint8_t* __restrict__ phase,
-                                                         int64_t nB, const FitModel A,
+                                                         int64_t nB, const FitModel<NC> A,
                                                          const double* __restrict__ y,
                                                          float* __restrict__ rel_err,
                                                          double* __restrict__ partials,
@@ -407,10 +455,10 @@ __global__ __launch_bounds__(kFitWG) void k_fit_metrics1(const int64_t* __restri
   double acc[kMetricVals] = {0, 0, 0, 0, 0, 0, 0, 0};
   const int64_t stride = (int64_t)gridDim.x * kFitWG;
   for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
-    const BatchRegs r = load_batch(sums, phase, y, nB, b);
+    const BatchRegs r = load_batch<NC>(sums, phase, y, nB, b);
     float e = __builtin_nanf("");
     if (r.ph >= 0) {
-      const double yhat = predict(A, r);
+      const double yhat = predict<NC>(A, r);
       if (r.y > 0) e = (float)(fabs(yhat - r.y) / r.y);
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
@@ -439,9 +487,10 @@ __global__ __launch_bounds__(kReduceWG) void k_fit_metrics_sum(const double* __r
 // Pass 2: per phase (and all), sum (y - mean)^2 and sum (y - yhat)^2 with
 // the means of the pass-1 sums tot1[8]: partials[block][8] = (prefill
 // sst, sse, decode sst, sse, all sst, sse, -, -).
+template <int NC>
 __global__ __launch_bounds__(kFitWG) void k_fit_metrics2(const int64_t* __restrict__ sums,
                                                          const uint8_t* __restrict__ phase,
-                                                         int64_t nB, const FitModel A,
+                                                         int64_t nB, const FitModel<NC> A,
                                                          const double* __restrict__ y,
                                                          const double* __restrict__ tot1,
                                                          double* __restrict__ partials) {
@@ -451,9 +500,9 @@ __global__ __launch_bounds__(kFitWG) void k_fit_metrics2(const int64_t* __restri
   double acc[kMetricVals] = {0, 0, 0, 0, 0, 0, 0, 0};
   const int64_t stride = (int64_t)gridDim.x * kFitWG;
   for (int64_t b = (int64_t)blockIdx.x * kFitWG + threadIdx.x; b < nB; b += stride) {
-    const BatchRegs r = load_batch(sums, phase, y, nB, b);
+    const BatchRegs r = load_batch<NC>(sums, phase, y, nB, b);
     if (r.ph < 0) continue;
-    const double res = r.y - predict(A, r);
+    const double res = r.y - predict<NC>(A, r);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const double dv = r.y - mean[q];

@@ -71,8 +71,11 @@ struct ChunkMap {
 // MODE_ATTR: latency, regime, share, tenant sums of one (shape, theta).
 // MODE_FEAT: the feature rows.  MODE_EXT: the outputs of MODE_ATTR under the
 // extended model (Eq. 1 plus a cross term a5*S5*sum p*c and a per-request
-// term a6*S6*|B|).
-enum { MODE_ATTR = 0, MODE_FEAT = 1, MODE_EXT = 2 };
+// term a6*S6*|B|).  MODE_SUMS: the exact batch sums with the extended
+// model's sum p*c, and the phase (no per-request outputs).
+enum { MODE_ATTR = 0, MODE_FEAT = 1, MODE_EXT = 2, MODE_SUMS = 3 };
+// modes that form the batch sums of p*c
+template <int MODE> constexpr bool kCrossSum = MODE == MODE_EXT || MODE == MODE_SUMS;
 template <int MODE> constexpr bool kAttrMode = MODE == MODE_ATTR || MODE == MODE_EXT;
 
 // Native vectors: 16-byte global loads / stores (dwordx4).
@@ -100,7 +103,8 @@ struct Params {
   double* tenant_sums;      // [n_tenants] (HIST_GLOBAL: the tenant cache's output)
   float* x_req;             // [5][N] (MODE_FEAT) or null
   double* x_batch;          // [5][nB] (MODE_FEAT) or null
-  int64_t* bsums;           // [4][nB] (|B|, sum p, sum c, sum p^2) (MODE_FEAT) or null
+  int64_t* bsums;           // [4][nB] (|B|, sum p, sum c, sum p^2) (MODE_FEAT), with
+                            // sum p*c as a fifth row (MODE_SUMS), or null
   uint8_t* bphase;          // [nB] phase, 255 for an empty batch (MODE_FEAT) or null
   int32_t n_tenants;
   int32_t hist_rep;         // MODE_ATTR, HIST_LDS: histogram replicas (1, 2 or 4)
@@ -252,13 +256,27 @@ __device__ __forceinline__ float share_of(const float* k, int32_t p, int32_t c) 
   return fmaf(k[3], pf * pf, fmaf(k[2], (float)c, fmaf(k[1], pf, k[0])));
 }
 
+// MODE_SUMS: the exact sums of a nonempty batch and its phase.
+__device__ __forceinline__ void sums_out(const Params& P, int64_t bg, int64_t n, uint64_t Psum,
+                                         uint64_t Csum, uint64_t Qsum, uint64_t Rsum,
+                                         bool prefill) {
+  if (P.bsums) {
+    P.bsums[0 * P.nB + bg] = n;
+    P.bsums[1 * P.nB + bg] = (int64_t)Psum;
+    P.bsums[2 * P.nB + bg] = (int64_t)Csum;
+    P.bsums[3 * P.nB + bg] = (int64_t)Qsum;
+    P.bsums[4 * P.nB + bg] = (int64_t)Rsum;
+  }
+  if (P.bphase) P.bphase[bg] = prefill ? 0 : 1;
+}
+
 template <int MODE>
 __device__ __forceinline__ void empty_batch(const Params& P, int64_t bg) {
-  if (MODE == MODE_FEAT) {
+  if (MODE == MODE_FEAT || MODE == MODE_SUMS) {
     if (P.x_batch)
       for (int q = 0; q < 5; ++q) P.x_batch[q * P.nB + bg] = 0.0;
     if (P.bsums)
-      for (int q = 0; q < 4; ++q) P.bsums[q * P.nB + bg] = 0;
+      for (int q = 0; q < (MODE == MODE_SUMS ? 5 : 4); ++q) P.bsums[q * P.nB + bg] = 0;
     if (P.bphase) P.bphase[bg] = 255;
   } else {
     if (P.latency) P.latency[bg] = 0.0f;
@@ -534,15 +552,22 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
         sp += p;
         scz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
         sq += (uint64_t)p * p;
-        if constexpr (MODE == MODE_EXT) sr += (uint64_t)p * c;
+        if constexpr (kCrossSum<MODE>) sr += (uint64_t)p * c;
       }
     }
   }
   sp = wave_sum(sp);
   scz = wave_sum(scz);
   sq = wave_sum(sq);
-  if constexpr (MODE == MODE_EXT) sr = wave_sum(sr);
+  if constexpr (kCrossSum<MODE>) sr = wave_sum(sr);
   const int64_t n = re - rs;
+  if constexpr (MODE == MODE_SUMS) {
+    if (lane == 0) {
+      const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
+      sums_out(P, bg, n, sp, scz & kCMask, sq, sr, prefill);
+    }
+    return;
+  }
   if (lane == 0) {
     const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
     if constexpr (MODE == MODE_EXT)
@@ -587,8 +612,9 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
   __shared__ WaveLds s_wave[kWaves];
   constexpr bool STAGE = kAttrMode<MODE> && SHARE;
   constexpr bool EXT = MODE == MODE_EXT;
+  constexpr bool RSUM = kCrossSum<MODE>;
   // extended model, per wave: sum p*c and the share constant k4 of each batch
-  __shared__ uint64_t s_rsum[EXT ? kWaves * kTileBatches : 1];
+  __shared__ uint64_t s_rsum[RSUM ? kWaves * kTileBatches : 1];
   __shared__ double s_k4[EXT ? kWaves * kTileBatches : 1];
   __shared__ float s_stage[STAGE ? kWaves * 64 * kStagePitch : 1];  // shares, per wave
   constexpr bool TEN = HIST != HIST_NONE;
@@ -596,7 +622,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   WaveLds& W = s_wave[tid >> 6];
-  uint64_t* W_r = s_rsum + (EXT ? (tid >> 6) * kTileBatches : 0);
+  uint64_t* W_r = s_rsum + (RSUM ? (tid >> 6) * kTileBatches : 0);
   double* W_k4 = s_k4 + (EXT ? (tid >> 6) * kTileBatches : 0);
   float* stage = s_stage + (STAGE ? (tid >> 6) * 64 * kStagePitch : 0);
   const int32_t x0 = lane * kVec;  // first slot of this lane in a round
@@ -704,7 +730,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
         // ---- batch-start bitmask, accumulators
         if (lane < kTileMaskWords + 2) W.mask[lane] = 0u;
         if (lane < count) W.acc[lane] = BatchAcc{0, 0, 0};
-        if (EXT && lane < count) W_r[lane] = 0ull;
+        if (RSUM && lane < count) W_r[lane] = 0ull;
         wave_lds_sync();
         if (ne) atomicOr(&W.mask[lo >> 5], 1u << (lo & 31));
         wave_lds_sync();
@@ -742,13 +768,13 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
               rp += p;
               rcz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
               rq += (uint64_t)p * p;
-              if constexpr (EXT) rr += (uint64_t)p * c;
+              if constexpr (RSUM) rr += (uint64_t)p * c;
               if ((ends >> q) & 1u) {
                 const uint32_t k = ord0[r] + __builtin_popcount(bits[r] & ((2u << q) - 1u)) - 1u;
                 atomicAdd((unsigned long long*)&W.acc[k].p, (unsigned long long)rp);
                 atomicAdd((unsigned long long*)&W.acc[k].cz, (unsigned long long)rcz);
                 atomicAdd((unsigned long long*)&W.acc[k].q, (unsigned long long)rq);
-                if constexpr (EXT) atomicAdd((unsigned long long*)&W_r[k], (unsigned long long)rr);
+                if constexpr (RSUM) atomicAdd((unsigned long long*)&W_r[k], (unsigned long long)rr);
                 rp = 0;
                 rcz = 0;
                 rq = 0;
@@ -773,6 +799,8 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
               const bool prefill = (a.p != (uint64_t)n) || ((a.cz >> 48) != 0);
               if constexpr (EXT)
                 ext_model(P, V, bg, n, a.p, a.cz & kCMask, a.q, W_r[k], prefill, W.k[k], &W_k4[k]);
+              else if constexpr (MODE == MODE_SUMS)
+                sums_out(P, bg, n, a.p, a.cz & kCMask, a.q, W_r[k], prefill);
               else
                 batch_model<MODE>(P, bg, n, a.p, a.cz & kCMask, a.q, prefill, W.k[k]);
             }
@@ -782,7 +810,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
           // ---- per request: share (+ tenant) or features
   #pragma unroll
           for (int r = 0; r < kRounds; ++r) {
-            if (r * kRoundSlots >= L) break;  // wave-uniform
+            if (MODE == MODE_SUMS || r * kRoundSlots >= L) break;  // wave-uniform
             const int64_t pos = ra + r * kRoundSlots + x0;
             uint32_t kcur = 0xffffffffu;
             float kk[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};

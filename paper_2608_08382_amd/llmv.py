@@ -26,8 +26,9 @@ LLMV_TENANTS_MAX = 1 << 24
 
 EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_sweep_workspace_size",
            "llmv_attribute", "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
-           "llmv_batch_sums", "llmv_admit", "llmv_fit_workspace_size", "llmv_fit",
-           "llmv_fit_metrics", "llmv_shape_constants_ext", "llmv_attribute_ext",
+           "llmv_batch_sums", "llmv_batch_sums_ext", "llmv_admit", "llmv_fit_workspace_size", "llmv_fit",
+           "llmv_fit_metrics", "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
+           "llmv_attribute_ext",
            "llmv_last_error", "llmv_set_kernel_events")
 
 
@@ -73,6 +74,7 @@ def load(path: str = LIB_PATH):
             lib.llmv_features.argtypes = [P, P, P, P, P, sz, P]
             lib.llmv_tenant_sums.argtypes = [P, P, i64, i32, P, P, sz, P]
             lib.llmv_batch_sums.argtypes = [P, P, P, P, sz, P]
+            lib.llmv_batch_sums_ext.argtypes = [P, P, P, P, sz, P]
             lib.llmv_admit.argtypes = [P, P, i64, P, P, P, P, P, i64, P, P, P, P, P]
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
             lib.llmv_shape_constants_ext.argtypes = [P, P]
@@ -81,13 +83,16 @@ def load(path: str = LIB_PATH):
             lib.llmv_fit_workspace_size.restype = sz
             lib.llmv_fit.argtypes = [P, P, i64, P, P, P, i32, P, P, P, sz, P]
             lib.llmv_fit_metrics.argtypes = [P, P, i64, P, P, P, P, P, P, sz, P]
+            lib.llmv_fit_ext.argtypes = [P, P, i64, P, P, P, i32, P, P, P, sz, P]
+            lib.llmv_fit_metrics_ext.argtypes = [P, P, i64, P, P, P, P, P, P, sz, P]
             lib.llmv_last_error.argtypes = []
             lib.llmv_last_error.restype = ctypes.c_char_p
             lib.llmv_set_kernel_events.argtypes = [P, P]
             lib.llmv_set_kernel_events.restype = ctypes.c_int
             for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
                       "llmv_features", "llmv_tenant_sums", "llmv_validate", "llmv_batch_sums",
-                      "llmv_admit", "llmv_fit", "llmv_fit_metrics", "llmv_shape_constants_ext",
+                      "llmv_batch_sums_ext", "llmv_admit", "llmv_fit", "llmv_fit_metrics",
+                      "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
                       "llmv_attribute_ext"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
@@ -195,6 +200,14 @@ def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out
         nbytes, _stream(stream)), "llmv_attribute_sweep")
 
 
+def llmv_batch_sums_ext(trace: DeviceTrace, sums=None, phase=None, ws=None, stream=None):
+    """sums: device int64 [5, n_batches] (with sum p*c); phase: device uint8 [n_batches]."""
+    tr = trace.struct(with_tenant=False)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().llmv_batch_sums_ext(ctypes.byref(tr), _ptr(sums), _ptr(phase), _ptr(ws), nbytes,
+                                      _stream(stream)), "llmv_batch_sums_ext")
+
+
 def llmv_batch_sums(trace: DeviceTrace, sums=None, phase=None, ws=None, stream=None):
     """sums: device int64 [4, n_batches]; phase: device uint8 [n_batches]."""
     tr = trace.struct(with_tenant=False)
@@ -248,32 +261,48 @@ def llmv_fit_workspace_size(n_batches: int) -> int:
 
 
 def llmv_fit(sums, phase, shape, y, theta0, rounds: int, theta, counts=None, ws=None,
-             stream=None):
+             stream=None, ext=False):
     """Device tensors: sums int64 [4, n_batches], phase uint8 [n_batches],
     y fp64 [n_batches]; outputs theta fp64 [20], counts int64 [4] (or None).
-    theta0: 20 host numbers."""
+    theta0: 20 host numbers.  With ext the extended model (llmv_fit_ext):
+    sums [5, n_batches], theta0 and theta 28 values."""
     n = int(phase.numel())
-    th0 = (ctypes.c_double * 20)(*[float(v) for v in theta0])
+    k = 28 if ext else 20
+    th0 = (ctypes.c_double * k)(*[float(v) for v in theta0])
     sh = make_shape(shape)
     if ws is None:
         ws = fit_workspace(n, theta.device)
-    _check(load().llmv_fit(_ptr(sums), _ptr(phase), n, _shape_ref(sh), _ptr(y), th0, int(rounds),
-                           _ptr(theta), _ptr(counts), _ptr(ws), ws.numel(), _stream(stream)),
-           "llmv_fit")
+    fn, name = (load().llmv_fit_ext, "llmv_fit_ext") if ext else (load().llmv_fit, "llmv_fit")
+    _check(fn(_ptr(sums), _ptr(phase), n, _shape_ref(sh), _ptr(y), th0, int(rounds), _ptr(theta),
+              _ptr(counts), _ptr(ws), ws.numel(), _stream(stream)), name)
 
 
-def llmv_fit_metrics(sums, phase, shape, coeffs, y, out, rel_err=None, ws=None, stream=None):
+def llmv_fit_metrics(sums, phase, shape, coeffs, y, out, rel_err=None, ws=None, stream=None,
+                     ext=False):
     """Device tensors as for llmv_fit; out fp64 [3, 4] (prefill, decode, all)
-    x (r2, p90, p99, batches); rel_err fp32 [n_batches] or None."""
+    x (r2, p90, p99, batches); rel_err fp32 [n_batches] or None.  With ext the
+    extended model (llmv_fit_metrics_ext, 28 coefficients)."""
     n = int(phase.numel())
-    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    k = 28 if ext else 20
+    co = (ctypes.c_float * k)(*[float(v) for v in coeffs])
     sh = make_shape(shape)
     if ws is None:
         ws = fit_workspace(n, out.device)
-    _check(load().llmv_fit_metrics(_ptr(sums), _ptr(phase), n, _shape_ref(sh), co, _ptr(y),
-                                   _ptr(rel_err), _ptr(out), _ptr(ws), ws.numel(),
-                                   _stream(stream)),
-           "llmv_fit_metrics")
+    fn, name = ((load().llmv_fit_metrics_ext, "llmv_fit_metrics_ext") if ext
+                else (load().llmv_fit_metrics, "llmv_fit_metrics"))
+    _check(fn(_ptr(sums), _ptr(phase), n, _shape_ref(sh), co, _ptr(y), _ptr(rel_err), _ptr(out),
+              _ptr(ws), ws.numel(), _stream(stream)), name)
+
+
+def llmv_fit_ext(sums, phase, shape, y, theta0, rounds: int, theta, counts=None, ws=None,
+                 stream=None):
+    """llmv_fit for the extended model: sums [5, n_batches], theta0/theta 28 values."""
+    llmv_fit(sums, phase, shape, y, theta0, rounds, theta, counts, ws, stream, ext=True)
+
+
+def llmv_fit_metrics_ext(sums, phase, shape, coeffs, y, out, rel_err=None, ws=None, stream=None):
+    """llmv_fit_metrics for the extended model: sums [5, n_batches], 28 coefficients."""
+    llmv_fit_metrics(sums, phase, shape, coeffs, y, out, rel_err, ws, stream, ext=True)
 
 
 def llmv_features(trace: DeviceTrace, shape, x_req=None, x_batch=None, ws=None, stream=None):
@@ -376,14 +405,15 @@ def tenant_sums(tenant, share, n_tenants: int, ws=None):
     return out
 
 
-def batch_sums(trace: DeviceTrace, ws=None):
-    """Allocates and returns (sums int64 [4, n_batches], phase uint8 [n_batches])."""
+def batch_sums(trace: DeviceTrace, ws=None, ext=False):
+    """Allocates and returns (sums int64 [4, n_batches], phase uint8
+    [n_batches]); with ext the sums have a fifth row, sum p*c."""
     dev = trace.p.device
-    sums = torch.empty((4, trace.n_batches), dtype=torch.int64, device=dev)
+    sums = torch.empty((5 if ext else 4, trace.n_batches), dtype=torch.int64, device=dev)
     phase = torch.empty(trace.n_batches, dtype=torch.uint8, device=dev)
     if ws is None:
         ws = workspace(trace.n_batches, trace.n_requests, 0, dev)
-    llmv_batch_sums(trace, sums, phase, ws)
+    (llmv_batch_sums_ext if ext else llmv_batch_sums)(trace, sums, phase, ws)
     return sums, phase
 
 
@@ -407,27 +437,28 @@ def fit_workspace(n_batches: int, device="cuda"):
                        device=device)
 
 
-def fit(sums, phase, shape, y, theta0, rounds: int, ws=None):
-    """Allocates the outputs and runs llmv_fit; returns (theta fp64 [20],
-    counts int64 [4]) as device tensors."""
+def fit(sums, phase, shape, y, theta0, rounds: int, ws=None, ext=False):
+    """Allocates the outputs and runs llmv_fit (llmv_fit_ext with ext);
+    returns (theta fp64 [20] or [28], counts int64 [4]) as device tensors."""
     dev = y.device
-    theta = torch.empty(20, dtype=torch.float64, device=dev)
+    theta = torch.empty(28 if ext else 20, dtype=torch.float64, device=dev)
     counts = torch.empty(4, dtype=torch.int64, device=dev)
-    llmv_fit(sums, phase, shape, y, theta0, rounds, theta, counts, ws)
+    llmv_fit(sums, phase, shape, y, theta0, rounds, theta, counts, ws, ext=ext)
     return theta, counts
 
 
 METRIC_GROUPS = ("prefill", "decode", "all")
 
 
-def fit_metrics(sums, phase, shape, coeffs, y, ws=None, rel_err=False):
-    """Runs llmv_fit_metrics; returns {"prefill"|"decode"|"all": {"r2",
-    "p90", "p99", "n"}} (waits for the result), plus the per-batch relative
-    errors under "rel_err" when asked for."""
+def fit_metrics(sums, phase, shape, coeffs, y, ws=None, rel_err=False, ext=False):
+    """Runs llmv_fit_metrics (llmv_fit_metrics_ext with ext); returns
+    {"prefill"|"decode"|"all": {"r2", "p90", "p99", "n"}} (waits for the
+    result), plus the per-batch relative errors under "rel_err" when asked
+    for."""
     dev = y.device
     out = torch.empty((3, 4), dtype=torch.float64, device=dev)
     err = torch.empty(int(phase.numel()), dtype=torch.float32, device=dev) if rel_err else None
-    llmv_fit_metrics(sums, phase, shape, coeffs, y, out, err, ws)
+    llmv_fit_metrics(sums, phase, shape, coeffs, y, out, err, ws, ext=ext)
     o = out.cpu().tolist()
     res = {g: {"r2": o[i][0], "p90": o[i][1], "p99": o[i][2], "n": int(o[i][3])}
            for i, g in enumerate(METRIC_GROUPS)}
