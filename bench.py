@@ -154,9 +154,11 @@ def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
     """Admission queries on the trace's batches: llmv_batch_sums over every
     batch, then 2^20 candidate requests (20% prefill-type) in one llmv_admit
     call; plus the host-side latency of one query and of one single-batch
-    attribution step (median of 50 synchronous calls)."""
+    attribution step (median of 50 synchronous calls).  Then the same
+    queries under the extended model."""
     import numpy as np
     import torch
+    import tracegen
     from paper_2608_08382_amd import llmv
 
     dev = dt.p.device
@@ -228,6 +230,17 @@ def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
         f"({res['value']:.3e}/s); one query {res['single_query_us']:.1f} us, one 256-request "
         f"step {res['single_step_256_us']:.1f} us (host, synchronous); on the GPU's clock "
         f"{res['single_query_gpu_us']:.1f} and {res['single_step_256_gpu_us']:.1f} us")
+    # the same 2^20 queries under the extended model, from llmv_batch_sums_ext's state
+    sums5 = torch.empty((5, tr.n_batches), dtype=torch.int64, device=dev)
+    llmv.llmv_batch_sums_ext(dt, sums5, phase, ws)
+    co28 = tracegen.ext_coeffs(104)
+    ms_ax = timed(lambda: llmv.llmv_admit_ext(sums5, phase, tr.n_batches, tr.shape, co28, cb, cp,
+                                              cc, out["t_after"], out["delta"], out["share"],
+                                              out["regime"]))
+    del sums5
+    res["extended"] = {"admit_ms": ms_ax, "value": m / (ms_ax / 1e3), "unit": "queries/s"}
+    log(f"[bench] admission (extended model): {m} queries in {ms_ax:.3f} ms "
+        f"({res['extended']['value']:.3e}/s)")
     if with_oracle:
         import oracle
         sys.path.insert(0, os.path.join(ROOT, "tests"))

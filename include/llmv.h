@@ -231,6 +231,17 @@ int llmv_admit(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
                const int32_t *cand_p, const int32_t *cand_c, int64_t n_cand, float *t_after,
                float *delta, float *share, uint8_t *regime, void *stream);
 
+/* llmv_admit under the extended model (readings X1-X3):
+ *   sums    device [5][n_batches] as written by llmv_batch_sums_ext.
+ *   coeffs  host, 28 finite fp32 as for llmv_attribute_ext.
+ * B' also adds the candidate's p*c to sum p*c; the candidate's share gains
+ * its a5*S5*p*c and a6*S6 terms.  Other arguments, outputs and rules as
+ * llmv_admit. */
+int llmv_admit_ext(const int64_t *sums, const uint8_t *phase, int64_t n_batches,
+                   const llmv_shape *shape, const float coeffs[28], const int64_t *cand_batch,
+                   const int32_t *cand_p, const int32_t *cand_c, int64_t n_cand, float *t_after,
+                   float *delta, float *share, uint8_t *regime, void *stream);
+
 /* Fitting Eq. 1 (Sec. 2.1: the coefficients are fitted by ordinary least
  * squares on profiled batch latencies, one set per phase and segment) and
  * the accuracy metrics (Sec. 3 and Appendix A: r^2 and the 90th / 99th

@@ -105,12 +105,13 @@ class Oracle:
         lib.orc_batch_sums.argtypes = [i64, i64, P, P, P, P, P]
         lib.orc_batch_sums_ext.argtypes = [i64, i64, P, P, P, P, P]
         lib.orc_admit.argtypes = [i64, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
+        lib.orc_admit_ext.argtypes = [i64, P, P, i32, i32, P, P, P, P, P, P, P, P, P]
         lib.orc_shape_constants_ext.argtypes = [P, P]
         lib.orc_attribute_ext.argtypes = [i64, i64, P, P, P, P, P, P, i32,
                                           P, P, P, P, P, P, P, P]
         for f in ("orc_shape_constants", "orc_validate", "orc_features",
                   "orc_attribute", "orc_tenant_sums", "orc_batch_sums", "orc_batch_sums_ext",
-                  "orc_admit",
+                  "orc_admit", "orc_admit_ext",
                   "orc_shape_constants_ext", "orc_attribute_ext"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
@@ -204,19 +205,20 @@ class Oracle:
                                            _ptr(phase)), "batch_sums_ext")
         return sums, phase
 
-    def admit(self, p, c, cand_p, cand_c, shape, coeffs) -> dict:
+    def admit(self, p, c, cand_p, cand_c, shape, coeffs, ext=False) -> dict:
         """Admission query for the batch of requests (p, c) and one candidate
         request (cand_p, cand_c): T_after, delta, share, share_alt, TM_after,
-        TC_after, regime."""
+        TC_after, regime.  With ext=True, the extended model (28 coefficients)."""
         p, c = _arr(p, np.int32), _arr(c, np.int32)
         co = _arr(coeffs, np.float32)
-        if co.shape != (20,):
-            raise ValueError("coeffs must hold 20 fp32 values")
+        if co.shape != ((28,) if ext else (20,)):
+            raise ValueError("coeffs must hold 20 (28 with ext) fp32 values")
         vals = [ctypes.c_double() for _ in range(6)]
         reg = ctypes.c_uint8()
         keep, sp = _shape_ptr(shape)
-        rc = self.lib.orc_admit(len(p), _ptr(p), _ptr(c), int(cand_p), int(cand_c), sp, _ptr(co),
-                                *[ctypes.addressof(v) for v in vals], ctypes.addressof(reg))
+        fn = self.lib.orc_admit_ext if ext else self.lib.orc_admit
+        rc = fn(len(p), _ptr(p), _ptr(c), int(cand_p), int(cand_c), sp, _ptr(co),
+                *[ctypes.addressof(v) for v in vals], ctypes.addressof(reg))
         del keep
         _check(rc, "admit")
         names = ("T_after", "delta", "share", "share_alt", "TM_after", "TC_after")
@@ -283,3 +285,8 @@ def batch_sums_ext(offsets, p, c):
 
 def admit(p, c, cand_p, cand_c, shape, coeffs):
     return default().admit(p, c, cand_p, cand_c, shape, coeffs)
+
+
+def admit_ext(p, c, cand_p, cand_c, shape, coeffs):
+    """The admission query under the extended model: coeffs [28]."""
+    return default().admit(p, c, cand_p, cand_c, shape, coeffs, ext=True)

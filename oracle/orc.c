@@ -380,12 +380,14 @@ int orc_batch_sums_ext(int64_t nB, int64_t N, const int64_t *off, const int32_t 
   return ORC_OK;
 }
 
-int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
-              const orc_shape *shape, const float coeffs[20], double *T_after,
-              double *delta, double *share, double *share_alt, double *TM_after,
-              double *TC_after, uint8_t *regime) {
+/* Admission query of either model (ext = 0: Eq. 1 with 20 coefficients,
+ * ext = 1: the extended model with 28), by its definition: the attribution
+ * of B' = B followed by the candidate, and of B. */
+static int admit_query(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
+                       const orc_shape *shape, const float *coeffs, int ext, double *T_after,
+                       double *delta, double *share, double *share_alt, double *TM_after,
+                       double *TC_after, uint8_t *regime) {
   if (n < 0 || (n > 0 && (!p || !c)) || !coeffs) return ORC_EINVAL;
-  /* B' = B followed by the candidate. */
   int32_t *p1 = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
   int32_t *c1 = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
   double *f1 = (double *)malloc(sizeof(double) * (size_t)(n + 1));
@@ -403,11 +405,20 @@ int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t
   const int64_t off0[2] = {0, n}, off1[2] = {0, n + 1};
   double T0 = 0.0, T1 = 0.0, tm1 = 0.0, tc1 = 0.0;
   uint8_t reg1 = ORC_REGIME_EMPTY;
-  int rc = orc_attribute(1, n, off0, p, c, NULL, shape, coeffs, 0, &T0, NULL, NULL, NULL, NULL,
-                         NULL, NULL, NULL);
-  if (rc == ORC_OK)
-    rc = orc_attribute(1, n + 1, off1, p1, c1, NULL, shape, coeffs, 0, &T1, &tm1, &tc1, NULL,
-                       &reg1, f1, g1, NULL);
+  int rc;
+  if (ext) {
+    rc = orc_attribute_ext(1, n, off0, p, c, NULL, shape, coeffs, 0, &T0, NULL, NULL, NULL,
+                           NULL, NULL, NULL, NULL);
+    if (rc == ORC_OK)
+      rc = orc_attribute_ext(1, n + 1, off1, p1, c1, NULL, shape, coeffs, 0, &T1, &tm1, &tc1,
+                             NULL, &reg1, f1, g1, NULL);
+  } else {
+    rc = orc_attribute(1, n, off0, p, c, NULL, shape, coeffs, 0, &T0, NULL, NULL, NULL, NULL,
+                       NULL, NULL, NULL);
+    if (rc == ORC_OK)
+      rc = orc_attribute(1, n + 1, off1, p1, c1, NULL, shape, coeffs, 0, &T1, &tm1, &tc1, NULL,
+                         &reg1, f1, g1, NULL);
+  }
   if (rc == ORC_OK) {
     if (T_after) *T_after = T1;
     if (delta) *delta = T1 - T0;
@@ -419,6 +430,22 @@ int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t
   }
   free(p1); free(c1); free(f1); free(g1);
   return rc;
+}
+
+int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
+              const orc_shape *shape, const float coeffs[20], double *T_after,
+              double *delta, double *share, double *share_alt, double *TM_after,
+              double *TC_after, uint8_t *regime) {
+  return admit_query(n, p, c, cp, cc, shape, coeffs, 0, T_after, delta, share, share_alt,
+                     TM_after, TC_after, regime);
+}
+
+int orc_admit_ext(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
+                  const orc_shape *shape, const float coeffs[28], double *T_after,
+                  double *delta, double *share, double *share_alt, double *TM_after,
+                  double *TC_after, uint8_t *regime) {
+  return admit_query(n, p, c, cp, cc, shape, coeffs, 1, T_after, delta, share, share_alt,
+                     TM_after, TC_after, regime);
 }
 
 int orc_tenant_sums(const int32_t *tenant, const double *share, int64_t N,

@@ -159,6 +159,13 @@ int orc_admit(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t
               double *delta, double *share, double *share_alt, double *TM_after,
               double *TC_after, uint8_t *regime);
 
+/* orc_admit under the extended model (readings X1-X3): coeffs [28], index
+ * (phase*2 + segment)*7 + k; B and B' attributed by orc_attribute_ext. */
+int orc_admit_ext(int64_t n, const int32_t *p, const int32_t *c, int32_t cp, int32_t cc,
+                  const orc_shape *shape, const float coeffs[28], double *T_after,
+                  double *delta, double *share, double *share_alt, double *TM_after,
+                  double *TC_after, uint8_t *regime);
+
 /* Tenant sums of given shares, in request order:
  * out[u] = sum_{i : tenant[i] == u} share[i].  ORC_ERANGE for a tenant id
  * outside [0, n_tenants). */

@@ -329,6 +329,35 @@ int attribute_params(const llmv_trace* trace, const llmv_shape* shape, const flo
   return LLMV_OK;
 }
 
+// The admission queries of Eq. 1 (NC = 5) or of the extended model (NC = 7).
+template <int NC>
+int admit_run(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+              const llmv_shape* shape, const float* coeffs, const int64_t* cand_batch,
+              const int32_t* cand_p, const int32_t* cand_c, int64_t n_cand, float* t_after,
+              float* delta, float* share, uint8_t* regime, void* stream) {
+  if (n_batches < 0 || n_cand < 0)
+    return fail(LLMV_EINVAL, "negative sizes (n_batches=%lld, n_cand=%lld)",
+                (long long)n_batches, (long long)n_cand);
+  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
+  for (int i = 0; i < 4 * NC; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
+  AdmitParams<NC> A{};
+  int rc = NC == 7 ? shape_constants_ext(shape, A.S) : shape_constants(shape, A.S);
+  if (rc) return rc;
+  for (int i = 0; i < 4 * NC; ++i) A.th[i] = (double)coeffs[i];
+  if (n_cand == 0) return LLMV_OK;
+  if (!cand_batch || !cand_p || !cand_c)
+    return fail(LLMV_EINVAL, "candidate arrays must not be NULL");
+  if (n_batches > 0 && (!sums || !phase)) return fail(LLMV_EINVAL, "sums or phase is NULL");
+  const int64_t blocks = (n_cand + kWG - 1) / kWG;
+  if (blocks > 0x7fffffff) return fail(LLMV_EINVAL, "n_cand=%lld too large", (long long)n_cand);
+  hipLaunchKernelGGL(k_admit<NC>, dim3((unsigned)blocks), dim3(kWG), 0, (hipStream_t)stream, sums,
+                     phase, n_batches, A, cand_batch, cand_p, cand_c, n_cand, t_after, delta,
+                     share, regime);
+  HIP_TRY(hipGetLastError(), "k_admit launch");
+  return LLMV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -590,27 +619,16 @@ int llmv_admit(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
                const llmv_shape* shape, const float coeffs[20], const int64_t* cand_batch,
                const int32_t* cand_p, const int32_t* cand_c, int64_t n_cand, float* t_after,
                float* delta, float* share, uint8_t* regime, void* stream) {
-  if (n_batches < 0 || n_cand < 0)
-    return fail(LLMV_EINVAL, "negative sizes (n_batches=%lld, n_cand=%lld)",
-                (long long)n_batches, (long long)n_cand);
-  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
-  for (int i = 0; i < 20; ++i)
-    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
-  AdmitParams A{};
-  int rc = shape_constants(shape, A.S);
-  if (rc) return rc;
-  for (int i = 0; i < 20; ++i) A.th[i] = (double)coeffs[i];
-  if (n_cand == 0) return LLMV_OK;
-  if (!cand_batch || !cand_p || !cand_c)
-    return fail(LLMV_EINVAL, "candidate arrays must not be NULL");
-  if (n_batches > 0 && (!sums || !phase)) return fail(LLMV_EINVAL, "sums or phase is NULL");
-  const int64_t blocks = (n_cand + kWG - 1) / kWG;
-  if (blocks > 0x7fffffff) return fail(LLMV_EINVAL, "n_cand=%lld too large", (long long)n_cand);
-  hipLaunchKernelGGL(k_admit, dim3((unsigned)blocks), dim3(kWG), 0, (hipStream_t)stream, sums,
-                     phase, n_batches, A, cand_batch, cand_p, cand_c, n_cand, t_after, delta,
-                     share, regime);
-  HIP_TRY(hipGetLastError(), "k_admit launch");
-  return LLMV_OK;
+  return admit_run<5>(sums, phase, n_batches, shape, coeffs, cand_batch, cand_p, cand_c, n_cand,
+                      t_after, delta, share, regime, stream);
+}
+
+int llmv_admit_ext(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
+                   const llmv_shape* shape, const float coeffs[28], const int64_t* cand_batch,
+                   const int32_t* cand_p, const int32_t* cand_c, int64_t n_cand, float* t_after,
+                   float* delta, float* share, uint8_t* regime, void* stream) {
+  return admit_run<7>(sums, phase, n_batches, shape, coeffs, cand_batch, cand_p, cand_c, n_cand,
+                      t_after, delta, share, regime, stream);
 }
 
 int llmv_features(const llmv_trace* trace, const llmv_shape* shape, float* x_req,

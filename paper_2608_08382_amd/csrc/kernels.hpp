@@ -893,21 +893,33 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
 
 // ------------------------------------------------------ admission queries
 
+// Shape constants (S0..S3, and S5, S6 for the extended model) and the
+// coefficients theta[phase][segment][k] of NC terms per set (5: Eq. 1, 7: the
+// extended model).
+template <int NC>
 struct AdmitParams {
-  double S[4];    // shape constants
-  double th[20];  // theta[phase][segment][k]
+  double S[6];
+  double th[4 * NC];
 };
+
+template <int NC>
+__device__ __forceinline__ double admit_eq(const double* th, const double* X) {
+  if constexpr (NC == 7) return eq7(th, X);
+  else return eq1(th, X);
+}
 
 // One admission query per thread (Sec. 1: admission control): candidate j
 // (p_j, c_j) joins batch b_j, whose exact sums and phase are given.  B' =
 // B + candidate has |B|+1 requests, the sums plus the candidate's terms, and
 // is a prefill batch if B is one or the candidate is prefill-type (p > 1 or
 // c = 0).  Outputs (each optional): f(B'), f(B') - f(B), the candidate's
-// share in B' (its own Eq. 1 terms under B''s segment, fp64, rounded once),
-// and B''s regime.  A batch index outside [0, nB) gives NaN and regime 255.
+// share in B' (its own terms under B''s segment, fp64, rounded once), and
+// B''s regime.  A batch index outside [0, nB) gives NaN and regime 255.
+// sums: [4][nB], for the extended model [5][nB] with sum p*c.
+template <int NC>
 __global__ __launch_bounds__(kWG) void k_admit(const int64_t* __restrict__ sums,
                                                const uint8_t* __restrict__ phase, int64_t nB,
-                                               const AdmitParams A,
+                                               const AdmitParams<NC> A,
                                                const int64_t* __restrict__ cand_b,
                                                const int32_t* __restrict__ cand_p,
                                                const int32_t* __restrict__ cand_c, int64_t m,
@@ -915,6 +927,7 @@ __global__ __launch_bounds__(kWG) void k_admit(const int64_t* __restrict__ sums,
                                                float* __restrict__ delta,
                                                float* __restrict__ share,
                                                uint8_t* __restrict__ regime) {
+  static_assert(NC == 5 || NC == 7, "Eq. 1 or the extended model");
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= m) return;
   const int64_t b = cand_b[j];
@@ -927,33 +940,35 @@ __global__ __launch_bounds__(kWG) void k_admit(const int64_t* __restrict__ sums,
     return;
   }
   const int64_t n = sums[b], Ps = sums[nB + b], Cs = sums[2 * nB + b], Qs = sums[3 * nB + b];
+  const int64_t Rs = NC == 7 ? sums[4 * nB + b] : 0;
   const int64_t p = cand_p[j], c = cand_c[j];
   // f(B): 0 for an empty batch
   double t0 = 0.0;
   const bool pre0 = n > 0 && phase[b] == 0;
   if (n > 0) {
-    const double X[5] = {A.S[0], A.S[1] * (double)Ps, A.S[2] * (double)Cs, A.S[3] * (double)Qs,
-                         (double)n * (double)n};
-    const double* thm = A.th + ((pre0 ? 0 : 1) * 2 + 0) * 5;
-    const double* thc = A.th + ((pre0 ? 0 : 1) * 2 + 1) * 5;
-    const double tm = eq1(thm, X), tc = eq1(thc, X);
+    const double X[7] = {A.S[0], A.S[1] * (double)Ps, A.S[2] * (double)Cs, A.S[3] * (double)Qs,
+                         (double)n * (double)n, A.S[4] * (double)Rs, A.S[5] * (double)n};
+    const double* thm = A.th + ((pre0 ? 0 : 1) * 2 + 0) * NC;
+    const double* thc = A.th + ((pre0 ? 0 : 1) * 2 + 1) * NC;
+    const double tm = admit_eq<NC>(thm, X), tc = admit_eq<NC>(thc, X);
     t0 = (tc > tm) ? tc : tm;
   }
   // f(B')
   const int64_t n1 = n + 1;
   const int ph1 = (pre0 || p > 1 || c == 0) ? 0 : 1;
-  const double X1[5] = {A.S[0], A.S[1] * (double)(Ps + p), A.S[2] * (double)(Cs + c),
-                        A.S[3] * (double)(Qs + p * p), (double)n1 * (double)n1};
-  const double* thm = A.th + (ph1 * 2 + 0) * 5;
-  const double* thc = A.th + (ph1 * 2 + 1) * 5;
-  const double tm = eq1(thm, X1), tc = eq1(thc, X1);
+  const double X1[7] = {A.S[0], A.S[1] * (double)(Ps + p), A.S[2] * (double)(Cs + c),
+                        A.S[3] * (double)(Qs + p * p), (double)n1 * (double)n1,
+                        A.S[4] * (double)(Rs + p * c), A.S[5] * (double)n1};
+  const double* thm = A.th + (ph1 * 2 + 0) * NC;
+  const double* thc = A.th + (ph1 * 2 + 1) * NC;
+  const double tm = admit_eq<NC>(thm, X1), tc = admit_eq<NC>(thc, X1);
   // Roofline max of the two segments; ties stay memory-bound.
   const int seg = (tc > tm) ? 1 : 0;
   const double t1 = seg ? tc : tm;
-  // the candidate's own terms of Eq. 1 in B'
-  const double x[5] = {A.S[0] / (double)n1, A.S[1] * (double)p, A.S[2] * (double)c,
-                       A.S[3] * (double)(p * p), (double)n1};
-  const double f = eq1(seg ? thc : thm, x);
+  // the candidate's own terms in B'
+  const double x[7] = {A.S[0] / (double)n1, A.S[1] * (double)p, A.S[2] * (double)c,
+                       A.S[3] * (double)(p * p), (double)n1, A.S[4] * (double)(p * c), A.S[5]};
+  const double f = admit_eq<NC>(seg ? thc : thm, x);
   if (t_after) t_after[j] = (float)t1;
   if (delta) delta[j] = (float)(t1 - t0);
   if (share) share[j] = (float)f;

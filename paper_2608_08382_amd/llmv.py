@@ -26,7 +26,7 @@ LLMV_TENANTS_MAX = 1 << 24
 
 EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_sweep_workspace_size",
            "llmv_attribute", "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
-           "llmv_batch_sums", "llmv_batch_sums_ext", "llmv_admit", "llmv_fit_workspace_size", "llmv_fit",
+           "llmv_batch_sums", "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit_workspace_size", "llmv_fit",
            "llmv_fit_metrics", "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
            "llmv_attribute_ext",
            "llmv_last_error", "llmv_set_kernel_events")
@@ -76,6 +76,7 @@ def load(path: str = LIB_PATH):
             lib.llmv_batch_sums.argtypes = [P, P, P, P, sz, P]
             lib.llmv_batch_sums_ext.argtypes = [P, P, P, P, sz, P]
             lib.llmv_admit.argtypes = [P, P, i64, P, P, P, P, P, i64, P, P, P, P, P]
+            lib.llmv_admit_ext.argtypes = [P, P, i64, P, P, P, P, P, i64, P, P, P, P, P]
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
             lib.llmv_shape_constants_ext.argtypes = [P, P]
             lib.llmv_attribute_ext.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
@@ -91,7 +92,8 @@ def load(path: str = LIB_PATH):
             lib.llmv_set_kernel_events.restype = ctypes.c_int
             for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
                       "llmv_features", "llmv_tenant_sums", "llmv_validate", "llmv_batch_sums",
-                      "llmv_batch_sums_ext", "llmv_admit", "llmv_fit", "llmv_fit_metrics",
+                      "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit",
+                      "llmv_fit_metrics",
                       "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
                       "llmv_attribute_ext"):
                 getattr(lib, f).restype = ctypes.c_int
@@ -217,16 +219,27 @@ def llmv_batch_sums(trace: DeviceTrace, sums=None, phase=None, ws=None, stream=N
 
 
 def llmv_admit(sums, phase, n_batches: int, shape, coeffs, cand_batch, cand_p, cand_c,
-               t_after=None, delta=None, share=None, regime=None, stream=None):
+               t_after=None, delta=None, share=None, regime=None, stream=None, ext=False):
     """Device tensors: sums int64 [4, n_batches], phase uint8 [n_batches],
-    cand_batch int64 [m], cand_p / cand_c int32 [m]; outputs fp32 / uint8 [m]."""
-    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    cand_batch int64 [m], cand_p / cand_c int32 [m]; outputs fp32 / uint8 [m].
+    With ext the extended model (llmv_admit_ext): sums [5, n_batches], 28
+    coefficients."""
+    k = 28 if ext else 20
+    co = (ctypes.c_float * k)(*[float(v) for v in coeffs])
     sh = make_shape(shape)
     m = int(cand_p.numel())
-    _check(load().llmv_admit(_ptr(sums), _ptr(phase), int(n_batches), _shape_ref(sh), co,
-                             _ptr(cand_batch), _ptr(cand_p), _ptr(cand_c), m, _ptr(t_after),
-                             _ptr(delta), _ptr(share), _ptr(regime), _stream(stream)),
-           "llmv_admit")
+    fn, name = (load().llmv_admit_ext, "llmv_admit_ext") if ext else (load().llmv_admit,
+                                                                     "llmv_admit")
+    _check(fn(_ptr(sums), _ptr(phase), int(n_batches), _shape_ref(sh), co, _ptr(cand_batch),
+              _ptr(cand_p), _ptr(cand_c), m, _ptr(t_after), _ptr(delta), _ptr(share), _ptr(regime),
+              _stream(stream)), name)
+
+
+def llmv_admit_ext(sums, phase, n_batches: int, shape, coeffs, cand_batch, cand_p, cand_c,
+                   t_after=None, delta=None, share=None, regime=None, stream=None):
+    """llmv_admit for the extended model: sums [5, n_batches], 28 coefficients."""
+    llmv_admit(sums, phase, n_batches, shape, coeffs, cand_batch, cand_p, cand_c, t_after, delta,
+               share, regime, stream, ext=True)
 
 
 def llmv_shape_constants_ext(shape=None):
@@ -417,9 +430,9 @@ def batch_sums(trace: DeviceTrace, ws=None, ext=False):
     return sums, phase
 
 
-def admit(sums, phase, shape, coeffs, cand_batch, cand_p, cand_c):
+def admit(sums, phase, shape, coeffs, cand_batch, cand_p, cand_c, ext=False):
     """Allocates the outputs (t_after, delta, share fp32; regime uint8) and
-    runs llmv_admit; returns them in a dict."""
+    runs llmv_admit (llmv_admit_ext with ext); returns them in a dict."""
     m = int(cand_p.numel())
     dev = cand_p.device
     out = {"t_after": torch.empty(m, dtype=torch.float32, device=dev),
@@ -427,7 +440,7 @@ def admit(sums, phase, shape, coeffs, cand_batch, cand_p, cand_c):
            "share": torch.empty(m, dtype=torch.float32, device=dev),
            "regime": torch.empty(m, dtype=torch.uint8, device=dev)}
     llmv_admit(sums, phase, int(phase.numel()), shape, coeffs, cand_batch, cand_p, cand_c,
-               out["t_after"], out["delta"], out["share"], out["regime"])
+               out["t_after"], out["delta"], out["share"], out["regime"], ext=ext)
     return out
 
 

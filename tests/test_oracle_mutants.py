@@ -69,6 +69,10 @@ MUTANTS = [
     ("ext coefficient stride 5", "(double)coeffs[(ph * 2 + s) * 7 + k];",
      "(double)coeffs[(ph * 2 + s) * 5 + k];"),
     ("ext last term dropped", "for (int k = 1; k < 7; ++k)", "for (int k = 1; k < 6; ++k)"),
+    ("ext admission: B under Eq. 1", "rc = orc_attribute_ext(1, n, off0, p, c,",
+     "rc = orc_attribute(1, n, off0, p, c,"),
+    ("ext admission: candidate's other-segment share", "if (share) *share = f1[n];",
+     "if (share) *share = g1[n];"),
 ]
 EXT = json.load(open(os.path.join(ROOT, "tests", "golden", "ext_examples.json")))
 EXT_SETS = ("prefill_mem", "prefill_comp", "decode_mem", "decode_comp")
@@ -161,6 +165,11 @@ def battery(orc: oracle.Oracle):
     tr = tracegen.from_batches([([2], [0]), ([], []), ([1], [3])], None, 1)
     r = orc.attribute(tr.offsets, tr.p, tr.c, None, None, wide, 0, ("T", "regime"), ext=True)
     assert r["regime"][1] == 255 and r["T"][1] == 0.0
+    # the extended admission query (hand-worked, test_oracle_admission_ext.py)
+    co = np.array([8, 1, 0.5, 0, 0, 0.25, 2, 1, 2, 0, 0.25, 0, 0, 0] + [0] * 14, np.float32)
+    r = orc.admit([4], [8], 2, 4, None, co, ext=True)
+    assert (r["T_after"], r["delta"], r["share"], r["share_alt"], r["regime"]) == \
+        (34.0, 8.0, 12.0, 5.5, 0)
 
 
 def _build(tmp_path, text, tag):
