@@ -234,9 +234,10 @@ def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
     sums5 = torch.empty((5, tr.n_batches), dtype=torch.int64, device=dev)
     llmv.llmv_batch_sums_ext(dt, sums5, phase, ws)
     co28 = tracegen.ext_coeffs(104)
+    ox = {k: torch.empty_like(v) for k, v in out.items()}
     ms_ax = timed(lambda: llmv.llmv_admit_ext(sums5, phase, tr.n_batches, tr.shape, co28, cb, cp,
-                                              cc, out["t_after"], out["delta"], out["share"],
-                                              out["regime"]))
+                                              cc, ox["t_after"], ox["delta"], ox["share"],
+                                              ox["regime"]))
     del sums5
     res["extended"] = {"admit_ms": ms_ax, "value": m / (ms_ax / 1e3), "unit": "queries/s"}
     log(f"[bench] admission (extended model): {m} queries in {ms_ax:.3f} ms "
@@ -259,6 +260,18 @@ def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
                         abs(float(host["share"][j]) - r["share"]) / abs(r["share"]))
         dt_o = time.perf_counter() - t0
         assert worst <= parity.RTOL, worst
+        hx = {k: v.cpu().numpy() for k, v in ox.items()}
+        worst_x = 0.0
+        for j in idx[:100]:
+            b = cb_h[j]
+            lo, hi = tr.offsets[b], tr.offsets[b + 1]
+            r = oracle.admit_ext(tr.p[lo:hi], tr.c[lo:hi], cp_h[j], cc_h[j], tr.shape, co28)
+            if parity.tie_zone(np.array([r["TM_after"]]), np.array([r["TC_after"]]))[0]:
+                continue
+            worst_x = max(worst_x, abs(float(hx["t_after"][j]) - r["T_after"]) / r["T_after"],
+                          abs(float(hx["share"][j]) - r["share"]) / abs(r["share"]))
+        assert worst_x <= parity.RTOL, worst_x
+        res["extended"]["parity_max_rel_err"] = worst_x
         res["cpu_baseline"] = {"value": len(idx) / dt_o, "unit": "queries/s", "cores": 1,
                                "kind": "oracle", "sample": f"{len(idx)} of {m} queries"}
         res["parity_max_rel_err"] = worst
