@@ -100,7 +100,9 @@ def cpu_baseline(tr, coeffs, gpu_out, budget_s=30.0):
 
 def bench_sweep(hip, stream, with_oracle):
     """What-if sweep: tenant sums of the 100k-batch mixed trace under 4 model
-    shapes x 256 coefficient vectors, one llmv_attribute_sweep call."""
+    shapes x 256 coefficient vectors, one llmv_attribute_sweep call; then the
+    same under 4 x 256 settings of the extended model
+    (llmv_attribute_sweep_ext)."""
     import numpy as np
     import torch
     import tracegen
@@ -147,6 +149,32 @@ def bench_sweep(hip, stream, with_oracle):
                                "unit": "request-variants/s", "cores": 1, "kind": "oracle",
                                "sample": f"{len(sample)} of {variants} variants, full trace"}
         res["parity_tenant_max_rel_err"] = worst
+    # the extended model: 28 coefficients per setting
+    del ws
+    co28 = np.stack([tracegen.ext_coeffs(600 + j) for j in range(256)])
+    wsx = llmv.sweep_workspace(tr.n_batches, tr.n_requests, tr.n_tenants, ext=True)
+    llmv.llmv_attribute_sweep_ext(dt, shapes, co28, tr.n_tenants, out, wsx)
+    torch.cuda.synchronize()
+    evs = [(hip.create(), hip.create()) for _ in range(reps)]
+    for a, b in evs:
+        hip.record(a, stream)
+        llmv.llmv_attribute_sweep_ext(dt, shapes, co28, tr.n_tenants, out, wsx)
+        hip.record(b, stream)
+    torch.cuda.synchronize()
+    msx = sorted(hip.elapsed_ms(a, b) for a, b in evs)[reps // 2]
+    res["extended"] = {"ms": msx, "value": tr.n_requests * variants / (msx / 1e3),
+                       "unit": "request-variants/s"}
+    log(f"[bench] what-if sweep (extended model): {variants} variants in {msx:.2f} ms, "
+        f"{res['extended']['value']:.3e} request-variants/s")
+    if with_oracle:
+        host = out.cpu().numpy()
+        worst_x = 0.0
+        for s, v in [(0, 3), (3, 250)]:
+            ref = oracle.attribute_ext(tr.offsets, tr.p, tr.c, tr.tenant, shapes[s], co28[v],
+                                       tr.n_tenants, ("tenant_sums",))["tenant_sums"]
+            worst_x = max(worst_x, float(parity.rel_err(host[s, v], ref).max()))
+        assert worst_x <= parity.RTOL, worst_x
+        res["extended"]["parity_tenant_max_rel_err"] = worst_x
     return res
 
 

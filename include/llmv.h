@@ -113,6 +113,10 @@ size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tena
  * and a few KiB. */
 size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
 
+/* llmv_sweep_workspace_size for llmv_attribute_sweep_ext: 4 more bytes per
+ * request (the groups' sums of p*c) and 8 more per batch. */
+size_t llmv_sweep_workspace_size_ext(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
+
 /* Batched attribution (Sec. 2 Problem formulation; Sec. 2.1, Eq. 1).
  *   trace     host struct, device arrays as above.
  *   shape     host, or NULL for the unit shape.
@@ -187,6 +191,24 @@ int llmv_attribute_sweep(const llmv_trace *trace, const llmv_shape *shapes,
                          int32_t n_shapes, const float *coeffs, int32_t n_coeffs,
                          int32_t n_tenants, double *out, void *ws, size_t ws_bytes,
                          void *stream);
+
+/* llmv_attribute_sweep under the extended model (readings X1-X3; Sec. 1
+ * what-if planning):
+ *   shapes   as llmv_attribute_sweep; each one's S5 and S6 as in
+ *            llmv_shape_constants_ext.
+ *   coeffs   host [n_coeffs][28] finite fp32, laid out as in
+ *            llmv_attribute_ext.
+ * Equivalent, up to rounding, to n_shapes*n_coeffs calls of
+ * llmv_attribute_ext with only tenant_sums requested: a group's shares sum
+ * to k0*n + k1*sum p + k2*sum c + k3*sum p^2 + k5*sum p*c, with k0 holding
+ * the a6 term and k5 = fp32(a5*S5), the group's sums rounded to fp32.
+ * Regimes come from the exact batch sums, as in llmv_attribute_ext.  Other
+ * arguments, limits (sum p*c per batch below 2^63, not checked) and errors
+ * as llmv_attribute_sweep; the workspace is llmv_sweep_workspace_size_ext's. */
+int llmv_attribute_sweep_ext(const llmv_trace *trace, const llmv_shape *shapes,
+                             int32_t n_shapes, const float *coeffs, int32_t n_coeffs,
+                             int32_t n_tenants, double *out, void *ws, size_t ws_bytes,
+                             void *stream);
 
 /* Exact per-batch sums of Eq. 1 and the batch phase (Sec. 2.1), the state
  * an admission query starts from:

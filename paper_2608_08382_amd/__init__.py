@@ -7,6 +7,7 @@ from . import llmv  # noqa: F401
 from .llmv import (DeviceTrace, LlmvError, admit, attribute, attribute_ext,  # noqa: F401
                    attribute_sweep, batch_sums, features, fit, fit_metrics, fit_workspace, llmv_admit,
                    llmv_attribute, llmv_attribute_ext, llmv_attribute_sweep, llmv_batch_sums,
+                   llmv_attribute_sweep_ext, llmv_sweep_workspace_size_ext,
                    llmv_batch_sums_ext, llmv_fit_ext, llmv_fit_metrics_ext, llmv_admit_ext,
                    llmv_features, llmv_shape_constants_ext,
                    llmv_fit, llmv_fit_metrics, llmv_fit_workspace_size, llmv_last_error,

@@ -73,11 +73,13 @@ int sweep_group(int32_t T) {
 }
 static_assert(2 * (kHistLdsMax + kHotSlots) * sizeof(double) <= kSweepHistLds, "sweep LDS");
 
-typedef void (*SweepKernel)(const GroupSweep, const VarTable);
-SweepKernel pick_sweep(int g) {
-  if (g >= 8) return k_sweep_groups<8>;
-  if (g >= 4) return k_sweep_groups<4>;
-  return k_sweep_groups<2>;
+template <int NC>
+using SweepKernel = void (*)(const GroupSweep, const VarTableOf<NC>);
+template <int NC>
+SweepKernel<NC> pick_sweep(int g) {
+  if (g >= 8) return k_sweep_groups<8, NC>;
+  if (g >= 4) return k_sweep_groups<4, NC>;
+  return k_sweep_groups<2, NC>;
 }
 
 struct Layout {
@@ -146,11 +148,12 @@ Layout layout(int64_t n, int32_t T, int rows = 1) {
 // The what-if sweep's groups after a Layout ending at o: slice table, slice
 // group counts and offsets, batch group offsets, exact batch sums, scan tile
 // sums, and the groups (at most one per request, plus a tile of slack that
-// the sweep tiles read past the last group).
+// the sweep tiles read past the last group); under the extended model a
+// fourth batch sum and the groups' sums of p*c.
 struct GroupLayout {
-  size_t first, scnt, soff, gofs, bsum, tsum, gw, gf, total;
+  size_t first, scnt, soff, gofs, bsum, tsum, gw, gf, gr, total;
 };
-GroupLayout group_layout(size_t o, int64_t nB, int64_t N) {
+GroupLayout group_layout(size_t o, int64_t nB, int64_t N, bool ext) {
   GroupLayout G{};
   const int64_t nS = (N + kSlice - 1) / kSlice;
   const int64_t nt = (nS + kScanTile - 1) / kScanTile;
@@ -163,13 +166,15 @@ GroupLayout group_layout(size_t o, int64_t nB, int64_t N) {
   G.gofs = o;
   o += align_up((size_t)(nB + 1) * sizeof(int64_t));
   G.bsum = o;
-  o += align_up((size_t)(3 * nB + 1) * sizeof(unsigned long long));
+  o += align_up((size_t)((ext ? 4 : 3) * nB + 1) * sizeof(unsigned long long));
   G.tsum = o;
   o += align_up((size_t)(nt + 1) * sizeof(int64_t));
   G.gw = o;
   o += align_up((size_t)(N + kGT) * sizeof(uint32_t));
   G.gf = o;
   o += align_up((size_t)(N + kGT) * sizeof(v4f));
+  G.gr = o;
+  if (ext) o += align_up((size_t)(N + kGT) * sizeof(float));
   G.total = o;
   return G;
 }
@@ -358,6 +363,163 @@ int admit_run(const int64_t* sums, const uint8_t* phase, int64_t n_batches,
   return LLMV_OK;
 }
 
+// The what-if sweep under Eq. 1 (NC = 5) or the extended model (NC = 7).
+template <int NC>
+int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shapes,
+              const float* coeffs, int32_t n_coeffs, int32_t n_tenants, double* out, void* ws,
+              size_t ws_bytes, hipStream_t st) {
+  constexpr bool EXT = NC == 7;
+  int rc = check_trace(trace, true);
+  if (rc) return rc;
+  if (n_shapes < 1 || (!shapes && n_shapes != 1))
+    return fail(LLMV_EINVAL, "n_shapes=%d (NULL shapes needs n_shapes == 1)", n_shapes);
+  if (n_coeffs < 1 || !coeffs) return fail(LLMV_EINVAL, "n_coeffs=%d or coeffs NULL", n_coeffs);
+  if (!lds_hist(n_tenants))
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, %d] for the sweep", n_tenants, kHistLdsMax);
+  if (!out) return fail(LLMV_EINVAL, "out is NULL");
+  for (int64_t i = 0; i < (int64_t)n_coeffs * 4 * NC; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%lld] is not finite", (long long)i);
+  double S[64][6];  // S0..S3 (and S5, S6)
+  if (n_shapes > 64) return fail(LLMV_EINVAL, "n_shapes=%d > 64", n_shapes);
+  for (int s = 0; s < n_shapes; ++s) {
+    const llmv_shape* sh = shapes ? &shapes[s] : nullptr;
+    rc = EXT ? shape_constants_ext(sh, S[s]) : shape_constants(sh, S[s]);
+    if (rc) return rc;
+  }
+  int cus = 0;
+  rc = device_cus(&cus);
+  if (rc) return rc;
+  const int64_t nB = trace->n_batches, N = trace->n_requests;
+  // One pass over the groups per G consecutive settings (shape-major, as in
+  // out); each pass keeps G tenant histograms in LDS.
+  const int G = sweep_group(n_tenants);
+  const Layout L = layout(N, n_tenants, G);
+  const GroupLayout GL = group_layout(L.total, nB, N, EXT);
+  rc = check_ws(ws, ws_bytes, GL.total);
+  if (rc) return rc;
+  char* base = (char*)ws;
+  const int64_t n_var = (int64_t)n_shapes * n_coeffs;
+  if (N == 0) {  // no requests: every tenant sum is zero
+    const int64_t n_out = n_var * n_tenants;
+    int64_t blocks = (n_out + kWG - 1) / kWG;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(k_zero_f64, dim3((unsigned)blocks), dim3(kWG), 0, st, out, n_out);
+    HIP_TRY(hipGetLastError(), "k_zero_f64 launch");
+    return LLMV_OK;
+  }
+  const size_t dyn = (size_t)G * (size_t)(n_tenants + kHotSlots) * sizeof(double);
+  const SweepKernel<NC> kern = pick_sweep<NC>(G);
+  const int64_t grid = grid_for(N, cus, blocks_per_cu(kern, dyn));
+  unsigned long long* claims = (unsigned long long*)(base + L.claims);
+
+  // the most frequent tenants get replicated histogram entries
+  unsigned long long* counts = (unsigned long long*)(base + L.counts);
+  int32_t* hot = (int32_t*)(base + L.hot);
+  hipLaunchKernelGGL(k_zero_u64, dim3(16), dim3(kWG), 0, st, counts, (int64_t)n_tenants);
+  HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
+  int64_t blocks = (N + (int64_t)kWG * 64 - 1) / ((int64_t)kWG * 64);
+  blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+  hipLaunchKernelGGL(k_tenant_count, dim3((unsigned)blocks), dim3(kWG),
+                     (size_t)n_tenants * sizeof(unsigned int), st, trace->tenant, N, n_tenants,
+                     counts);
+  HIP_TRY(hipGetLastError(), "k_tenant_count launch");
+  hipLaunchKernelGGL(k_hot_tenants, dim3(1), dim3(kWG), 0, st, (const unsigned long long*)counts,
+                     n_tenants, hot);
+  HIP_TRY(hipGetLastError(), "k_hot_tenants launch");
+
+  // the groups: counts and exact batch sums per slice, slice offsets, then
+  // the groups themselves
+  const int64_t nS = (N + kSlice - 1) / kSlice;
+  int64_t* first = (int64_t*)(base + GL.first);
+  int64_t* scnt = (int64_t*)(base + GL.scnt);
+  int64_t* soff = (int64_t*)(base + GL.soff);
+  int64_t* gofs = (int64_t*)(base + GL.gofs);
+  unsigned long long* bsum = (unsigned long long*)(base + GL.bsum);
+  int64_t* tsum = (int64_t*)(base + GL.tsum);
+  uint32_t* gw = (uint32_t*)(base + GL.gw);
+  v4f* gf = (v4f*)(base + GL.gf);
+  float* gr = EXT ? (float*)(base + GL.gr) : nullptr;
+  ChunkMap sm{};  // equal slices, none claimed
+  sm.s1 = kSlice;
+  sm.s2 = 1;
+  sm.n_static = nS;
+  sm.n_chunks = nS;
+  sm.F = nS * kSlice;
+  rc = partition(trace, sm, first, claims, st);
+  if (rc) return rc;
+  hipLaunchKernelGGL(k_zero_u64, dim3(256), dim3(kWG), 0, st, bsum, (EXT ? 4 : 3) * nB);
+  HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
+  int64_t bgrid = (nS + kWaves - 1) / kWaves;
+  const int64_t bcap = (int64_t)cus * blocks_per_cu(k_group_build<true, EXT>, 0);
+  if (bgrid > bcap) bgrid = bcap;
+  hipLaunchKernelGGL((k_group_build<false, EXT>), dim3((unsigned)bgrid), dim3(kWG), 0, st,
+                     trace->offsets, trace->p, trace->c, trace->tenant, nB, N, (const int64_t*)first,
+                     nS, scnt, bsum, (const int64_t*)nullptr, (int64_t*)nullptr, (uint32_t*)nullptr,
+                     (v4f*)nullptr, (float*)nullptr);
+  HIP_TRY(hipGetLastError(), "k_group_build launch");
+  const int64_t nt = (nS + kScanTile - 1) / kScanTile;  // >= 1
+  hipLaunchKernelGGL(k_scan_tiles, dim3((unsigned)nt), dim3(kScanWG), 0, st, (const int64_t*)scnt, nS,
+                     tsum);
+  HIP_TRY(hipGetLastError(), "k_scan_tiles launch");
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanWG), 0, st, tsum, nt);
+  HIP_TRY(hipGetLastError(), "k_scan_top launch");
+  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nt), dim3(kScanWG), 0, st, (const int64_t*)scnt, nS,
+                     (const int64_t*)tsum, soff);
+  HIP_TRY(hipGetLastError(), "k_scan_apply launch");
+  hipLaunchKernelGGL((k_group_build<true, EXT>), dim3((unsigned)bgrid), dim3(kWG), 0, st,
+                     trace->offsets, trace->p, trace->c, trace->tenant, nB, N, (const int64_t*)first,
+                     nS, (int64_t*)nullptr, (unsigned long long*)nullptr, (const int64_t*)soff, gofs,
+                     gw, gf, gr);
+  HIP_TRY(hipGetLastError(), "k_group_build launch");
+
+  // the passes: the chunks of k_tiles over the batches; every launch takes
+  // exactly n_chunks claims (one per chunk it runs, the static ones
+  // included), so launch i starts at claim i * n_chunks
+  const ChunkMap cm = chunk_map(N, grid * kWaves, false);  // one static chunk per wave
+  int64_t* wg_first = (int64_t*)(base + L.wg_first);
+  rc = partition(trace, cm, wg_first, claims, st);
+  if (rc) return rc;
+  GroupSweep Q{};
+  Q.off = trace->offsets;
+  Q.gofs = gofs;
+  Q.bsum = bsum;
+  Q.gw = gw;
+  Q.gf = gf;
+  Q.gr = gr;
+  Q.nB = nB;
+  Q.wg_first = wg_first;
+  Q.claims = claims;
+  Q.n_chunks = cm.n_chunks;
+  Q.partials = (double*)(base + L.partials);
+  Q.n_tenants = n_tenants;
+  Q.hot = hot;
+  int64_t launch = 0;
+  for (int64_t v0 = 0; v0 < n_var; v0 += G, ++launch) {
+    VarTableOf<NC> V{};
+    V.n = (int32_t)(n_var - v0 < G ? n_var - v0 : G);
+    for (int g = 0; g < V.n; ++g) {
+      const int64_t v = v0 + g;
+      const int s = (int)(v / n_coeffs);
+      const int64_t j = v % n_coeffs;
+      for (int k = 0; k < NC - 1; ++k) V.S[g][k] = S[s][k];
+      for (int i = 0; i < 4 * NC; ++i) V.th[g][i] = (double)coeffs[j * 4 * NC + i];
+      for (int r = 0; r < 4; ++r) {
+        for (int k = 1; k < 4; ++k) V.K[g][r][k - 1] = (float)(V.th[g][r * NC + k] * S[s][k]);
+        if (EXT) V.K[g][r][3] = (float)(V.th[g][r * NC + 5] * S[s][4]);
+      }
+    }
+    Q.claim_base = (uint64_t)launch * (uint64_t)cm.n_chunks;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, Q, V);
+    HIP_TRY(hipGetLastError(), "k_sweep_groups launch");
+    const int n_hist = V.n * n_tenants;
+    hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)((n_hist + kTenantChunk - 1) / kTenantChunk)),
+                       dim3(64 * kReduceWaves), 0, st, (const double*)Q.partials, (int)grid, n_hist,
+                       out + v0 * n_tenants);
+    HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+  }
+  return LLMV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -383,12 +545,20 @@ size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tena
   return layout(n, n_tenants > 0 ? n_tenants : 0).total;
 }
 
-size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
+static size_t sweep_ws(int64_t n_batches, int64_t n_requests, int32_t n_tenants, bool ext) {
   const int64_t nB = n_batches > 0 ? n_batches : 0;
   const int64_t n = n_requests > 0 ? n_requests : 0;
   const int32_t T = n_tenants > 0 ? n_tenants : 0;
   const Layout L = layout(n, T, lds_hist(T) ? sweep_group(T) : 1);
-  return group_layout(L.total, nB, n).total;
+  return group_layout(L.total, nB, n, ext).total;
+}
+
+size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
+  return sweep_ws(n_batches, n_requests, n_tenants, false);
+}
+
+size_t llmv_sweep_workspace_size_ext(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {
+  return sweep_ws(n_batches, n_requests, n_tenants, true);
 }
 
 int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[20],
@@ -431,150 +601,15 @@ int llmv_attribute_ext(const llmv_trace* trace, const llmv_shape* shape, const f
 int llmv_attribute_sweep(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shapes,
                          const float* coeffs, int32_t n_coeffs, int32_t n_tenants, double* out,
                          void* ws, size_t ws_bytes, void* stream) {
-  int rc = check_trace(trace, true);
-  if (rc) return rc;
-  if (n_shapes < 1 || (!shapes && n_shapes != 1))
-    return fail(LLMV_EINVAL, "n_shapes=%d (NULL shapes needs n_shapes == 1)", n_shapes);
-  if (n_coeffs < 1 || !coeffs) return fail(LLMV_EINVAL, "n_coeffs=%d or coeffs NULL", n_coeffs);
-  if (!lds_hist(n_tenants))
-    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, %d] for the sweep", n_tenants, kHistLdsMax);
-  if (!out) return fail(LLMV_EINVAL, "out is NULL");
-  for (int64_t i = 0; i < (int64_t)n_coeffs * 20; ++i)
-    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%lld] is not finite", (long long)i);
-  double S[64][4];
-  if (n_shapes > 64) return fail(LLMV_EINVAL, "n_shapes=%d > 64", n_shapes);
-  for (int s = 0; s < n_shapes; ++s) {
-    rc = shape_constants(shapes ? &shapes[s] : nullptr, S[s]);
-    if (rc) return rc;
-  }
-  hipStream_t st = (hipStream_t)stream;
-  int cus = 0;
-  rc = device_cus(&cus);
-  if (rc) return rc;
-  const int64_t nB = trace->n_batches, N = trace->n_requests;
-  // One pass over the groups per G consecutive settings (shape-major, as in
-  // out); each pass keeps G tenant histograms in LDS.
-  const int G = sweep_group(n_tenants);
-  const Layout L = layout(N, n_tenants, G);
-  const GroupLayout GL = group_layout(L.total, nB, N);
-  rc = check_ws(ws, ws_bytes, GL.total);
-  if (rc) return rc;
-  char* base = (char*)ws;
-  const int64_t n_var = (int64_t)n_shapes * n_coeffs;
-  if (N == 0) {  // no requests: every tenant sum is zero
-    const int64_t n_out = n_var * n_tenants;
-    int64_t blocks = (n_out + kWG - 1) / kWG;
-    if (blocks > 1024) blocks = 1024;
-    hipLaunchKernelGGL(k_zero_f64, dim3((unsigned)blocks), dim3(kWG), 0, st, out, n_out);
-    HIP_TRY(hipGetLastError(), "k_zero_f64 launch");
-    return LLMV_OK;
-  }
-  const size_t dyn = (size_t)G * (size_t)(n_tenants + kHotSlots) * sizeof(double);
-  const SweepKernel kern = pick_sweep(G);
-  const int64_t grid = grid_for(N, cus, blocks_per_cu(kern, dyn));
-  unsigned long long* claims = (unsigned long long*)(base + L.claims);
+  return sweep_run<5>(trace, shapes, n_shapes, coeffs, n_coeffs, n_tenants, out, ws, ws_bytes,
+                      (hipStream_t)stream);
+}
 
-  // the most frequent tenants get replicated histogram entries
-  unsigned long long* counts = (unsigned long long*)(base + L.counts);
-  int32_t* hot = (int32_t*)(base + L.hot);
-  hipLaunchKernelGGL(k_zero_u64, dim3(16), dim3(kWG), 0, st, counts, (int64_t)n_tenants);
-  HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
-  int64_t blocks = (N + (int64_t)kWG * 64 - 1) / ((int64_t)kWG * 64);
-  blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
-  hipLaunchKernelGGL(k_tenant_count, dim3((unsigned)blocks), dim3(kWG),
-                     (size_t)n_tenants * sizeof(unsigned int), st, trace->tenant, N, n_tenants,
-                     counts);
-  HIP_TRY(hipGetLastError(), "k_tenant_count launch");
-  hipLaunchKernelGGL(k_hot_tenants, dim3(1), dim3(kWG), 0, st, (const unsigned long long*)counts,
-                     n_tenants, hot);
-  HIP_TRY(hipGetLastError(), "k_hot_tenants launch");
-
-  // the groups: counts and exact batch sums per slice, slice offsets, then
-  // the groups themselves
-  const int64_t nS = (N + kSlice - 1) / kSlice;
-  int64_t* first = (int64_t*)(base + GL.first);
-  int64_t* scnt = (int64_t*)(base + GL.scnt);
-  int64_t* soff = (int64_t*)(base + GL.soff);
-  int64_t* gofs = (int64_t*)(base + GL.gofs);
-  unsigned long long* bsum = (unsigned long long*)(base + GL.bsum);
-  int64_t* tsum = (int64_t*)(base + GL.tsum);
-  uint32_t* gw = (uint32_t*)(base + GL.gw);
-  v4f* gf = (v4f*)(base + GL.gf);
-  ChunkMap sm{};  // equal slices, none claimed
-  sm.s1 = kSlice;
-  sm.s2 = 1;
-  sm.n_static = nS;
-  sm.n_chunks = nS;
-  sm.F = nS * kSlice;
-  rc = partition(trace, sm, first, claims, st);
-  if (rc) return rc;
-  hipLaunchKernelGGL(k_zero_u64, dim3(256), dim3(kWG), 0, st, bsum, 3 * nB);
-  HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
-  int64_t bgrid = (nS + kWaves - 1) / kWaves;
-  const int64_t bcap = (int64_t)cus * blocks_per_cu(k_group_build<true>, 0);
-  if (bgrid > bcap) bgrid = bcap;
-  hipLaunchKernelGGL(k_group_build<false>, dim3((unsigned)bgrid), dim3(kWG), 0, st, trace->offsets,
-                     trace->p, trace->c, trace->tenant, nB, N, (const int64_t*)first, nS, scnt, bsum,
-                     (const int64_t*)nullptr, (int64_t*)nullptr, (uint32_t*)nullptr, (v4f*)nullptr);
-  HIP_TRY(hipGetLastError(), "k_group_build launch");
-  const int64_t nt = (nS + kScanTile - 1) / kScanTile;  // >= 1
-  hipLaunchKernelGGL(k_scan_tiles, dim3((unsigned)nt), dim3(kScanWG), 0, st, (const int64_t*)scnt, nS,
-                     tsum);
-  HIP_TRY(hipGetLastError(), "k_scan_tiles launch");
-  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanWG), 0, st, tsum, nt);
-  HIP_TRY(hipGetLastError(), "k_scan_top launch");
-  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nt), dim3(kScanWG), 0, st, (const int64_t*)scnt, nS,
-                     (const int64_t*)tsum, soff);
-  HIP_TRY(hipGetLastError(), "k_scan_apply launch");
-  hipLaunchKernelGGL(k_group_build<true>, dim3((unsigned)bgrid), dim3(kWG), 0, st, trace->offsets,
-                     trace->p, trace->c, trace->tenant, nB, N, (const int64_t*)first, nS,
-                     (int64_t*)nullptr, (unsigned long long*)nullptr, (const int64_t*)soff, gofs, gw,
-                     gf);
-  HIP_TRY(hipGetLastError(), "k_group_build launch");
-
-  // the passes: the chunks of k_tiles over the batches; every launch takes
-  // exactly n_chunks claims (one per chunk it runs, the static ones
-  // included), so launch i starts at claim i * n_chunks
-  const ChunkMap cm = chunk_map(N, grid * kWaves, false);  // one static chunk per wave
-  int64_t* wg_first = (int64_t*)(base + L.wg_first);
-  rc = partition(trace, cm, wg_first, claims, st);
-  if (rc) return rc;
-  GroupSweep Q{};
-  Q.off = trace->offsets;
-  Q.gofs = gofs;
-  Q.bsum = bsum;
-  Q.gw = gw;
-  Q.gf = gf;
-  Q.nB = nB;
-  Q.wg_first = wg_first;
-  Q.claims = claims;
-  Q.n_chunks = cm.n_chunks;
-  Q.partials = (double*)(base + L.partials);
-  Q.n_tenants = n_tenants;
-  Q.hot = hot;
-  int64_t launch = 0;
-  for (int64_t v0 = 0; v0 < n_var; v0 += G, ++launch) {
-    VarTable V{};
-    V.n = (int32_t)(n_var - v0 < G ? n_var - v0 : G);
-    for (int g = 0; g < V.n; ++g) {
-      const int64_t v = v0 + g;
-      const int s = (int)(v / n_coeffs);
-      const int64_t j = v % n_coeffs;
-      for (int k = 0; k < 4; ++k) V.S[g][k] = S[s][k];
-      for (int i = 0; i < 20; ++i) V.th[g][i] = (double)coeffs[j * 20 + i];
-      for (int r = 0; r < 4; ++r)
-        for (int k = 1; k < 4; ++k) V.K[g][r][k - 1] = (float)(V.th[g][r * 5 + k] * S[s][k]);
-    }
-    Q.claim_base = (uint64_t)launch * (uint64_t)cm.n_chunks;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, Q, V);
-    HIP_TRY(hipGetLastError(), "k_sweep_groups launch");
-    const int n_hist = V.n * n_tenants;
-    hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)((n_hist + kTenantChunk - 1) / kTenantChunk)),
-                       dim3(64 * kReduceWaves), 0, st, (const double*)Q.partials, (int)grid, n_hist,
-                       out + v0 * n_tenants);
-    HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
-  }
-  return LLMV_OK;
+int llmv_attribute_sweep_ext(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shapes,
+                             const float* coeffs, int32_t n_coeffs, int32_t n_tenants, double* out,
+                             void* ws, size_t ws_bytes, void* stream) {
+  return sweep_run<7>(trace, shapes, n_shapes, coeffs, n_coeffs, n_tenants, out, ws, ws_bytes,
+                      (hipStream_t)stream);
 }
 
 int llmv_batch_sums(const llmv_trace* trace, int64_t* sums, uint8_t* phase, void* ws,

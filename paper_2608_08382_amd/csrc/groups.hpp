@@ -7,7 +7,10 @@
 // a4 term per request), so the shares of one tenant's requests in one batch
 // sum to k0*n + k1*P + k2*C + k3*Q over that group's count n and sums P, C,
 // Q.  The sweep forms these (batch, tenant) groups once per call and then,
-// per setting, adds one term per group instead of one per request.
+// per setting, adds one term per group instead of one per request.  Under
+// the extended model (NC = 7: the a5 term on p*c, the a6 term per request)
+// a share gains k5*p*c and k0 gains a6*S6, so a group also carries R = its
+// sum of p*c and adds k5*R.
 //
 //  * k_group_build<false>: per slice of kSlice requests, the number of
 //    groups, and the exact batch sums; k_scan_*: the slices' group offsets;
@@ -15,10 +18,10 @@
 //    per slice; a wave-private LDS hash table keyed by tenant collects the
 //    group sums and is emitted when it fills or the batch part ends (a tenant
 //    emitted twice in one batch only costs an extra group: sums are linear).
-//  * k_sweep_groups<NV>: one pass of NV settings over the groups.  Wave
+//  * k_sweep_groups<NV, NC>: one pass of NV settings over the groups.  Wave
 //    tiles are runs of whole batches (at most kGB batches, kGT group slots);
 //    lane j evaluates batch j of the tile under every setting into a per-wave
-//    LDS table of (k0, k1, k2, k3); lane-local runs of kGV groups then add
+//    LDS table of (k0, k1, k2, k3) (and k5); lane-local runs of kGV groups then add
 //    their group sums into per-setting fp64 LDS tenant histograms, flushed to
 //    [grid][NV][n_tenants] partials that k_tenant_reduce folds.
 #pragma once
@@ -29,18 +32,22 @@ namespace llmv {
 
 // ------------------------------------------------------------ settings
 
-// The settings of one pass: shape constants and Eq. 1 coefficients
-// (theta[phase][segment][k], as in Params) of each, and the batch-independent
-// share constants k1..k3 = fp32(theta_a1*S1, theta_a2*S2, theta_a3*S3) of each
-// regime (2*phase + segment), rounded from the same fp64 products as in
-// MODE_ATTR.
+// The settings of one pass: shape constants and coefficients
+// (theta[phase][segment][k], NC terms per set, as in Params or ExtModel) of
+// each, and the batch-independent share constants k1..k3 = fp32(theta_a1*S1,
+// theta_a2*S2, theta_a3*S3) and k5 = fp32(theta_a5*S5) of each regime
+// (2*phase + segment), rounded from the same fp64 products as in MODE_ATTR
+// and MODE_EXT.
 constexpr int kSweepG = 8;
-struct VarTable {
-  int32_t n;                // settings in this pass, 1..kSweepG
-  double S[kSweepG][4];
-  double th[kSweepG][20];
-  float K[kSweepG][4][4];   // [setting][regime][k1, k2, k3, unused]
+template <int NC>
+struct VarTableOf {
+  static_assert(NC == 5 || NC == 7, "Eq. 1 or the extended model");
+  int32_t n;                    // settings in this pass, 1..kSweepG
+  double S[kSweepG][NC - 1];    // S0..S3 (and S5, S6)
+  double th[kSweepG][4 * NC];
+  float K[kSweepG][4][4];       // [setting][regime][k1, k2, k3, k5 (NC = 7)]
 };
+using VarTable = VarTableOf<5>;
 // Under tenant skew many lanes of one LDS atomic hit the same histogram
 // entry and serialize.  Each of the kHot most frequent tenants gets kHotRep
 // histogram entries per setting (lane l adds into entry l % kHotRep), folded
@@ -50,24 +57,36 @@ constexpr int kHotRep = 4;
 constexpr int kHotSlots = kHot * kHotRep;
 
 // One batch under every setting: k0 of setting g (fp32, rounded from fp64
-// as in MODE_ATTR) into k0[g]; returns the segments (bit g).
-template <int NV>
-__device__ __forceinline__ uint32_t sweep_batch(const VarTable& V, int64_t n, uint64_t Psum,
-                                                uint64_t Csum, uint64_t Qsum, bool prefill,
-                                                float* k0) {
+// as in MODE_ATTR / MODE_EXT) into k0[g]; returns the segments (bit g).
+// Rsum (sum p*c) is read only under the extended model.
+template <int NV, int NC>
+__device__ __forceinline__ uint32_t sweep_batch(const VarTableOf<NC>& V, int64_t n, uint64_t Psum,
+                                                uint64_t Csum, uint64_t Qsum, uint64_t Rsum,
+                                                bool prefill, float* k0) {
+  (void)Rsum;
   const int phase = prefill ? 0 : 1;
   uint32_t segs = 0;
   for (int g = 0; g < NV; ++g) {
     const double* S = V.S[g];
-    const double X[5] = {S[0], S[1] * (double)Psum, S[2] * (double)Csum, S[3] * (double)Qsum,
-                         (double)n * (double)n};
-    const double* thm = V.th[g] + (phase * 2 + 0) * 5;
-    const double* thc = V.th[g] + (phase * 2 + 1) * 5;
-    // Roofline max of the two segments; ties stay memory-bound.
-    const bool comp = eq1(thc, X) > eq1(thm, X);
+    const double* thm = V.th[g] + (phase * 2 + 0) * NC;
+    const double* thc = V.th[g] + (phase * 2 + 1) * NC;
+    bool comp;
+    if constexpr (NC == 5) {
+      const double X[5] = {S[0], S[1] * (double)Psum, S[2] * (double)Csum, S[3] * (double)Qsum,
+                           (double)n * (double)n};
+      // Roofline max of the two segments; ties stay memory-bound.
+      comp = eq1(thc, X) > eq1(thm, X);
+    } else {
+      const double X[7] = {S[0], S[1] * (double)Psum, S[2] * (double)Csum, S[3] * (double)Qsum,
+                           (double)n * (double)n, S[4] * (double)Rsum, S[5] * (double)n};
+      comp = eq7(thc, X) > eq7(thm, X);
+    }
     const double* th = comp ? thc : thm;
     segs |= (uint32_t)comp << g;
-    k0[g] = (float)(th[0] * (S[0] / (double)n) + th[4] * (double)n);
+    if constexpr (NC == 5)
+      k0[g] = (float)(th[0] * (S[0] / (double)n) + th[4] * (double)n);
+    else
+      k0[g] = (float)(th[0] * (S[0] / (double)n) + th[4] * (double)n + th[6] * S[5]);
   }
   return segs;
 }
@@ -135,10 +154,12 @@ constexpr int64_t kSlice = 2048;           // requests per build slice
 static_assert(kHistLdsMax <= (1 << kGrpTenantBits), "sweep tenant ids fit the group word");
 static_assert(kGrpFlush + 64 < kGrpSlots, "a round always finds a free slot");
 
+template <bool EXT>
 struct GroupTable {  // one wave's
   uint32_t key[kGrpSlots];
   uint32_t n[kGrpSlots];
   unsigned long long p[kGrpSlots], c[kGrpSlots], q[kGrpSlots];
+  unsigned long long r[EXT ? kGrpSlots : 1];  // sum p*c (EXT)
 };
 
 __device__ __forceinline__ uint32_t grp_hash(uint32_t t) {
@@ -152,28 +173,29 @@ __device__ __forceinline__ uint32_t grp_hash(uint32_t t) {
 // contiguous even when slices split it.  first[k] = the first batch starting
 // at or after request k*kSlice (k_partition over equal chunks).
 // WRITE = false: slice_cnt[k] = groups of slice k; bsum[j*nB + b] (zeroed
-// beforehand) += (sum p, sum c + 2^48 * count of c == 0, sum p^2) of the part
-// of batch b in the slice.  WRITE = true: the groups from slice_off[k] on,
-// gw = ((b mod 2^20) << 12) | tenant and gf = (n, P, C, Q) rounded to fp32,
-// and gofs[b] for every batch starting in the slice (gofs[nB] by the last).
-// Both passes emit the same groups: the emission points depend only on the
-// data.
-template <bool WRITE>
+// beforehand) += (sum p, sum c + 2^48 * count of c == 0, sum p^2, and with
+// EXT sum p*c) of the part of batch b in the slice.  WRITE = true: the groups
+// from slice_off[k] on, gw = ((b mod 2^20) << 12) | tenant, gf = (n, P, C, Q)
+// and with EXT gr = R (sum p*c), rounded to fp32, and gofs[b] for every
+// batch starting in the slice (gofs[nB] by the last).  Both passes emit the
+// same groups: the emission points depend only on the data.
+template <bool WRITE, bool EXT>
 __global__ __launch_bounds__(kWG) void k_group_build(
     const int64_t* __restrict__ off, const int32_t* __restrict__ p, const int32_t* __restrict__ c,
     const int32_t* __restrict__ tenant, int64_t nB, int64_t N, const int64_t* __restrict__ first,
     int64_t nS, int64_t* __restrict__ slice_cnt, unsigned long long* __restrict__ bsum,
     const int64_t* __restrict__ slice_off, int64_t* __restrict__ gofs, uint32_t* __restrict__ gw,
-    v4f* __restrict__ gf) {
-  __shared__ GroupTable s_tab[kWaves];
+    v4f* __restrict__ gf, float* __restrict__ gr) {
+  __shared__ GroupTable<EXT> s_tab[kWaves];
   const int lane = threadIdx.x & 63;
-  GroupTable& H = s_tab[threadIdx.x >> 6];
+  GroupTable<EXT>& H = s_tab[threadIdx.x >> 6];
   for (int s = lane; s < kGrpSlots; s += 64) {
     H.key[s] = kGrpEmpty;
     H.n[s] = 0;
     H.p[s] = 0;
     H.c[s] = 0;
     H.q[s] = 0;
+    if (EXT) H.r[s] = 0;
   }
   wave_lds_sync();
   const int64_t waves = (int64_t)gridDim.x * kWaves;
@@ -189,17 +211,19 @@ __global__ __launch_bounds__(kWG) void k_group_build(
       if (WRITE && bo0 >= r0 && lane == 0) gofs[b] = out;
       const int64_t lo = max(bo0, r0), hi = min(bo1, r1);
       int32_t taken = 0;
-      uint64_t sp = 0, scz = 0, sq = 0;
+      uint64_t sp = 0, scz = 0, sq = 0, sr = 0;
       for (int64_t base = lo; base < hi; base += 64) {
         const int64_t i = base + lane;
         bool fresh = false;
         if (i < hi) {
           const uint32_t pi = (uint32_t)p[i], ci = (uint32_t)c[i], ti = (uint32_t)tenant[i];
           const uint64_t pp = (uint64_t)pi * pi;
+          const uint64_t pc = (uint64_t)pi * ci;
           if (!WRITE) {
             sp += pi;
             scz += (uint64_t)ci + (ci == 0 ? kZeroUnit : 0ull);
             sq += pp;
+            if (EXT) sr += pc;
           }
           uint32_t h = grp_hash(ti);
           while (true) {  // ends: fewer than kGrpSlots keys are ever held
@@ -216,6 +240,7 @@ __global__ __launch_bounds__(kWG) void k_group_build(
             atomicAdd(&H.p[h], (unsigned long long)pi);
             atomicAdd(&H.c[h], (unsigned long long)ci);
             atomicAdd(&H.q[h], (unsigned long long)pp);
+            if (EXT) atomicAdd(&H.r[h], (unsigned long long)pc);
           }
         }
         taken += __builtin_popcountll(__ballot(fresh));
@@ -233,6 +258,10 @@ __global__ __launch_bounds__(kWG) void k_group_build(
                 const int64_t at = out + __builtin_popcountll(m & ((1ull << lane) - 1ull));
                 gw[at] = (((uint32_t)b & kGrpBatchMask) << kGrpTenantBits) | key;
                 gf[at] = (v4f){(float)H.n[s], (float)H.p[s], (float)H.c[s], (float)H.q[s]};
+                if (EXT) {
+                  gr[at] = (float)H.r[s];
+                  H.r[s] = 0;
+                }
                 H.n[s] = 0;
                 H.p[s] = 0;
                 H.c[s] = 0;
@@ -250,15 +279,18 @@ __global__ __launch_bounds__(kWG) void k_group_build(
         sp = wave_sum(sp);
         scz = wave_sum(scz);
         sq = wave_sum(sq);
+        if (EXT) sr = wave_sum(sr);
         if (lane == 0) {
           if (bo0 >= r0 && bo1 <= r1) {  // the whole batch
             bsum[b] = sp;
             bsum[nB + b] = scz;
             bsum[2 * nB + b] = sq;
+            if (EXT) bsum[3 * nB + b] = sr;
           } else {
             atomicAdd(&bsum[b], (unsigned long long)sp);
             atomicAdd(&bsum[nB + b], (unsigned long long)scz);
             atomicAdd(&bsum[2 * nB + b], (unsigned long long)sq);
+            if (EXT) atomicAdd(&bsum[3 * nB + b], (unsigned long long)sr);
           }
         }
       }
@@ -354,15 +386,19 @@ __global__ __launch_bounds__(kScanWG) void k_scan_apply(const int64_t* __restric
 
 constexpr int kGV = 16;                    // group slots per lane of a sweep tile
 constexpr int kGT = 64 * kGV;              // group slots per sweep tile
-constexpr int kGB = 28;                    // batches per sweep tile
-static_assert(kGV % 4 == 0 && kGB < 64, "sweep tile shape");
+// batches per sweep tile: the per-wave constant tables of 8 settings then
+// leave room for two workgroups per CU beside 8 histograms of 1040 entries
+template <int NC> constexpr int kGBof = NC == 5 ? 28 : 22;
+static_assert(kGV % 4 == 0 && kGBof<5> < 64 && kGBof<7> < 64, "sweep tile shape");
 
 struct GroupSweep {
   const int64_t* off;               // request offsets [nB + 1]
   const int64_t* gofs;              // group offsets [nB + 1]
-  const unsigned long long* bsum;   // [3][nB]: sum p, sum c | zero count << 48, sum p^2
+  const unsigned long long* bsum;   // [3][nB]: sum p, sum c | zero count << 48, sum p^2;
+                                    // [4][nB] with sum p*c (extended model)
   const uint32_t* gw;               // [groups + kGT] ((b mod 2^20) << 12) | tenant
   const v4f* gf;                    // [groups + kGT] (n, P, C, Q)
+  const float* gr;                  // [groups + kGT] R = sum p*c (extended model)
   int64_t nB;
   const int64_t* wg_first;          // chunk table over batches (k_partition)
   unsigned long long* claims;
@@ -373,23 +409,30 @@ struct GroupSweep {
   const int32_t* hot;               // [kHot]
 };
 
-// NV: histogram rows, i.e. settings per pass, >= V.n.  Work: the chunks of
-// k_tiles (one static chunk per wave, then claimed ones).  LDS per workgroup:
-// NV * (n_tenants + kHotSlots) doubles (dynamic) plus the per-wave tables.
-template <int NV>
-__global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const VarTable V) {
+// NV: histogram rows, i.e. settings per pass, >= V.n; NC: 5 (Eq. 1) or 7
+// (the extended model).  Work: the chunks of k_tiles (one static chunk per
+// wave, then claimed ones).  LDS per workgroup: NV * (n_tenants + kHotSlots)
+// doubles (dynamic) plus the per-wave tables.
+template <int NV, int NC>
+__global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const VarTableOf<NC> V) {
+  constexpr bool EXT = NC == 7;
+  constexpr int kGB = kGBof<NC>;
+  constexpr int KC = EXT ? 4 : 3;                    // batch-independent constants
   extern __shared__ double s_hist[];                 // [NV][n_tenants + kHotSlots]
   __shared__ v4f s_kt[kWaves][NV][kGB];              // per wave: (k0, k1, k2, k3)
-  __shared__ float s_K[NV * 4 * 3];                  // [setting][regime][k1..k3]
+  __shared__ float s_kt5[kWaves][EXT ? NV : 1][EXT ? kGB : 1];  // per wave: k5
+  __shared__ float s_K[NV * 4 * KC];                 // [setting][regime][k1..k3 (, k5)]
   const int tid = threadIdx.x, lane = tid & 63;
   // [setting][batch of the tile]: lanes of one read that hold different
   // batches fall in different banks
   v4f(*kt)[kGB] = s_kt[tid >> 6];
+  float(*kt5)[EXT ? kGB : 1] = s_kt5[tid >> 6];
   const int32_t T = P.n_tenants, TS = T + kHotSlots;
   int32_t hot[kHot];
 #pragma unroll
   for (int h = 0; h < kHot; ++h) hot[h] = uni(P.hot[h]);
-  for (int i = tid; i < NV * 12; i += kWG) s_K[i] = V.K[i / 12][(i / 3) % 4][i % 3];
+  for (int i = tid; i < NV * 4 * KC; i += kWG)
+    s_K[i] = V.K[i / (4 * KC)][(i / KC) % 4][i % KC];
   for (int u = tid; u < NV * TS; u += kWG) s_hist[u] = 0.0;
   __syncthreads();
 
@@ -420,16 +463,18 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
         const int64_t n = P.off[bb + 1] - P.off[bb];
         if (n > 0) {
           const uint64_t sp = P.bsum[bb], scz = P.bsum[P.nB + bb], sq = P.bsum[2 * P.nB + bb];
+          const uint64_t sr = EXT ? P.bsum[3 * P.nB + bb] : 0;
           // decode iff every request processes one token over a nonzero context
           const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
           float k0[kSweepG];
-          const uint32_t sg = sweep_batch<NV>(V, n, sp, scz & kCMask, sq, prefill, k0);
+          const uint32_t sg = sweep_batch<NV, NC>(V, n, sp, scz & kCMask, sq, sr, prefill, k0);
           const int ph = prefill ? 0 : 1;
 #pragma unroll
           for (int g = 0; g < NV; ++g) {
             const int r = 2 * ph + (int)((sg >> g) & 1u);
-            const float* kr = &s_K[(g * 4 + r) * 3];
+            const float* kr = &s_K[(g * 4 + r) * KC];
             kt[g][lane] = (v4f){k0[g], kr[0], kr[1], kr[2]};
+            if (EXT) kt5[g][lane] = kr[KC - 1];
           }
         }
       }
@@ -441,6 +486,7 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
         const int64_t x = base + (int64_t)lane * kGV;
         uint32_t wv[kGV];
         v4f fv[kGV];
+        float rv[EXT ? kGV : 1];
         // (x is a multiple of 4; the group arrays hold kGT slots past the last group)
 #pragma unroll
         for (int v = 0; v < kGV / 4; ++v) {
@@ -452,8 +498,19 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
         }
 #pragma unroll
         for (int q = 0; q < kGV; ++q) fv[q] = P.gf[x + q];
+        if constexpr (EXT) {
+#pragma unroll
+          for (int v = 0; v < kGV / 4; ++v) {
+            const v4f a = *(const v4f*)(P.gr + x + 4 * v);
+            rv[4 * v] = a.x;
+            rv[4 * v + 1] = a.y;
+            rv[4 * v + 2] = a.z;
+            rv[4 * v + 3] = a.w;
+          }
+        }
         uint32_t kcur = 0xffffffffu;
         v4f K[NV];
+        float K5[EXT ? NV : 1];
 #pragma unroll
         for (int q = 0; q < kGV; ++q) {
           if (x + q >= g0 && x + q < g1) {
@@ -467,14 +524,19 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
             if (lb != kcur) {
               kcur = lb;
 #pragma unroll
-              for (int g = 0; g < NV; ++g) K[g] = kt[g][lb];
+              for (int g = 0; g < NV; ++g) {
+                K[g] = kt[g][lb];
+                if (EXT) K5[g] = kt5[g][lb];
+              }
             }
             const v4f f = fv[q];
             // all NV rows: rows past V.n are scratch, never flushed
 #pragma unroll
-            for (int g = 0; g < NV; ++g)
-              atomicAdd(s_hist + g * TS + e,
-                        (double)fmaf(K[g].w, f.w, fmaf(K[g].z, f.z, fmaf(K[g].y, f.y, K[g].x * f.x))));
+            for (int g = 0; g < NV; ++g) {
+              float t = fmaf(K[g].w, f.w, fmaf(K[g].z, f.z, fmaf(K[g].y, f.y, K[g].x * f.x)));
+              if constexpr (EXT) t = fmaf(K5[g], rv[q], t);
+              atomicAdd(s_hist + g * TS + e, (double)t);
+            }
           }
         }
       }

@@ -25,7 +25,8 @@ LLMV_BATCH_MAX = 1 << 22
 LLMV_TENANTS_MAX = 1 << 24
 
 EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_sweep_workspace_size",
-           "llmv_attribute", "llmv_attribute_sweep", "llmv_features", "llmv_tenant_sums", "llmv_validate",
+           "llmv_sweep_workspace_size_ext", "llmv_attribute", "llmv_attribute_sweep",
+           "llmv_attribute_sweep_ext", "llmv_features", "llmv_tenant_sums", "llmv_validate",
            "llmv_batch_sums", "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit_workspace_size", "llmv_fit",
            "llmv_fit_metrics", "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
            "llmv_attribute_ext",
@@ -69,8 +70,11 @@ def load(path: str = LIB_PATH):
             lib.llmv_workspace_size.restype = sz
             lib.llmv_sweep_workspace_size.argtypes = [i64, i64, i32]
             lib.llmv_sweep_workspace_size.restype = sz
+            lib.llmv_sweep_workspace_size_ext.argtypes = [i64, i64, i32]
+            lib.llmv_sweep_workspace_size_ext.restype = sz
             lib.llmv_attribute.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
             lib.llmv_attribute_sweep.argtypes = [P, P, i32, P, i32, i32, P, P, sz, P]
+            lib.llmv_attribute_sweep_ext.argtypes = [P, P, i32, P, i32, i32, P, P, sz, P]
             lib.llmv_features.argtypes = [P, P, P, P, P, sz, P]
             lib.llmv_tenant_sums.argtypes = [P, P, i64, i32, P, P, sz, P]
             lib.llmv_batch_sums.argtypes = [P, P, P, P, sz, P]
@@ -91,6 +95,7 @@ def load(path: str = LIB_PATH):
             lib.llmv_set_kernel_events.argtypes = [P, P]
             lib.llmv_set_kernel_events.restype = ctypes.c_int
             for f in ("llmv_shape_constants", "llmv_attribute", "llmv_attribute_sweep",
+                      "llmv_attribute_sweep_ext",
                       "llmv_features", "llmv_tenant_sums", "llmv_validate", "llmv_batch_sums",
                       "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit",
                       "llmv_fit_metrics",
@@ -172,6 +177,10 @@ def llmv_sweep_workspace_size(n_batches: int, n_requests: int, n_tenants: int) -
     return int(load().llmv_sweep_workspace_size(n_batches, n_requests, n_tenants))
 
 
+def llmv_sweep_workspace_size_ext(n_batches: int, n_requests: int, n_tenants: int) -> int:
+    return int(load().llmv_sweep_workspace_size_ext(n_batches, n_requests, n_tenants))
+
+
 def llmv_attribute(trace: DeviceTrace, shape, coeffs, latency=None, regime=None, share=None,
                    n_tenants: int = 0, tenant_sums=None, ws=None, stream=None):
     co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
@@ -184,11 +193,12 @@ def llmv_attribute(trace: DeviceTrace, shape, coeffs, latency=None, regime=None,
 
 
 def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out, ws=None,
-                         stream=None):
+                         stream=None, ext: bool = False):
     """shapes: list of shape dicts (or [None] for the unit shape); coeffs:
-    array-like [n_coeffs, 20]; out: device fp64 [n_shapes, n_coeffs, n_tenants]."""
+    array-like [n_coeffs, 20] ([n_coeffs, 28] with ext: llmv_attribute_sweep_ext);
+    out: device fp64 [n_shapes, n_coeffs, n_tenants]."""
     import numpy as np
-    co = np.ascontiguousarray(coeffs, dtype=np.float32).reshape(-1, 20)
+    co = np.ascontiguousarray(coeffs, dtype=np.float32).reshape(-1, 28 if ext else 20)
     if shapes == [None] or shapes is None:
         arr, n_sh = None, 1
     else:
@@ -196,10 +206,16 @@ def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out
         n_sh = len(shapes)
     tr = trace.struct(with_tenant=True)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(load().llmv_attribute_sweep(
+    name = "llmv_attribute_sweep_ext" if ext else "llmv_attribute_sweep"
+    _check(getattr(load(), name)(
         ctypes.byref(tr), None if arr is None else ctypes.cast(arr, ctypes.c_void_p), n_sh,
         co.ctypes.data_as(ctypes.c_void_p), co.shape[0], int(n_tenants), _ptr(out), _ptr(ws),
-        nbytes, _stream(stream)), "llmv_attribute_sweep")
+        nbytes, _stream(stream)), name)
+
+
+def llmv_attribute_sweep_ext(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out, ws=None,
+                             stream=None):
+    llmv_attribute_sweep(trace, shapes, coeffs, n_tenants, out, ws, stream, ext=True)
 
 
 def llmv_batch_sums_ext(trace: DeviceTrace, sums=None, phase=None, ws=None, stream=None):
@@ -361,9 +377,11 @@ def workspace(n_batches: int, n_requests: int, n_tenants: int, device="cuda"):
     return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
 
 
-def sweep_workspace(n_batches: int, n_requests: int, n_tenants: int, device="cuda"):
-    """A device workspace tensor of llmv_sweep_workspace_size bytes."""
-    n = llmv_sweep_workspace_size(n_batches, n_requests, n_tenants)
+def sweep_workspace(n_batches: int, n_requests: int, n_tenants: int, device="cuda",
+                    ext: bool = False):
+    """A device workspace tensor of llmv_sweep_workspace_size(_ext) bytes."""
+    size = llmv_sweep_workspace_size_ext if ext else llmv_sweep_workspace_size
+    n = size(n_batches, n_requests, n_tenants)
     return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
 
 
@@ -387,16 +405,18 @@ def attribute(trace: DeviceTrace, shape, coeffs, n_tenants: int = 0,
     return out
 
 
-def attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, ws=None):
-    """Allocates out [n_shapes, n_coeffs, n_tenants] and runs the sweep."""
+def attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, ws=None,
+                    ext: bool = False):
+    """Allocates out [n_shapes, n_coeffs, n_tenants] and runs the sweep (under
+    the extended model with ext, coeffs [n_coeffs, 28])."""
     import numpy as np
     n_sh = 1 if shapes is None else len(shapes)
-    n_co = int(np.asarray(coeffs).reshape(-1, 20).shape[0])
+    n_co = int(np.asarray(coeffs).reshape(-1, 28 if ext else 20).shape[0])
     out = torch.empty((n_sh, n_co, n_tenants), dtype=torch.float64, device=trace.p.device)
     if ws is None:
-        ws = sweep_workspace(trace.n_batches, trace.n_requests, n_tenants, trace.p.device)
+        ws = sweep_workspace(trace.n_batches, trace.n_requests, n_tenants, trace.p.device, ext)
     llmv_attribute_sweep(trace, shapes if shapes is not None else [None], coeffs, n_tenants,
-                         out, ws)
+                         out, ws, ext=ext)
     return out
 
 

@@ -134,6 +134,18 @@ def test_host_argument_errors(llmv):
     co[25] = float("nan")
     assert sw(ctypes.byref(tr), None, 1, co, 2, 4, FAKE, None, 0, None) == E
     assert sw(ctypes.byref(_trace(llmv, t=0)), None, 1, co, 2, 4, FAKE, None, 0, None) == E
+    # the extended sweep: the same checks, 28 coefficients per set
+    cx = (ctypes.c_float * 56)(*([1.0] * 56))
+    sx = lib.llmv_attribute_sweep_ext
+    assert sx(ctypes.byref(tr), None, 2, cx, 2, 4, FAKE, None, 0, None) == E
+    assert sx(ctypes.byref(tr), None, 1, cx, 0, 4, FAKE, None, 0, None) == E
+    assert sx(ctypes.byref(tr), None, 1, None, 2, 4, FAKE, None, 0, None) == E
+    assert sx(ctypes.byref(tr), None, 1, cx, 2, 4097, FAKE, None, 0, None) == E
+    assert sx(ctypes.byref(tr), None, 1, cx, 2, 4, None, None, 0, None) == E
+    cx[55] = float("inf")  # the last coefficient of the second set
+    assert sx(ctypes.byref(tr), None, 1, cx, 2, 4, FAKE, None, 0, None) == E
+    assert "coeffs[55]" in lib.llmv_last_error().decode()
+    assert sx(ctypes.byref(_trace(llmv, t=0)), None, 1, cx, 2, 4, FAKE, None, 0, None) == E
 
 
 def test_batch_sums_and_admit_argument_errors(llmv):
@@ -259,6 +271,19 @@ def test_sweep_workspace_size(llmv):
     assert 32 << 16 <= db <= (32 << 16) + 3 * 256
     assert lib.llmv_sweep_workspace_size(0, 0, 1) > 0
     assert lib.llmv_sweep_workspace_size(-5, -5, -5) == lib.llmv_sweep_workspace_size(0, 0, 0)
+
+
+def test_sweep_workspace_size_ext(llmv):
+    """The extended sweep's workspace: the Eq. 1 sweep's plus the groups'
+    sums of p*c (4 bytes per request) and a fourth exact batch sum (8 bytes
+    per batch)."""
+    lib = llmv.load()
+    nB, N, T = 10_000, 1 << 24, 1024
+    for n_b, n in ((nB, N), (nB + (1 << 16), N), (nB, N + (1 << 20))):
+        d = lib.llmv_sweep_workspace_size_ext(n_b, n, T) - lib.llmv_sweep_workspace_size(n_b, n, T)
+        assert 4 * n + 8 * n_b <= d <= 4 * n + 8 * n_b + 4 * 1024 + 2 * 256, (n_b, n, d)
+    assert lib.llmv_sweep_workspace_size_ext(-5, -5, -5) == \
+        lib.llmv_sweep_workspace_size_ext(0, 0, 0) > 0
 
 
 def test_python_binding_refuses_without_library(tmp_path):
