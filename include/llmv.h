@@ -162,8 +162,9 @@ int llmv_shape_constants_ext(const llmv_shape *shape, double S[6]);
  *           (phase*2 + segment)*7 + k, k = (beta, a1, a2, a3, a4, a5, a6).
  * Other arguments, outputs, precision and workspace as llmv_attribute.  The
  * batch sum of p_i*c_i is exact in uint64 and must stay below 2^63 (not
- * checked).  With a5 = a6 = 0 in every set the results are bit-identical
- * to llmv_attribute with the first five coefficients of each set. */
+ * checked).  With a5 = a6 = 0 in every set, latency, regime and shares are
+ * bit-identical to llmv_attribute's with the first five coefficients of each
+ * set, and tenant sums equal up to the order of their fp64 additions. */
 int llmv_attribute_ext(const llmv_trace *trace, const llmv_shape *shape,
                        const float coeffs[28], float *latency, uint8_t *regime,
                        float *share, int32_t n_tenants, double *tenant_sums,
