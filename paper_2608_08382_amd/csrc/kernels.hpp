@@ -40,7 +40,7 @@ constexpr int kVec = LLMV_LANE_SLOTS;        // consecutive requests held per la
 constexpr int kCap = 64 * kVec;              // request slots per wave tile
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 1024;                   // persistent workgroups, upper bound (256 CUs x 4)
-constexpr int kTenantChunk = 64;                 // tenants per k_tenant_reduce block
+constexpr int kTenantChunk = 16;                 // tenants per k_tenant_reduce block
 #ifndef LLMV_STATIC_EIGHTHS
 #define LLMV_STATIC_EIGHTHS 6
 #endif
@@ -983,35 +983,47 @@ __global__ void k_zero_u64(unsigned long long* __restrict__ x, int64_t n) {
 // ------------------------------------------------------ tenant reductions
 
 // out[u] = sum over rows w of part[w][u], folded in a fixed order.  One
-// block of kReduceWaves waves per 64 tenants: wave v sums rows v, v +
-// kReduceWaves, ... with eight independent partial sums (eight loads in
-// flight per lane), then the waves' sums are added in wave order.
+// block of kReduceWaves waves per kTenantChunk tenants; lane l of a wave
+// takes tenant l % kTenantChunk and row offset l / kTenantChunk, so one load
+// instruction reads kReduceRows rows of 128 contiguous bytes.  Wave v sums
+// rows v*kReduceRows + l / kTenantChunk + k*kReduceStep (k = 0, 1, ...) into
+// eight independent partial sums (up to 8*kReduceStep rows in one round of
+// loads); the row offsets are then added by lane shuffles and the waves'
+// sums in wave order.
 constexpr int kReduceWaves = 16;
+constexpr int kReduceRows = 64 / kTenantChunk;                 // rows per wave load
+constexpr int kReduceStep = kReduceWaves * kReduceRows;        // rows per block load
+static_assert(64 % kTenantChunk == 0 && kTenantChunk * 8 == 128, "128-byte row segments");
 
 __global__ __launch_bounds__(64 * kReduceWaves) void k_tenant_reduce(
     const double* __restrict__ part, int rows, int T, double* __restrict__ out) {
   __shared__ double red[kReduceWaves][kTenantChunk];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int u = blockIdx.x * kTenantChunk + lane;
+  const int j = lane % kTenantChunk, rs = lane / kTenantChunk;
+  const int u = blockIdx.x * kTenantChunk + j;
   double acc = 0.0;
   if (u < T) {
     double a8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    int w = wave;
-    for (; w + 7 * kReduceWaves < rows; w += 8 * kReduceWaves) {
+    int w = wave * kReduceRows + rs;
+    for (; w + 7 * kReduceStep < rows; w += 8 * kReduceStep) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) a8[i] += part[(int64_t)(w + i * kReduceWaves) * T + u];
+      for (int i = 0; i < 8; ++i) a8[i] += part[(int64_t)(w + i * kReduceStep) * T + u];
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      if (w + i * kReduceWaves < rows) a8[i] += part[(int64_t)(w + i * kReduceWaves) * T + u];
+      if (w + i * kReduceStep < rows) a8[i] += part[(int64_t)(w + i * kReduceStep) * T + u];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc += a8[i];
   }
-  red[wave][lane] = acc;
+  // the row offsets of one tenant: lanes j, j + 16, j + 32, j + 48
+  static_assert(kReduceRows == 4, "two shuffle steps");
+  acc += __shfl_xor(acc, 16, 64);
+  acc += __shfl_xor(acc, 32, 64);
+  if (rs == 0) red[wave][j] = acc;
   __syncthreads();
-  if (wave == 0 && u < T) {
-    double t = red[0][lane];
-    for (int v = 1; v < kReduceWaves; ++v) t += red[v][lane];
+  if (wave == 0 && rs == 0 && u < T) {
+    double t = red[0][j];
+    for (int v = 1; v < kReduceWaves; ++v) t += red[v][j];
     out[u] = t;
   }
 }
