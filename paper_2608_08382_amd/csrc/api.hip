@@ -22,10 +22,10 @@ thread_local hipEvent_t g_ev_before = nullptr;  // measurement hook
 thread_local hipEvent_t g_ev_after = nullptr;
 
 // Upper bound of the persistent grid for n requests (sizes the workspace):
-// no more than one workgroup per kWaves wave tiles of requests, at most
-// kMaxGrid.
+// no more than one workgroup per kWaves (narrow) wave tiles of requests, at
+// most kMaxGrid.
 int64_t grid_max_for(int64_t n) {
-  const int64_t per = (int64_t)kCap * kWaves;
+  const int64_t per = (int64_t)kCapNarrow * kWaves;
   const int64_t by_work = (n + per - 1) / per;
   return by_work < 1 ? 1 : (by_work > kMaxGrid ? kMaxGrid : by_work);
 }
@@ -49,10 +49,10 @@ int64_t grid_for(int64_t n, int cus, int per_cu) {
 
 bool lds_hist(int32_t T) { return T > 0 && T <= kHistLdsMax; }
 
-// Traces up to this many requests run as one workgroup in one launch: two
-// wave tiles per wave at most, so a longer serial walk never costs more than
-// the launches it saves.
-constexpr int64_t kSmallN = 2 * (int64_t)kCap * kWaves;
+// Traces up to this many requests run as one workgroup in one launch (wave
+// tiles of `cap` slots): two wave tiles per wave at most, so a longer serial
+// walk never costs more than the launches it saves.
+constexpr int64_t small_n(int64_t cap) { return 2 * cap * kWaves; }
 
 // Replicas of the attribution path's LDS tenant histogram: 4, 2 or 1, within
 // 32 KiB (two workgroups per CU keep fitting).
@@ -86,19 +86,21 @@ struct Layout {
   size_t wg_first, claims, partials, counts, hot, flag, total;
 };
 
-// Chunks for `workers` wave workers over n requests.  When a worker's share
-// is at least kMinDynShare requests: kStaticEighths/8 of the requests in
-// static chunks, the rest in up to kDynPerWorker claimed chunks per worker of
-// at least kMinChunk requests.  The static part is one chunk per worker, or
-// with `pieces` chunks of kPiece requests dealt round-robin (neighbouring
+// Chunks for `workers` wave workers over n requests, for wave tiles of `cap`
+// slots.  When a worker's share is at least min_dyn_share(cap) requests:
+// kStaticEighths/8 of the requests in static chunks, the rest in up to
+// kDynPerWorker claimed chunks per worker of at least min_chunk(cap)
+// requests.  The static part is one chunk per worker, or with `pieces`
+// chunks of piece(cap) requests dealt round-robin (neighbouring
 // waves then stream neighbouring memory).  Otherwise one static chunk per
 // worker and no claims (a claim is a device-wide atomic on one counter;
 // thousands of them cost more than a short launch can win back).
-ChunkMap chunk_map(int64_t n, int64_t workers, bool pieces) {
+ChunkMap chunk_map(int64_t n, int64_t workers, bool pieces, int64_t cap) {
+  const int64_t kPiece = piece(cap), kMinChunk = min_chunk(cap);
   ChunkMap m{};
   m.n_static = workers;
   m.s2 = 1;
-  if (n / workers < kMinDynShare) {
+  if (n / workers < min_dyn_share(cap)) {
     m.s1 = (n + workers - 1) / workers;
     if (m.s1 < 1) m.s1 = 1;
     m.F = m.s1 * workers;
@@ -130,7 +132,8 @@ Layout layout(int64_t n, int32_t T, int rows = 1) {
   size_t o = 0;
   const int64_t grid = grid_max_for(n);
   L.wg_first = o;  // first batch of each chunk (chunk_map's n_chunks + 1 at most)
-  o += align_up((size_t)(n / kPiece + grid * kWaves * (1 + kDynPerWorker) + 1) * sizeof(int64_t));
+  o += align_up((size_t)(n / piece(kCapNarrow) + grid * kWaves * (1 + kDynPerWorker) + 1) *
+                sizeof(int64_t));
   L.claims = o;
   o += align_up(sizeof(unsigned long long));
   L.partials = o;  // [grid][rows][T]
@@ -252,7 +255,8 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   const auto kern = TilePick<VT>::get(mode, hist, want_share);
   P.hist_rep = rep;
 
-  if (tr->n_requests <= kSmallN && hist != HIST_GLOBAL) {
+  const int64_t cap = tile_cap(mode, hist);
+  if (tr->n_requests <= small_n(cap) && hist != HIST_GLOBAL) {
     // A small trace (one scheduler step, say) in one launch: one workgroup,
     // its waves split the batches by count (no chunk table), and the
     // workgroup's tenant histogram is the result (no reduction).
@@ -274,7 +278,7 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   const int n_chunks = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
-  const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves, true);
+  const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves, true, cap);
   P.wg_first = wg_first;
   P.split_by_count = 0;
   P.claims = (unsigned long long*)(base + L.claims);
@@ -475,7 +479,7 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   // the passes: the chunks of k_tiles over the batches; every launch takes
   // exactly n_chunks claims (one per chunk it runs, the static ones
   // included), so launch i starts at claim i * n_chunks
-  const ChunkMap cm = chunk_map(N, grid * kWaves, false);  // one static chunk per wave
+  const ChunkMap cm = chunk_map(N, grid * kWaves, false, kCapNarrow);  // one static chunk per wave
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   rc = partition(trace, cm, wg_first, claims, st);
   if (rc) return rc;

@@ -13,7 +13,7 @@
 //    self-scheduling, so no wave waits on a slower one at the end).
 //  * k_tiles: persistent workgroups of four independent wave workers.  A wave
 //    walks each of its chunks in wave tiles: runs of whole batches whose
-//    requests fit in kCap slots (lane l holds kVec consecutive requests), so every request is
+//    requests fit in 64*kVec slots (lane l holds kVec consecutive requests), so every request is
 //    read from HBM once, held in registers while its batch totals are formed,
 //    and its share written once.  Batch totals are lane-local run sums added
 //    into per-batch LDS accumulators; batch membership comes from an LDS
@@ -33,11 +33,11 @@ namespace llmv {
 
 constexpr int kWG = 256;                     // threads per workgroup
 constexpr int kWaves = kWG / 64;             // wave64
-#ifndef LLMV_LANE_SLOTS
-#define LLMV_LANE_SLOTS 24
-#endif
-constexpr int kVec = LLMV_LANE_SLOTS;        // consecutive requests held per lane
-constexpr int kCap = 64 * kVec;              // request slots per wave tile
+// Consecutive requests held per lane (a tile kernel instance takes one of
+// the two: kVecOf below); a wave tile holds 64 times as many.
+constexpr int kVecNarrow = 24;
+constexpr int kVecWide = 28;
+constexpr int kCapNarrow = 64 * kVecNarrow;  // request slots per narrow wave tile
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 1024;                   // persistent workgroups, upper bound (256 CUs x 4)
 constexpr int kTenantChunk = 16;                 // tenants per k_tenant_reduce block
@@ -49,9 +49,10 @@ constexpr int kTenantChunk = 16;                 // tenants per k_tenant_reduce 
 #endif
 constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;  // requests in static chunks, in eighths
 constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave worker, at most
-constexpr int64_t kMinChunk = 4 * kCap;              // requests per claimed chunk, at least
-constexpr int64_t kMinDynShare = 32 * kCap;          // requests per worker for claimed chunks
-constexpr int64_t kPiece = 16 * kCap;                // requests per static piece (tile kernel)
+// For wave tiles of `cap` request slots:
+constexpr int64_t min_chunk(int64_t cap) { return 4 * cap; }       // requests per claimed chunk, at least
+constexpr int64_t min_dyn_share(int64_t cap) { return 32 * cap; }  // per worker, for claimed chunks
+constexpr int64_t piece(int64_t cap) { return 16 * cap; }          // requests per static piece
 
 // Chunks of the tile kernel's work.  Chunk w < n_static (static) starts at
 // request w*s1; chunk n_static + j (claimed) starts at request F + j*s2,
@@ -82,6 +83,16 @@ template <int MODE> constexpr bool kAttrMode = MODE == MODE_ATTR || MODE == MODE
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 enum { HIST_NONE = 0, HIST_LDS = 1, HIST_GLOBAL = 2 };
+
+// Lane slots of a tile kernel instance: the wide tile where it is faster
+// (Eq. 1 attribution without the tenant cache: 28 slots, about 2% on the
+// heavy-tailed trace); elsewhere the narrow one, where the wide tile's
+// registers (up to 255 VGPRs) cost more than its longer tiles gain.
+template <int MODE, int HIST>
+constexpr int kVecOf = (MODE == MODE_ATTR && HIST != HIST_GLOBAL) ? kVecWide : kVecNarrow;
+__host__ __device__ constexpr int64_t tile_cap(int mode, int hist) {
+  return 64 * ((mode == MODE_ATTR && hist != HIST_GLOBAL) ? kVecWide : kVecNarrow);
+}
 
 struct Params {
   const int64_t* off;
@@ -422,11 +433,29 @@ __global__ void k_zero_f64(double* __restrict__ x, int64_t n) {
 // kVec-1.
 
 constexpr int kRounds = 1;
-constexpr int kRoundSlots = 64 * kVec;
-constexpr int kTile = kRounds * kRoundSlots;    // request slots per wave tile
-constexpr int kTileMaskWords = kTile / 32;      // batch-start bitmask words
 constexpr int kTileBatches = 63;                // batches per wave tile (64 offsets)
-constexpr int kStagePitch = kVec + 4;           // padded lane pitch of the share stage
+
+// The wave tile of VEC slots per lane.
+template <int VEC>
+struct TileShape {
+  static_assert(VEC % 4 == 0 && VEC <= 28, "lane slots: multiple of 4, bits fit a word pair");
+  static constexpr int kRoundSlots = 64 * VEC;
+  static constexpr int kTile = kRounds * kRoundSlots;  // request slots per wave tile
+  static constexpr int kTileMaskWords = kTile / 32;    // batch-start bitmask words
+  // Lane pitch of the share stage, in floats: an odd number of 16-byte
+  // units, so that the 16-byte stage writes of 16 consecutive lanes fall in
+  // distinct groups of four of the 64 LDS banks (28 needs no padding; 24 is
+  // padded to 28).
+  static constexpr int kStagePitch = (VEC / 4) % 2 ? VEC : VEC + 4;
+};
+// The tile constants of VEC as local names.
+#define LLMV_TILE_CONSTANTS(VEC)                                          \
+  constexpr int kVec = (VEC);                                             \
+  constexpr int kRoundSlots = TileShape<(VEC)>::kRoundSlots;              \
+  constexpr int kTile = TileShape<(VEC)>::kTile;                          \
+  constexpr int kTileMaskWords = TileShape<(VEC)>::kTileMaskWords;        \
+  constexpr int kStagePitch = TileShape<(VEC)>::kStagePitch;              \
+  (void)kVec; (void)kRoundSlots; (void)kTile; (void)kTileMaskWords; (void)kStagePitch
 
 constexpr uint64_t kZeroUnit = 1ull << 48;      // count of c == 0, above the c sum
 constexpr uint64_t kCMask = kZeroUnit - 1;
@@ -438,11 +467,11 @@ struct BatchAcc {
 };
 
 // LDS private to one wave.
+template <int VEC>
 struct WaveLds {
-  uint32_t mask[kTileMaskWords + 2];  // bit x: a nonempty batch starts at slot x
+  uint32_t mask[TileShape<VEC>::kTileMaskWords + 2];  // bit x: a nonempty batch starts at slot x
   BatchAcc acc[kTileBatches];         // per nonempty batch of the tile
   double k[kTileBatches][4];          // per nonempty batch: share / feature constants
-  static_assert(kVec % 4 == 0 && kVec <= 28, "lane slots: multiple of 4, bits fit a word pair");
 };
 
 // Orders LDS accesses between the lanes of one wave (a wave's LDS accesses
@@ -482,9 +511,10 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
 
 // Loads slots x .. x+kVec-1 (x a multiple of 4, x >= 0) of p, c (and
 // tenant); slots at or past N read as 0.
-template <bool TENANT>
+template <int VEC, bool TENANT>
 __device__ __forceinline__ void load_slots(const Params& P, int64_t x, int32_t* pv, int32_t* cv,
                                        int32_t* tv) {
+  LLMV_TILE_CONSTANTS(VEC);
   if (x + kVec <= P.N) {
 #pragma unroll
     for (int g = 0; g < kVec / 4; ++g) {
@@ -512,8 +542,10 @@ __device__ __forceinline__ void load_slots(const Params& P, int64_t x, int32_t* 
 // (lane l: slots s0 + kVec*l .. s0 + kVec*l + kVec-1, pitch kStagePitch) so
 // that every global store instruction writes 1 KB of consecutive shares.
 // Only slots in [xf, L) are written.
+template <int VEC>
 __device__ __forceinline__ void store_round(const Params& P, float* stage, int64_t ra, int32_t s0,
                                             int32_t xf, int32_t L) {
+  LLMV_TILE_CONSTANTS(VEC);
   const int lane = threadIdx.x & 63;
   wave_lds_sync();
 #pragma unroll
@@ -535,16 +567,18 @@ __device__ __forceinline__ void store_round(const Params& P, float* stage, int64
 // One batch too large for a wave tile: two passes over its requests by the
 // whole wave (the second pass mostly hits in L2).
 template <int MODE, int HIST, bool SHARE>
-__device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V, WaveLds& W,
-                          double* wk4, float* stage, int64_t bg, int64_t rs, int64_t re,
-                          double* s_hist) {
+__device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
+                          WaveLds<kVecOf<MODE, HIST>>& W, double* wk4, float* stage, int64_t bg,
+                          int64_t rs, int64_t re, double* s_hist) {
+  constexpr int VEC = kVecOf<MODE, HIST>;
+  LLMV_TILE_CONSTANTS(VEC);
   const int lane = threadIdx.x & 63;
   const int64_t ra = rs & ~(int64_t)3;
   uint64_t sp = 0, scz = 0, sq = 0, sr = 0;
   int32_t pv[kVec], cv[kVec], tv[kVec];
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
-    load_slots<false>(P, x, pv, cv, tv);
+    load_slots<VEC, false>(P, x, pv, cv, tv);
 #pragma unroll
     for (int q = 0; q < kVec; ++q) {
       if (x + q >= rs && x + q < re) {
@@ -581,7 +615,7 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
                       MODE == MODE_EXT ? (float)wk4[0] : 0.0f};
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
-    load_slots<HIST != HIST_NONE>(P, x, pv, cv, tv);
+    load_slots<VEC, HIST != HIST_NONE>(P, x, pv, cv, tv);
 #pragma unroll
     for (int g = 0; g < kVec / 4; ++g) {
       float sv[4];
@@ -596,7 +630,7 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
         *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
     }
     if (kAttrMode<MODE> && SHARE)
-      store_round(P, stage, ra, (int32_t)(base - ra), (int32_t)(rs - ra), (int32_t)(re - ra));
+      store_round<VEC>(P, stage, ra, (int32_t)(base - ra), (int32_t)(rs - ra), (int32_t)(re - ra));
   }
   wave_lds_sync();
 }
@@ -608,8 +642,10 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
 template <int MODE, int HIST, bool SHARE>
 __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
                                                const typename VarsOf<MODE>::type V) {
+  constexpr int VEC = kVecOf<MODE, HIST>;
+  LLMV_TILE_CONSTANTS(VEC);
   extern __shared__ double s_hist[];  // [hist_rep][n_tenants] when HIST_LDS
-  __shared__ WaveLds s_wave[kWaves];
+  __shared__ WaveLds<VEC> s_wave[kWaves];
   constexpr bool STAGE = kAttrMode<MODE> && SHARE;
   constexpr bool EXT = MODE == MODE_EXT;
   constexpr bool RSUM = kCrossSum<MODE>;
@@ -621,7 +657,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  WaveLds& W = s_wave[tid >> 6];
+  WaveLds<VEC>& W = s_wave[tid >> 6];
   uint64_t* W_r = s_rsum + (RSUM ? (tid >> 6) * kTileBatches : 0);
   double* W_k4 = s_k4 + (EXT ? (tid >> 6) * kTileBatches : 0);
   float* stage = s_stage + (STAGE ? (tid >> 6) * 64 * kStagePitch : 0);
@@ -720,7 +756,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
 #pragma unroll
         for (int r = 0; r < kRounds; ++r) {
           if (r * kRoundSlots + x0 < L) {
-            load_slots<TEN>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], tv[r]);
+            load_slots<VEC, TEN>(P, ra + r * kRoundSlots + x0, pv[r], cv[r], tv[r]);
           } else {
 #pragma unroll
             for (int q = 0; q < kVec; ++q) pv[r][q] = cv[r][q] = tv[r][q] = 0;
@@ -837,7 +873,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
               if (kAttrMode<MODE> && SHARE)
                 *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
             }
-            if (kAttrMode<MODE> && SHARE) store_round(P, stage, ra, r * kRoundSlots, xf, L);
+            if (kAttrMode<MODE> && SHARE) store_round<VEC>(P, stage, ra, r * kRoundSlots, xf, L);
           }
         }
         wave_lds_sync();

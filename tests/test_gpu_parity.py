@@ -137,8 +137,10 @@ def random_fill(rng, sizes, n_tenants=5, p_hi=5000, c_hi=200000):
 SIZE_SETS = {
     "wave-edges": [1, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513],
     "tile-edges": [767, 768, 769, 1023, 1024, 1025, 3068, 3069, 3070, 3071, 3072, 3073],
-    "wave-tile-edges": [1531, 1532, 1533, 1534, 1535, 1536, 1537, 1, 2044, 2045, 2046, 2047,
-                        2048, 2049, 2, 1280, 1281, 1279],
+    "wave-tile-edges": [1787, 1788, 1789, 1790, 1791, 1792, 1793, 1, 3583, 3584, 3585, 2,
+                        1795, 1796, 1797, 3, 1791, 1],
+    "old-tile-edges": [1531, 1532, 1533, 1534, 1535, 1536, 1537, 1, 2044, 2045, 2046, 2047,
+                       2048, 2049, 2, 1280, 1281, 1279],
     "big": [5000, 1, 2, 3, 100000, 7, 3075],
     "tiny": [1] * 700 + [2] * 300 + [3] * 100,
     "unaligned": [3, 5, 7, 1, 9, 11, 13, 2, 6, 10] * 50,
@@ -190,10 +192,11 @@ def test_request_count_tails(L, N):
     check(L, tr, None, tracegen.base_coeffs(33), tr.n_tenants, f"N={N}")
 
 
-@pytest.mark.parametrize("N", [1, 12287, 12288, 12289])
+@pytest.mark.parametrize("N", [1, 12287, 12288, 12289, 14335, 14336, 14337])
 def test_single_launch_boundary(L, N):
-    """Traces of up to 12288 requests run as one workgroup in one launch;
-    one more request takes the partitioned multi-workgroup path."""
+    """Traces of up to 14336 requests (two 1792-slot tiles per wave) run as
+    one workgroup in one launch; one more request takes the partitioned
+    multi-workgroup path."""
     rng = np.random.default_rng(N)
     sizes = []
     while sum(sizes) < N:
