@@ -86,12 +86,16 @@ enum { HIST_NONE = 0, HIST_LDS = 1, HIST_GLOBAL = 2 };
 
 // Lane slots of a tile kernel instance: the wide tile where it is faster
 // (Eq. 1 attribution without the tenant cache: 28 slots, about 2% on the
-// heavy-tailed trace); elsewhere the narrow one, where the wide tile's
+// heavy-tailed trace; the feature rows and batch sums, about 1%); the narrow
+// one for the extended model and the tenant cache, where the wide tile's
 // registers (up to 255 VGPRs) cost more than its longer tiles gain.
+__host__ __device__ constexpr bool wide_tile(int mode, int hist) {
+  return (mode == MODE_ATTR && hist != HIST_GLOBAL) || mode == MODE_FEAT || mode == MODE_SUMS;
+}
 template <int MODE, int HIST>
-constexpr int kVecOf = (MODE == MODE_ATTR && HIST != HIST_GLOBAL) ? kVecWide : kVecNarrow;
+constexpr int kVecOf = wide_tile(MODE, HIST) ? kVecWide : kVecNarrow;
 __host__ __device__ constexpr int64_t tile_cap(int mode, int hist) {
-  return 64 * ((mode == MODE_ATTR && hist != HIST_GLOBAL) ? kVecWide : kVecNarrow);
+  return 64 * (wide_tile(mode, hist) ? kVecWide : kVecNarrow);
 }
 
 struct Params {
