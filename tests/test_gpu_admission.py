@@ -84,6 +84,35 @@ def test_batch_sums_edges(L):
     assert np.array_equal(phase.cpu().numpy(), ref_p)
 
 
+@pytest.mark.parametrize("N", [12288, 12289, 14335, 14336, 14337])
+def test_batch_sums_single_launch_boundary(L, N):
+    """Up to two 1792-slot tiles per wave (14336 requests) the batch sums run
+    as one workgroup in one launch; one more request takes the partitioned
+    path.  Exact sums (and sum p*c) on both sides of the boundary, with
+    batches of mixed kinds and sizes ending exactly at N."""
+    import torch
+    rng = np.random.default_rng(N + 5)
+    sizes = []
+    while sum(sizes) < N:
+        sizes.append(int(min(rng.integers(0, 600), N - sum(sizes))))
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    pre = np.repeat(rng.random(len(sizes)) < 0.3, sizes)
+    p = np.where(pre, rng.integers(1, 8192, N), 1).astype(np.int32)
+    c = np.where(pre & (rng.random(N) < 0.5), 0, rng.integers(1, 131072, N)).astype(np.int32)
+    tr = tracegen.Trace(off, p, c, np.zeros(N, np.int32), 1, None)
+    assert tr.n_requests == N
+    sums, phase = gpu_sums(L, tr)
+    ref_s, ref_p = oracle.batch_sums(off, p, c)
+    assert np.array_equal(sums.cpu().numpy(), ref_s)
+    assert np.array_equal(phase.cpu().numpy(), ref_p)
+    dt = L.DeviceTrace.from_host(off, p, c, None)
+    s5, ph5 = L.batch_sums(dt, ext=True)
+    torch.cuda.synchronize()
+    ref5, refp5 = oracle.batch_sums_ext(off, p, c)
+    assert np.array_equal(s5.cpu().numpy(), ref5)
+    assert np.array_equal(ph5.cpu().numpy(), refp5)
+
+
 def test_admit_hand_examples(L):
     exs = ADM["examples"]
     tr = tracegen.from_batches([(e["p"], e["c"]) for e in exs], [[0] * len(e["p"]) for e in exs], 1)
