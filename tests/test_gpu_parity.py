@@ -336,6 +336,26 @@ def test_features(L, name, nb):
         assert e_b.max() <= 1e-12
 
 
+@pytest.mark.parametrize("N", [14336, 14337])
+def test_features_single_launch_boundary(L, N):
+    """The feature rows on both sides of the single-launch boundary (two
+    1792-slot tiles per wave), with batches larger than a tile among them."""
+    import torch
+    rng = np.random.default_rng(N)
+    sizes = [2000, 0, 1792, 1793]
+    while sum(sizes) < N:
+        sizes.append(int(min(rng.integers(0, 500), N - sum(sizes))))
+    tr = random_fill(rng, np.array(sizes), n_tenants=1)
+    assert tr.n_requests == N
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c)
+    shape = tracegen.SHAPES["qwen2.5-14b"]
+    xr, xb = L.features(dt, shape)
+    torch.cuda.synchronize()
+    rr, rb = oracle.features(tr.offsets, tr.p, tr.c, shape)
+    assert parity.rel_err(xr.cpu().numpy(), rr).max() <= parity.RTOL
+    assert parity.rel_err(xb.cpu().numpy(), rb).max() <= 1e-12
+
+
 # --------------------------------------------------------- tenant sums API
 
 
