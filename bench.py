@@ -54,10 +54,24 @@ def traffic_from_profile(workload, n_req, n_b):
     return prof.get("hbm_bytes_per_launch")
 
 
+def cpu_info():
+    """Host CPU model and logical CPU count (context for the oracle's rate)."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline(tr, coeffs, gpu_out, budget_s=30.0):
     """The oracle (single thread, fp64) on the same host arrays, with the same
-    outputs as the GPU step, timed.  Its results then check the GPU step's
-    outputs on sampled batches and on the tenant sums."""
+    outputs as the GPU step, timed.  Its results then check every output of
+    the GPU step: latency and regime of every batch, every share (copied back
+    in slices), every tenant sum."""
     import numpy as np
     import oracle
     sys.path.insert(0, os.path.join(ROOT, "tests"))
@@ -74,28 +88,163 @@ def cpu_baseline(tr, coeffs, gpu_out, budget_s=30.0):
     log(f"[bench] oracle on {nb} batches / {nreq} requests ...")
     t0 = time.perf_counter()
     ref = oracle.attribute(off, tr.p[:nreq], tr.c[:nreq], tr.tenant[:nreq], tr.shape, coeffs,
-                           tr.n_tenants, ("T", "regime", "share", "tenant_sums"))
+                           tr.n_tenants, ("T", "TM", "TC", "phase", "regime", "share",
+                                          "tenant_sums"))
     dt = time.perf_counter() - t0
     rate = nreq / dt
-    # parity on a sample of batches (the oracle re-run on just those batches
-    # also gives both segments' values for the tie rule)
-    rng = np.random.default_rng(5)
-    bids = np.unique(rng.integers(0, nb, min(nb, 2000)))
-    so, sp, sc, st = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
-    sub = oracle.attribute(so, sp, sc, st, tr.shape, coeffs, tr.n_tenants)
-    assert np.array_equal(sub["T"], ref["T"][bids])
-    idx = np.concatenate([np.arange(off[b], off[b + 1]) for b in bids])
-    assert np.array_equal(sub["share"], ref["share"][idx])
-    stats = parity.compare(sub, tr.offsets, gpu_out["latency"], gpu_out["regime"],
-                           gpu_out["share_sample"](idx), None, batch_ids=bids)
-    if nb == nB:
-        e = parity.rel_err(gpu_out["tenant_sums"], ref["tenant_sums"])
-        stats["tenant"] = float(e.max())
-        assert stats["tenant"] <= parity.RTOL
+    stats = parity.compare(ref, off, gpu_out["latency"][:nb], gpu_out["regime"][:nb], None,
+                           gpu_out["tenant_sums"] if nb == nB else None)
+
+    def alt_shares(bids):
+        so, sp, sc, st = parity.sub_trace(off, tr.p, tr.c, tr.tenant, bids)
+        return oracle.attribute(so, sp, sc, st, tr.shape, coeffs, tr.n_tenants,
+                                ("share_alt",))["share_alt"]
+
+    stats.update(parity.compare_all_shares(off, gpu_out["share_slice"], ref["share"], ref["TM"],
+                                           ref["TC"], ref["regime"], gpu_out["regime"][:nb],
+                                           gpu_out["latency"][:nb], alt_shares))
     sample = (f"full trace ({nreq} requests)" if nb == nB
               else f"first {nb} of {nB} batches ({nreq} requests)")
     return {"value": rate, "unit": "requests/s", "cores": 1, "kind": "oracle",
-            "sample": sample, "seconds": round(dt, 3)}, stats
+            "sample": sample, "seconds": round(dt, 3), **cpu_info()}, stats
+
+
+def calibration(hip, stream, dt, share, reps=5):
+    """STREAM-style rates of the attribution step's access mix on this GPU:
+    plain coalesced kernels (libllmv_calib) reading the trace's own p, c and
+    tenant arrays and writing the share array, over the same request count.
+    For each access kind (read 12 B, write 4 B, read 12 B + write 4 B per
+    request) and each choice of plain or non-temporal loads and stores, the
+    best of a few launch shapes (grid, elements per thread) is reported, in
+    GB/s of bytes moved."""
+    import ctypes
+    import torch
+    from paper_2608_08382_amd import build as hipbuild
+
+    lib = ctypes.CDLL(hipbuild.CALIB_OUT)
+    P = ctypes.c_void_p
+    lib.llmv_calib_stream.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      P, P, P, P, ctypes.c_int64, P, P]
+    lib.llmv_calib_stream.restype = ctypes.c_int
+    n4 = dt.n_requests // 4
+    sink = torch.zeros(4, dtype=torch.int32, device=share.device)
+    cus = torch.cuda.get_device_properties(share.device).multi_processor_count
+    ptrs = [P(x.data_ptr()) for x in (dt.p, dt.c, dt.tenant, share)]
+
+    def run(mode, flags, unroll, grid):
+        rc = lib.llmv_calib_stream(mode, flags, unroll, grid, *ptrs, n4, P(sink.data_ptr()),
+                                   P(stream))
+        if rc != 0:
+            raise RuntimeError("llmv_calib_stream failed")
+
+    kinds = {"read": (0, 12, (0, 1)), "write": (1, 4, (0, 2)), "mix_12r_4w": (2, 16, (0, 1, 2, 3))}
+    flag_names = {0: "plain", 1: "nt_loads", 2: "nt_stores", 3: "nt_loads_stores"}
+    out = {}
+    for kind, (mode, bpr, flag_set) in kinds.items():
+        for flags in flag_set:
+            best = None
+            for unroll in (1, 2, 4):
+                for per_cu in (4, 8):
+                    grid = cus * per_cu
+                    run(mode, flags, unroll, grid)
+                    torch.cuda.synchronize()
+                    ev = [(hip.create(), hip.create()) for _ in range(reps)]
+                    for a, b in ev:
+                        hip.record(a, stream)
+                        run(mode, flags, unroll, grid)
+                        hip.record(b, stream)
+                    torch.cuda.synchronize()
+                    ms = sorted(hip.elapsed_ms(a, b) for a, b in ev)[reps // 2]
+                    gbps = bpr * 4 * n4 / (ms / 1e3) / 1e9
+                    if best is None or gbps > best["gbps"]:
+                        best = {"gbps": gbps, "ms": ms, "unroll": unroll, "grid": grid}
+            name = f"{kind}_{flag_names[flags]}"
+            out[name] = best
+            log(f"[bench] calibration {name}: {best['gbps']:.0f} GB/s "
+                f"(grid {best['grid']}, {best['unroll']} per thread)")
+    best_mix = max(v["gbps"] for k, v in out.items() if k.startswith("mix"))
+    return {"unit": "GB/s", "bytes_per_request": {"read": 12, "write": 4, "mix_12r_4w": 16},
+            "n_requests": 4 * n4, "kinds": out, "best_mix_gbps": best_mix,
+            "best_mix_frac_of_peak": best_mix / PEAK_HBM_GBPS}
+
+
+def bench_configs(hip, stream, steps, with_oracle):
+    """The attribution step on the other single-GPU workloads: the tiny mixed
+    trace (1k batches; launch-bound, L2-resident, no roofline claim), the
+    decode-only trace (1M batches, Qwen2.5-14B) and the chunked-prefill trace
+    (1M batches, Qwen2.5-32B).  Each step between HIP events, the tile
+    kernel between the library's own events, and, with the oracle, every
+    output checked."""
+    import numpy as np
+    import torch
+    import tracegen
+    from paper_2608_08382_amd import llmv
+
+    res = {}
+    for name in ("tiny-mixed", "decode-only", "chunked-prefill"):
+        tr = tracegen.config_trace(name)
+        co = tracegen.config_coeffs(name)
+        dt = llmv.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+        dev = dt.p.device
+        lat = torch.empty(tr.n_batches, dtype=torch.float32, device=dev)
+        reg = torch.empty(tr.n_batches, dtype=torch.uint8, device=dev)
+        share = torch.empty(tr.n_requests, dtype=torch.float32, device=dev)
+        tsum = torch.empty(tr.n_tenants, dtype=torch.float64, device=dev)
+        ws = llmv.workspace(tr.n_batches, tr.n_requests, tr.n_tenants)
+
+        def step():
+            llmv.llmv_attribute(dt, tr.shape, co, lat, reg, share, tr.n_tenants, tsum, ws)
+
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        evs = [(hip.create(), hip.create()) for _ in range(steps)]
+        start, stop = hip.create(), hip.create()
+        hip.record(start, stream)
+        for i in range(steps):
+            llmv.llmv_set_kernel_events(*evs[i])
+            step()
+        llmv.llmv_set_kernel_events(None, None)
+        hip.record(stop, stream)
+        torch.cuda.synchronize()
+        ms = hip.elapsed_ms(start, stop) / steps
+        k_ms = sum(hip.elapsed_ms(a, b) for a, b in evs) / steps
+        nbytes = algorithmic_bytes(tr.n_requests, tr.n_batches)
+        gbps = nbytes / (k_ms / 1e3) / 1e9
+        r = {"n_requests": tr.n_requests, "n_batches": tr.n_batches, "n_tenants": tr.n_tenants,
+             "shape": tracegen.CONFIGS[name][2], "ms_per_step": ms,
+             "value": tr.n_requests / (ms / 1e3), "unit": "requests/s", "kernel_ms": k_ms,
+             "algorithmic_bytes": nbytes}
+        if name == "tiny-mixed":
+            r["note"] = ("launch-bound: 0.27 MB, one workgroup in one launch; not a roofline "
+                         "number")
+        else:
+            r["roofline"] = {"bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS,
+                             "unit": "GB/s", "frac": gbps / PEAK_HBM_GBPS, "kernel": "k_tiles"}
+        log(f"[bench] {name}: {ms:.4f} ms/step, tile kernel {k_ms:.4f} ms, {gbps:.0f} GB/s")
+        if with_oracle:
+            import oracle
+            sys.path.insert(0, os.path.join(ROOT, "tests"))
+            import parity
+            ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co,
+                                   tr.n_tenants, ("T", "TM", "TC", "phase", "regime", "share",
+                                                  "tenant_sums"))
+            lat_h, reg_h = lat.cpu().numpy(), reg.cpu().numpy()
+            st = parity.compare(ref, tr.offsets, lat_h, reg_h, None, tsum.cpu().numpy())
+
+            def alt_shares(bids):
+                so, sp, sc, stt = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
+                return oracle.attribute(so, sp, sc, stt, tr.shape, co, tr.n_tenants,
+                                        ("share_alt",))["share_alt"]
+
+            st.update(parity.compare_all_shares(
+                tr.offsets, lambda lo, hi: share[lo:hi].cpu().numpy(), ref["share"], ref["TM"],
+                ref["TC"], ref["regime"], reg_h, lat_h, alt_shares))
+            r["parity"] = st
+        res[name] = r
+        del dt, lat, reg, share, tsum, ws
+        torch.cuda.empty_cache()
+    return res
 
 
 def bench_sweep(hip, stream, with_oracle):
@@ -535,6 +684,10 @@ def main():
                     help="skip the fitting and metrics measurement")
     ap.add_argument("--no-admission", action="store_true",
                     help="skip the admission-query measurement")
+    ap.add_argument("--no-calibration", action="store_true",
+                    help="skip the STREAM-style bandwidth calibration")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the tiny, decode-only and chunked-prefill workloads")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="also run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -569,6 +722,12 @@ def main():
     def step():
         llmv.llmv_attribute(dt, tr.shape, coeffs, lat, reg, share, tr.n_tenants, tsum, ws)
 
+    hip = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    # bandwidth calibration on the same arrays (it overwrites the shares,
+    # so it runs before the steps)
+    calib = None if args.no_calibration else calibration(hip, stream, dt, share)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -576,8 +735,6 @@ def main():
     # timed region: K steps, HIP events on the stream the kernels run on:
     # one pair around the whole region, one pair around each step's tile
     # kernel (recorded by the library right before / after that launch)
-    hip = HipEvents()
-    stream = torch.cuda.current_stream().cuda_stream
     evs = [(hip.create(), hip.create()) for _ in range(args.steps)]
     start, stop = hip.create(), hip.create()
     torch.cuda.synchronize()
@@ -632,7 +789,7 @@ def main():
     regimes = np.bincount(reg_host[reg_host != 255], minlength=4)[:4]
     gpu_out = {"latency": lat.cpu().numpy(), "regime": reg_host,
                "tenant_sums": tsum.cpu().numpy(),
-               "share_sample": lambda idx: _gather(share, idx, tr.n_requests)}
+               "share_slice": lambda lo, hi: share[lo:hi].cpu().numpy()}
 
     traffic = traffic_from_profile(args.workload, tr.n_requests, tr.n_batches)
     result = {
@@ -646,7 +803,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64",
+        "dtype": "i64+f64+f32",
+        "dtype_detail": ("exact integer batch sums; fp64 batch model and share constants; "
+                         "fp32 per-request shares (three FMAs on fp32-rounded constants); fp64 "
+                         "tenant sums"),
         "data": "synthetic",
         "config": {"workload": args.workload, "n_batches": tr.n_batches,
                    "n_requests": tr.n_requests, "shape": tracegen.CONFIGS[args.workload][2],
@@ -658,11 +818,17 @@ def main():
         "regime_mix": {"prefill_mem": int(regimes[0]), "prefill_comp": int(regimes[1]),
                        "decode_mem": int(regimes[2]), "decode_comp": int(regimes[3])},
     }
+    if calib is not None:
+        result["calibration"] = calib
+        result["roofline"]["frac_of_calibrated_mix"] = achieved / calib["best_mix_gbps"]
     if not args.no_cpu_baseline:
         cb, stats = cpu_baseline(tr, coeffs, gpu_out)
         result["cpu_baseline"] = cb
         result["parity"] = {k: v for k, v in stats.items()}
         log(f"[bench] oracle {cb['value']:.3e} req/s on {cb['cores']} core; parity {stats}")
+    if not args.no_configs:
+        # the heavy-tailed trace stays resident; the others come and go
+        result["configs"] = bench_configs(hip, stream, args.steps, not args.no_cpu_baseline)
     if not args.no_ext:
         result["extended_model"] = bench_ext(hip, stream, dt, tr, (lat, reg, share, tsum), ws,
                                              max(5, args.steps // 2), not args.no_cpu_baseline)
@@ -719,14 +885,6 @@ class HipEvents:
         ms = self.ct.c_float()
         self._ok(self.lib.hipEventElapsedTime(self.ct.byref(ms), a, b), "hipEventElapsedTime")
         return ms.value
-
-
-def _gather(share, idx, n):
-    import numpy as np
-    import torch
-    out = np.zeros(n, np.float32)
-    out[idx] = share[torch.from_numpy(idx).to(share.device)].cpu().numpy()
-    return out
 
 
 if __name__ == "__main__":

@@ -10,6 +10,10 @@ SOURCES = [os.path.join(PKG, "csrc", "api.hip"), os.path.join(PKG, "csrc", "fit.
 DEPS = SOURCES + [os.path.join(PKG, "csrc", h) for h in ("kernels.hpp", "groups.hpp", "fit.hpp", "host.hpp")] + [
     os.path.join(ROOT, "include", "llmv.h")]
 OUT = os.path.join(PKG, "libllmv.so")
+# bandwidth calibration kernels (measurement context for the benchmark; not
+# part of libllmv's C ABI)
+CALIB_SOURCES = [os.path.join(PKG, "csrc", "calib.hip")]
+CALIB_OUT = os.path.join(PKG, "libllmv_calib.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -21,9 +25,10 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(out: str = OUT, verbose: bool = False) -> str:
+def build(out: str = OUT, verbose: bool = False, sources=None) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), *SOURCES, "-o", out + ".tmp"]
+    sources = SOURCES if sources is None else sources
+    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), *sources, "-o", out + ".tmp"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
@@ -40,5 +45,10 @@ def is_stale(out: str = OUT) -> bool:
     return any(os.path.getmtime(d) > t for d in DEPS)
 
 
+def build_calib(verbose: bool = False) -> str:
+    return build(CALIB_OUT, verbose, CALIB_SOURCES)
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_calib(verbose=True))

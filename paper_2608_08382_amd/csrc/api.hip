@@ -169,7 +169,7 @@ GroupLayout group_layout(size_t o, int64_t nB, int64_t N, bool ext) {
   G.gofs = o;
   o += align_up((size_t)(nB + 1) * sizeof(int64_t));
   G.bsum = o;
-  o += align_up((size_t)((ext ? 4 : 3) * nB + 1) * sizeof(unsigned long long));
+  o += align_up((size_t)((ext ? 5 : 4) * nB + 1) * sizeof(unsigned long long));
   G.tsum = o;
   o += align_up((size_t)(nt + 1) * sizeof(int64_t));
   G.gw = o;
@@ -451,7 +451,7 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   sm.F = nS * kSlice;
   rc = partition(trace, sm, first, claims, st);
   if (rc) return rc;
-  hipLaunchKernelGGL(k_zero_u64, dim3(256), dim3(kWG), 0, st, bsum, (EXT ? 4 : 3) * nB);
+  hipLaunchKernelGGL(k_zero_u64, dim3(256), dim3(kWG), 0, st, bsum, (EXT ? 5 : 4) * nB);
   HIP_TRY(hipGetLastError(), "k_zero_u64 launch");
   int64_t bgrid = (nS + kWaves - 1) / kWaves;
   const int64_t bcap = (int64_t)cus * blocks_per_cu(k_group_build<true, EXT>, 0);

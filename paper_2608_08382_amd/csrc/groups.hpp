@@ -173,8 +173,8 @@ __device__ __forceinline__ uint32_t grp_hash(uint32_t t) {
 // contiguous even when slices split it.  first[k] = the first batch starting
 // at or after request k*kSlice (k_partition over equal chunks).
 // WRITE = false: slice_cnt[k] = groups of slice k; bsum[j*nB + b] (zeroed
-// beforehand) += (sum p, sum c + 2^48 * count of c == 0, sum p^2, and with
-// EXT sum p*c) of the part of batch b in the slice.  WRITE = true: the groups
+// beforehand) += (sum p, sum c, sum p^2, count of c == 0, and with EXT
+// sum p*c) of the part of batch b in the slice.  WRITE = true: the groups
 // from slice_off[k] on, gw = ((b mod 2^20) << 12) | tenant, gf = (n, P, C, Q)
 // and with EXT gr = R (sum p*c), rounded to fp32, and gofs[b] for every
 // batch starting in the slice (gofs[nB] by the last).  Both passes emit the
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kWG) void k_group_build(
       if (WRITE && bo0 >= r0 && lane == 0) gofs[b] = out;
       const int64_t lo = max(bo0, r0), hi = min(bo1, r1);
       int32_t taken = 0;
-      uint64_t sp = 0, scz = 0, sq = 0, sr = 0;
+      uint64_t sp = 0, sc = 0, sq = 0, sz = 0, sr = 0;
       for (int64_t base = lo; base < hi; base += 64) {
         const int64_t i = base + lane;
         bool fresh = false;
@@ -221,7 +221,8 @@ __global__ __launch_bounds__(kWG) void k_group_build(
           const uint64_t pc = (uint64_t)pi * ci;
           if (!WRITE) {
             sp += pi;
-            scz += (uint64_t)ci + (ci == 0 ? kZeroUnit : 0ull);
+            sc += ci;
+            sz += ci == 0 ? 1u : 0u;
             sq += pp;
             if (EXT) sr += pc;
           }
@@ -277,20 +278,23 @@ __global__ __launch_bounds__(kWG) void k_group_build(
       }
       if (!WRITE) {
         sp = wave_sum(sp);
-        scz = wave_sum(scz);
+        sc = wave_sum(sc);
         sq = wave_sum(sq);
+        sz = wave_sum(sz);
         if (EXT) sr = wave_sum(sr);
         if (lane == 0) {
           if (bo0 >= r0 && bo1 <= r1) {  // the whole batch
             bsum[b] = sp;
-            bsum[nB + b] = scz;
+            bsum[nB + b] = sc;
             bsum[2 * nB + b] = sq;
-            if (EXT) bsum[3 * nB + b] = sr;
+            bsum[3 * nB + b] = sz;
+            if (EXT) bsum[4 * nB + b] = sr;
           } else {
             atomicAdd(&bsum[b], (unsigned long long)sp);
-            atomicAdd(&bsum[nB + b], (unsigned long long)scz);
+            atomicAdd(&bsum[nB + b], (unsigned long long)sc);
             atomicAdd(&bsum[2 * nB + b], (unsigned long long)sq);
-            if (EXT) atomicAdd(&bsum[3 * nB + b], (unsigned long long)sr);
+            atomicAdd(&bsum[3 * nB + b], (unsigned long long)sz);
+            if (EXT) atomicAdd(&bsum[4 * nB + b], (unsigned long long)sr);
           }
         }
       }
@@ -394,8 +398,8 @@ static_assert(kGV % 4 == 0 && kGBof<5> < 64 && kGBof<7> < 64, "sweep tile shape"
 struct GroupSweep {
   const int64_t* off;               // request offsets [nB + 1]
   const int64_t* gofs;              // group offsets [nB + 1]
-  const unsigned long long* bsum;   // [3][nB]: sum p, sum c | zero count << 48, sum p^2;
-                                    // [4][nB] with sum p*c (extended model)
+  const unsigned long long* bsum;   // [4][nB]: sum p, sum c, sum p^2, count of c == 0;
+                                    // [5][nB] with sum p*c (extended model)
   const uint32_t* gw;               // [groups + kGT] ((b mod 2^20) << 12) | tenant
   const v4f* gf;                    // [groups + kGT] (n, P, C, Q)
   const float* gr;                  // [groups + kGT] R = sum p*c (extended model)
@@ -462,12 +466,13 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
         const int64_t bb = b + lane;
         const int64_t n = P.off[bb + 1] - P.off[bb];
         if (n > 0) {
-          const uint64_t sp = P.bsum[bb], scz = P.bsum[P.nB + bb], sq = P.bsum[2 * P.nB + bb];
-          const uint64_t sr = EXT ? P.bsum[3 * P.nB + bb] : 0;
+          const uint64_t sp = P.bsum[bb], sc = P.bsum[P.nB + bb], sq = P.bsum[2 * P.nB + bb];
+          const uint64_t sz = P.bsum[3 * P.nB + bb];
+          const uint64_t sr = EXT ? P.bsum[4 * P.nB + bb] : 0;
           // decode iff every request processes one token over a nonzero context
-          const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
+          const bool prefill = (sp != (uint64_t)n) || (sz != 0);
           float k0[kSweepG];
-          const uint32_t sg = sweep_batch<NV, NC>(V, n, sp, scz & kCMask, sq, sr, prefill, k0);
+          const uint32_t sg = sweep_batch<NV, NC>(V, n, sp, sc, sq, sr, prefill, k0);
           const int ph = prefill ? 0 : 1;
 #pragma unroll
           for (int g = 0; g < NV; ++g) {

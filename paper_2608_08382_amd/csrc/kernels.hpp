@@ -461,8 +461,14 @@ struct TileShape {
   constexpr int kStagePitch = TileShape<(VEC)>::kStagePitch;              \
   (void)kVec; (void)kRoundSlots; (void)kTile; (void)kTileMaskWords; (void)kStagePitch
 
+// Within one wave tile the sum of c and the count of c == 0 share a word:
+// a tile holds fewer than 2^16 requests, each c < 2^31, so sum c < 2^47
+// stays below the count's bits.  (big_batch keeps them apart: a batch
+// larger than a tile may reach 2^22 requests and sum c up to 2^53.)
 constexpr uint64_t kZeroUnit = 1ull << 48;      // count of c == 0, above the c sum
 constexpr uint64_t kCMask = kZeroUnit - 1;
+static_assert(64 * kVecWide < (1 << 16) && 64ull * kVecWide * 0x7fffffffull < kZeroUnit,
+              "a wave tile's zero count and sum of c fit their fields");
 
 struct BatchAcc {
   uint64_t p;   // sum p
@@ -578,7 +584,11 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
   LLMV_TILE_CONSTANTS(VEC);
   const int lane = threadIdx.x & 63;
   const int64_t ra = rs & ~(int64_t)3;
-  uint64_t sp = 0, scz = 0, sq = 0, sr = 0;
+  // Sums over up to 2^22 requests: sum c reaches 2^53, so the tile path's
+  // packed (sum c, zero count) word does not apply; a zero context is
+  // recorded as a flag of its own.
+  uint64_t sp = 0, sc = 0, sq = 0, sr = 0;
+  bool zc = false;  // this lane saw a request with c == 0
   int32_t pv[kVec], cv[kVec], tv[kVec];
   for (int64_t base = ra; base < re; base += kRoundSlots) {
     const int64_t x = base + lane * kVec;
@@ -588,30 +598,29 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
       if (x + q >= rs && x + q < re) {
         const uint32_t p = (uint32_t)pv[q], c = (uint32_t)cv[q];
         sp += p;
-        scz += (uint64_t)c + (c == 0 ? kZeroUnit : 0ull);
+        sc += c;
+        zc |= c == 0;
         sq += (uint64_t)p * p;
         if constexpr (kCrossSum<MODE>) sr += (uint64_t)p * c;
       }
     }
   }
   sp = wave_sum(sp);
-  scz = wave_sum(scz);
+  sc = wave_sum(sc);
   sq = wave_sum(sq);
   if constexpr (kCrossSum<MODE>) sr = wave_sum(sr);
   const int64_t n = re - rs;
+  // decode iff every request processes one token over a nonzero context
+  const bool prefill = (sp != (uint64_t)n) || (__ballot(zc) != 0);
   if constexpr (MODE == MODE_SUMS) {
-    if (lane == 0) {
-      const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
-      sums_out(P, bg, n, sp, scz & kCMask, sq, sr, prefill);
-    }
+    if (lane == 0) sums_out(P, bg, n, sp, sc, sq, sr, prefill);
     return;
   }
   if (lane == 0) {
-    const bool prefill = (sp != (uint64_t)n) || ((scz >> 48) != 0);
     if constexpr (MODE == MODE_EXT)
-      ext_model(P, V, bg, n, sp, scz & kCMask, sq, sr, prefill, W.k[0], wk4);
+      ext_model(P, V, bg, n, sp, sc, sq, sr, prefill, W.k[0], wk4);
     else
-      batch_model<MODE>(P, bg, n, sp, scz & kCMask, sq, prefill, W.k[0]);
+      batch_model<MODE>(P, bg, n, sp, sc, sq, prefill, W.k[0]);
   }
   wave_lds_sync();
   const double kd[4] = {W.k[0][0], W.k[0][1], W.k[0][2], W.k[0][3]};

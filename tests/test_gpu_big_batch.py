@@ -1,0 +1,182 @@
+"""GPU parity for batches larger than a wave tile at the edges of the
+input limits (Sec. 2.1, Eq. 1: exact sums of p, c and p^2 per batch and the
+phase they imply).  A batch of more than 65,535 zero-context requests and a
+decode batch whose sum of c passes 2^48 must keep the exact sums and the
+phase, through every entry point that forms batch sums: attribution (Eq. 1
+and the extended model), feature rows, batch sums, and the what-if sweep."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import tracegen
+
+pytestmark = pytest.mark.gpu
+
+C_MAX = (1 << 31) - 1
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def L():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_08382_amd import llmv
+    llmv.load()
+    torch.cuda.set_device(0)
+    return llmv
+
+
+def fill(kind, n, rng):
+    """(p, c) of one batch of n requests."""
+    p = np.ones(n, np.int32)
+    if kind == "zero-context":        # prefill-type requests (c == 0): PREFILL
+        c = np.zeros(n, np.int32)
+    elif kind == "max-context":       # decode at the largest context: sum c >= 2^48
+        c = np.full(n, C_MAX, np.int32)
+    elif kind == "one-zero-last":     # decode except the last request: PREFILL
+        c = np.full(n, C_MAX, np.int32)
+        c[-1] = 0
+    elif kind == "decode":
+        c = rng.integers(1, 1 << 17, n).astype(np.int32)
+    elif kind == "prefill":
+        p = rng.integers(1, 4096, n).astype(np.int32)
+        c = np.zeros(n, np.int32)
+    else:
+        raise KeyError(kind)
+    return p, c
+
+
+# (kind, size): 65,536 and 131,072 zero-context requests (the count of
+# c == 0 is a multiple of 2^16), 131,073 requests at c = 2^31 - 1 (sum c =
+# 2^48 + 2^17 - ... > 2^48), small neighbours on both sides
+LAYOUTS = {
+    "zero-65536": [("decode", 3), ("zero-context", 65536), ("prefill", 5)],
+    "zero-131072": [("zero-context", 131072), ("decode", 2)],
+    "max-context-131073": [("decode", 7), ("max-context", 131073), ("decode", 1)],
+    "mixed-giants": [("prefill", 2), ("zero-context", 65536), ("decode", 4),
+                     ("max-context", 131073), ("one-zero-last", 70000), ("decode", 3)],
+}
+
+
+def make_trace(key, n_tenants=3):
+    rng = np.random.default_rng(sum(map(ord, key)))
+    ps, cs, sizes = [], [], []
+    for kind, n in LAYOUTS[key]:
+        p, c = fill(kind, n, rng)
+        ps.append(p)
+        cs.append(c)
+        sizes.append(n)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    p = np.concatenate(ps)
+    c = np.concatenate(cs)
+    t = rng.integers(0, n_tenants, len(p)).astype(np.int32)
+    return tracegen.Trace(off, p, c, t, n_tenants, None)
+
+
+def expected_phases(key):
+    want = []
+    for kind, _ in LAYOUTS[key]:
+        want.append(1 if kind in ("decode", "max-context") else 0)
+    return np.array(want, np.uint8)
+
+
+@pytest.mark.parametrize("key", sorted(LAYOUTS))
+def test_big_batch_sums_exact(L, key):
+    import torch
+    tr = make_trace(key)
+    say(f"[big] batch sums {key}: sizes {tr.sizes().tolist()}")
+    ref_s, ref_p = oracle.batch_sums(tr.offsets, tr.p, tr.c)
+    assert np.array_equal(ref_p, expected_phases(key))
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, None)
+    for ext in (False, True):
+        sums, phase = L.batch_sums(dt, ext=ext)
+        torch.cuda.synchronize()
+        want_s = oracle.batch_sums_ext(tr.offsets, tr.p, tr.c)[0] if ext else ref_s
+        assert np.array_equal(sums.cpu().numpy(), want_s), (key, ext)
+        assert np.array_equal(phase.cpu().numpy(), ref_p), (key, ext)
+    if "max-context" in key:
+        assert ref_s[2].max() >= 1 << 48
+
+
+@pytest.mark.parametrize("key", sorted(LAYOUTS))
+def test_big_batch_attribute(L, key):
+    import torch
+    tr = make_trace(key)
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    for shape, co in ((None, tracegen.base_coeffs(91)),
+                      (tracegen.SHAPES["llama3.1-8b"], tracegen.config_coeffs("heavy-tailed"))):
+        out = L.attribute(dt, shape, co, tr.n_tenants)
+        torch.cuda.synchronize()
+        g = {k: v.cpu().numpy() for k, v in out.items()}
+        ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shape, co, tr.n_tenants)
+        assert np.array_equal(g["regime"] // 2, expected_phases(key)), key
+        st = parity.compare(ref, tr.offsets, g["latency"], g["regime"], g["share"],
+                            g["tenant_sums"])
+        say(f"[big] attribute {key} shape={shape is not None}: {st}")
+
+
+@pytest.mark.parametrize("key", sorted(LAYOUTS))
+def test_big_batch_attribute_ext(L, key):
+    import torch
+    tr = make_trace(key)
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    shape = tracegen.SHAPES["qwen2.5-14b"]
+    co = tracegen.ext_coeffs(104)
+    out = L.attribute_ext(dt, shape, co, tr.n_tenants,
+                          ws=L.workspace(tr.n_batches, tr.n_requests, tr.n_tenants))
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.attribute_ext(tr.offsets, tr.p, tr.c, tr.tenant, shape, co, tr.n_tenants)
+    assert np.array_equal(g["regime"] // 2, expected_phases(key)), key
+    st = parity.compare(ref, tr.offsets, g["latency"], g["regime"], g["share"], g["tenant_sums"])
+    say(f"[big] attribute_ext {key}: {st}")
+
+
+@pytest.mark.parametrize("key", sorted(LAYOUTS))
+def test_big_batch_features(L, key):
+    import torch
+    tr = make_trace(key)
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c)
+    shape = tracegen.SHAPES["70b-like"]
+    xr, xb = L.features(dt, shape)
+    torch.cuda.synchronize()
+    rr, rb = oracle.features(tr.offsets, tr.p, tr.c, shape)
+    assert parity.rel_err(xr.cpu().numpy(), rr).max() <= parity.RTOL
+    assert parity.rel_err(xb.cpu().numpy(), rb).max() <= 1e-12
+
+
+@pytest.mark.parametrize("ext", [False, True])
+def test_big_batch_sweep(L, ext):
+    """The sweep's exact batch sums (built per 2048-request slice and added
+    across slices) on every layout at once: 10 settings, two passes."""
+    import torch
+    rng = np.random.default_rng(5)
+    parts = [make_trace(k) for k in sorted(LAYOUTS)]
+    sizes = np.concatenate([t.sizes() for t in parts])
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    tr = tracegen.Trace(off, np.concatenate([t.p for t in parts]),
+                        np.concatenate([t.c for t in parts]),
+                        rng.integers(0, 5, int(off[-1])).astype(np.int32), 5, None)
+    shapes = [tracegen.SHAPES["llama3.1-8b"], tracegen.SHAPES["qwen2.5-32b"]]
+    if ext:
+        co = np.stack([tracegen.ext_coeffs(700 + j) for j in range(5)])
+    else:
+        co = tracegen.sweep_coeffs(tracegen.config_coeffs("heavy-tailed"), 5)
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    out = L.attribute_sweep(dt, shapes, co, tr.n_tenants, ext=ext)
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    attr = oracle.attribute_ext if ext else oracle.attribute
+    for s in range(2):
+        for v in range(5):
+            ref = attr(tr.offsets, tr.p, tr.c, tr.tenant, shapes[s], co[v], tr.n_tenants,
+                       ("tenant_sums",))["tenant_sums"]
+            e = parity.rel_err(out[s, v], ref)
+            assert e.max() <= parity.RTOL, (ext, s, v, e.max())

@@ -402,13 +402,16 @@ def test_validate(L):
     assert v(tr.offsets[:-1], tr.p, tr.c, tr.tenant) == L.LLMV_ERANGE
 
 
-# ----------------------------------------- full-size workloads, sampled
+# ------------------------------------------------- full-size workloads
 
 
-def full_size_sampled(L, name, n_sample=1500):
-    """Latency, regime and tenant sums of every batch against the oracle;
-    shares of sampled batches against it, and of every request by property.
-    Outputs start as NaN (regime 0xEE), so an unwritten one fails."""
+def full_size(L, name):
+    """Every output of the whole trace against the oracle: latency and regime
+    of every batch, every share (copied back in slices of whole batches; each
+    batch's shares also add up to its latency), every tenant sum.  Outputs
+    start as NaN (regime 0xEE), so an unwritten one fails.  The traces of
+    ~1e8 requests and more run the static pieces and the claimed chunks of
+    the tile kernel's work split."""
     import torch
     tr = tracegen.config_trace(name)
     co = tracegen.config_coeffs(name)
@@ -425,38 +428,27 @@ def full_size_sampled(L, name, n_sample=1500):
     lat = lat_d.cpu().numpy()
     reg = reg_d.cpu().numpy()
     ts = ts_d.cpu().numpy()
-    # every share written; per batch they add up to the latency, so in total too
-    assert not bool(torch.isnan(share).any())
-    share_total = float(share.double().sum())
-    rng = np.random.default_rng(99)
-    sizes = tr.sizes()
-    bids = np.unique(np.concatenate([
-        rng.integers(0, tr.n_batches, n_sample), np.arange(5), tr.n_batches - 1 - np.arange(5),
-        np.argsort(sizes)[-20:]]))
-    # shares of the sampled batches only
-    idx = np.concatenate([np.arange(tr.offsets[b], tr.offsets[b + 1]) for b in bids])
-    g_share = np.zeros(tr.n_requests, np.float32)
-    g_share[idx] = share[torch.from_numpy(idx).cuda()].cpu().numpy()
-    del share, dt, ws
-    torch.cuda.empty_cache()
-    off, p, c, t = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
-    ref = oracle.attribute(off, p, c, t, tr.shape, co, tr.n_tenants,
-                           ("T", "TM", "TC", "phase", "regime", "share", "share_alt"))
-    st = parity.compare(ref, tr.offsets, lat, reg, g_share, None, batch_ids=bids)
-    # every batch and tenant of the whole trace
-    ref_all = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co, tr.n_tenants,
-                               ("T", "TM", "TC", "phase", "regime", "tenant_sums"))
-    st_all = parity.compare(ref_all, tr.offsets, lat, reg, None, ts)
-    st["all_batches"] = st_all
+    del dt, ws
+    ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, tr.shape, co, tr.n_tenants,
+                           ("T", "TM", "TC", "phase", "regime", "share", "tenant_sums"))
+    st = parity.compare(ref, tr.offsets, lat, reg, None, ts)
+
+    def alt_shares(bids):
+        off, p, c, t = parity.sub_trace(tr.offsets, tr.p, tr.c, tr.tenant, bids)
+        return oracle.attribute(off, p, c, t, tr.shape, co, tr.n_tenants,
+                                ("share_alt",))["share_alt"]
+
+    st.update(parity.compare_all_shares(tr.offsets, lambda lo, hi: share[lo:hi].cpu().numpy(),
+                                        ref["share"], ref["TM"], ref["TC"], ref["regime"], reg,
+                                        lat, alt_shares))
     tot = lat.astype(np.float64).sum()
     assert abs(ts.sum() - tot) / tot <= parity.RTOL
-    assert abs(share_total - tot) / tot <= parity.RTOL
     say(f"[full] {name}: {st}")
 
 
 @pytest.mark.parametrize("name", ["decode-only", "chunked-prefill", "heavy-tailed"])
-def test_full_size_sampled(L, name):
-    full_size_sampled(L, name)
+def test_full_size(L, name):
+    full_size(L, name)
 
 
 # ---------------------------------------------------------- what-if sweep
@@ -597,6 +589,26 @@ def test_sweep_refuses_a_small_workspace(L):
     assert e.value.code == L.LLMV_EWORKSPACE
     torch.cuda.synchronize()
     assert bool((out == -1.0).all())
+
+
+def test_sweep_claimed_chunks_two_passes(L):
+    """The decode-only trace (1.28e8 requests) under 10 settings: the pass
+    kernel's work split then has claimed chunks (a worker's share of the
+    requests passes 32 narrow tiles, 49,152 requests, at 2048 wave workers
+    and more), and the second pass starts at claim n_chunks.  Every setting's
+    tenant sums against the oracle."""
+    tr = tracegen.config_trace("decode-only")
+    assert tr.n_requests > 2048 * 49152
+    co = tracegen.sweep_coeffs(tracegen.config_coeffs("decode-only"), 10)
+    shapes = [tracegen.SHAPES["qwen2.5-14b"]]
+    say(f"[sweep] claimed chunks: N={tr.n_requests} settings=10")
+    out = run_sweep(L, tr, shapes, co)
+    for v in range(10):
+        ref = oracle.attribute(tr.offsets, tr.p, tr.c, tr.tenant, shapes[0], co[v], tr.n_tenants,
+                               ("tenant_sums",))["tenant_sums"]
+        e = parity.rel_err(out[0, v], ref)
+        say(f"[sweep] claimed chunks, setting {v}: max rel err {e.max():.2e}")
+        assert e.max() <= parity.RTOL, (v, e.max())
 
 
 def test_sweep_full_size_sampled(L):

@@ -259,7 +259,8 @@ def test_fit_workspace_size(llmv):
 def test_sweep_workspace_size(llmv):
     """The sweep's workspace: the common one (with a tenant histogram per
     setting of a pass) plus 20 bytes per request for the (batch, tenant)
-    groups, 32 bytes per batch for their offsets and the exact batch sums."""
+    groups, 40 bytes per batch for their offsets, the exact batch sums and
+    the count of zero-context requests."""
     lib = llmv.load()
     nB, N, T = 10_000, 1 << 24, 1024  # N large enough for the largest grid
     base = lib.llmv_sweep_workspace_size(nB, N, T)
@@ -268,15 +269,15 @@ def test_sweep_workspace_size(llmv):
     dn = lib.llmv_sweep_workspace_size(nB, N + (1 << 20), T) - base
     assert 20 << 20 <= dn <= (20 << 20) + 3 * 8 * ((1 << 20) // 2048) + 8 * 256
     db = lib.llmv_sweep_workspace_size(nB + (1 << 16), N, T) - base
-    assert 32 << 16 <= db <= (32 << 16) + 3 * 256
+    assert 40 << 16 <= db <= (40 << 16) + 3 * 256
     assert lib.llmv_sweep_workspace_size(0, 0, 1) > 0
     assert lib.llmv_sweep_workspace_size(-5, -5, -5) == lib.llmv_sweep_workspace_size(0, 0, 0)
 
 
 def test_sweep_workspace_size_ext(llmv):
     """The extended sweep's workspace: the Eq. 1 sweep's plus the groups'
-    sums of p*c (4 bytes per request) and a fourth exact batch sum (8 bytes
-    per batch)."""
+    sums of p*c (4 bytes per request) and one more row of exact batch sums
+    (8 bytes per batch)."""
     lib = llmv.load()
     nB, N, T = 10_000, 1 << 24, 1024
     for n_b, n in ((nB, N), (nB + (1 << 16), N), (nB, N + (1 << 20))):
