@@ -109,7 +109,7 @@ size_t llmv_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tena
 
 /* Bytes of device workspace llmv_attribute_sweep needs for a trace of this
  * size: llmv_workspace_size's (with a histogram per setting of a pass)
- * plus the (batch, tenant) groups: 20 bytes per request, 32 bytes per batch
+ * plus the (batch, tenant) groups: 20 bytes per request, 40 bytes per batch
  * and a few KiB. */
 size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants);
 
@@ -137,6 +137,27 @@ int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
                    const float coeffs[20], float *latency, uint8_t *regime,
                    float *share, int32_t n_tenants, double *tenant_sums,
                    void *ws, size_t ws_bytes, void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * llmv_attribute with no workspace argument.  The scratch it needs (chunk
+ * table, claim counter, per-workgroup tenant partials) is a static device
+ * array of LLMV_NOALLOC_SCRATCH_BYTES in the library, one per GPU, held
+ * until the process ends; its address is looked up once per device on the
+ * first call there.  The call allocates nothing (no hipMalloc, no library
+ * allocation); the caller still passes every input and output.  Outputs,
+ * precision, ordering and errors are those of llmv_attribute; a trace whose
+ * scratch (llmv_workspace_size of its sizes) exceeds the static array is
+ * refused with LLMV_EINVAL before anything is enqueued.  Every call on one
+ * GPU shares that GPU's array: calls that overlap in time on one GPU (other
+ * streams, other host threads) race and must be serialised by the caller.
+ * Each call rewrites what it reads of the array (the claim counter is
+ * cleared by its first kernel), so no state carries over between calls. */
+#define LLMV_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int llmv_attribute_noalloc(const llmv_trace *trace, const llmv_shape *shape,
+                           const float coeffs[20], float *latency, uint8_t *regime,
+                           float *share, int32_t n_tenants, double *tenant_sums,
+                           void *stream);
 
 /* Extended model (feature variants the paper leaves open; Sec. 2.1 defines
  * Eq. 1 only).  Two more features per batch, each with its own coefficient

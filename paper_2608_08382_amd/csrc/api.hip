@@ -13,6 +13,11 @@
 #include "kernels.hpp"
 #include "llmv.h"
 
+namespace llmv {
+// Scratch of llmv_attribute_noalloc, one copy per device (see llmv.h).
+__device__ __align__(256) unsigned char scratch[LLMV_NOALLOC_SCRATCH_BYTES];
+}  // namespace llmv
+
 using namespace llmv;
 using namespace llmv::host;
 
@@ -20,6 +25,27 @@ namespace {
 
 thread_local hipEvent_t g_ev_before = nullptr;  // measurement hook
 thread_local hipEvent_t g_ev_after = nullptr;
+
+// Static scratch of llmv_attribute_noalloc: the device address of `scratch`
+// on each device, looked up once per device (hipGetSymbolAddress with that
+// device current).  Host code uses these addresses, never the array's name.
+std::mutex g_scratch_mu;
+void* g_scratch_dev[64] = {};
+
+int scratch_address(void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(LLMV_EDEVICE, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(llmv::scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(LLMV_EDEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return LLMV_OK;
+}
 
 // Upper bound of the persistent grid for n requests (sizes the workspace):
 // no more than one workgroup per kWaves (narrow) wave tiles of requests, at
@@ -576,6 +602,29 @@ int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float
   if (!latency && !regime && !share && !tenant_sums) return LLMV_OK;  // nothing requested
   return run_tiles(MODE_ATTR, trace, P, NoVars{}, n_tenants, tenant_sums != nullptr,
                    share != nullptr, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int llmv_attribute_noalloc(const llmv_trace* trace, const llmv_shape* shape,
+                           const float coeffs[20], float* latency, uint8_t* regime, float* share,
+                           int32_t n_tenants, double* tenant_sums, void* stream) {
+  Params P{};
+  int rc = attribute_params(trace, shape, coeffs, 20, latency, regime, share, n_tenants,
+                            tenant_sums, P);
+  if (rc) return rc;
+  for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[i];
+  if (!latency && !regime && !share && !tenant_sums) return LLMV_OK;  // nothing requested
+  const size_t need = layout(trace->n_requests, tenant_sums ? n_tenants : 0).total;
+  if (need > LLMV_NOALLOC_SCRATCH_BYTES)
+    return fail(LLMV_EINVAL,
+                "llmv_attribute_noalloc: this trace needs %zu bytes of scratch "
+                "(n_requests=%lld, n_tenants=%d); the static scratch holds %zu",
+                need, (long long)trace->n_requests, (int)n_tenants,
+                (size_t)LLMV_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc) return rc;
+  return run_tiles(MODE_ATTR, trace, P, NoVars{}, n_tenants, tenant_sums != nullptr,
+                   share != nullptr, ws, LLMV_NOALLOC_SCRATCH_BYTES, (hipStream_t)stream);
 }
 
 int llmv_shape_constants_ext(const llmv_shape* shape, double S[6]) {

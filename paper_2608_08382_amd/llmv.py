@@ -29,7 +29,7 @@ EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_sweep_workspace_
            "llmv_attribute_sweep_ext", "llmv_features", "llmv_tenant_sums", "llmv_validate",
            "llmv_batch_sums", "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit_workspace_size", "llmv_fit",
            "llmv_fit_metrics", "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
-           "llmv_attribute_ext",
+           "llmv_attribute_ext", "llmv_attribute_noalloc",
            "llmv_last_error", "llmv_set_kernel_events")
 
 
@@ -84,6 +84,7 @@ def load(path: str = LIB_PATH):
             lib.llmv_validate.argtypes = [P, i32, P, sz, P]
             lib.llmv_shape_constants_ext.argtypes = [P, P]
             lib.llmv_attribute_ext.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
+            lib.llmv_attribute_noalloc.argtypes = [P, P, P, P, P, P, i32, P, P]
             lib.llmv_fit_workspace_size.argtypes = [i64]
             lib.llmv_fit_workspace_size.restype = sz
             lib.llmv_fit.argtypes = [P, P, i64, P, P, P, i32, P, P, P, sz, P]
@@ -100,7 +101,7 @@ def load(path: str = LIB_PATH):
                       "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit",
                       "llmv_fit_metrics",
                       "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
-                      "llmv_attribute_ext"):
+                      "llmv_attribute_ext", "llmv_attribute_noalloc"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -190,6 +191,18 @@ def llmv_attribute(trace: DeviceTrace, shape, coeffs, latency=None, regime=None,
     _check(load().llmv_attribute(ctypes.byref(tr), _shape_ref(sh), co, _ptr(latency),
                                  _ptr(regime), _ptr(share), int(n_tenants), _ptr(tenant_sums),
                                  _ptr(ws), nbytes, _stream(stream)), "llmv_attribute")
+
+
+def llmv_attribute_noalloc(trace: DeviceTrace, shape, coeffs, latency=None, regime=None,
+                           share=None, n_tenants: int = 0, tenant_sums=None, stream=None):
+    """llmv_attribute without a workspace (the library's static scratch)."""
+    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    sh = make_shape(shape)
+    tr = trace.struct(with_tenant=tenant_sums is not None)
+    _check(load().llmv_attribute_noalloc(ctypes.byref(tr), _shape_ref(sh), co, _ptr(latency),
+                                         _ptr(regime), _ptr(share), int(n_tenants),
+                                         _ptr(tenant_sums), _stream(stream)),
+           "llmv_attribute_noalloc")
 
 
 def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out, ws=None,
