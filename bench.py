@@ -114,9 +114,10 @@ def calibration(hip, stream, dt, share, reps=5):
     plain coalesced kernels (libllmv_calib) reading the trace's own p, c and
     tenant arrays and writing the share array, over the same request count.
     For each access kind (read 12 B, write 4 B, read 12 B + write 4 B per
-    request) and each choice of plain or non-temporal loads and stores, the
-    best of a few launch shapes (grid, elements per thread) is reported, in
-    GB/s of bytes moved."""
+    request, the last also as wave tiles dealt round-robin) and each choice
+    of plain or non-temporal loads and stores, the best of a few launch
+    shapes (grid, elements per thread, tiles per chunk) is reported, in GB/s
+    of bytes moved."""
     import ctypes
     import torch
     from paper_2608_08382_amd import build as hipbuild
@@ -124,48 +125,56 @@ def calibration(hip, stream, dt, share, reps=5):
     lib = ctypes.CDLL(hipbuild.CALIB_OUT)
     P = ctypes.c_void_p
     lib.llmv_calib_stream.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                      P, P, P, P, ctypes.c_int64, P, P]
+                                      P, P, P, P, ctypes.c_int64, P, P, ctypes.c_int]
     lib.llmv_calib_stream.restype = ctypes.c_int
     n4 = dt.n_requests // 4
     sink = torch.zeros(4, dtype=torch.int32, device=share.device)
     cus = torch.cuda.get_device_properties(share.device).multi_processor_count
     ptrs = [P(x.data_ptr()) for x in (dt.p, dt.c, dt.tenant, share)]
 
-    def run(mode, flags, unroll, grid):
+    def run(mode, flags, unroll, grid, chunk):
         rc = lib.llmv_calib_stream(mode, flags, unroll, grid, *ptrs, n4, P(sink.data_ptr()),
-                                   P(stream))
+                                   P(stream), chunk)
         if rc != 0:
             raise RuntimeError("llmv_calib_stream failed")
 
-    kinds = {"read": (0, 12, (0, 1)), "write": (1, 4, (0, 2)), "mix_12r_4w": (2, 16, (0, 1, 2, 3))}
+    # kind: (mode, bytes per request, flag choices, launch shapes (unroll,
+    # workgroups per CU, chunk))
+    grid_stride = [(u, w, 1) for u in (1, 2, 4) for w in (4, 8)]
+    wave_tiles = [(2, 2, 2), (2, 4, 2), (4, 2, 1), (4, 2, 8), (7, 2, 1), (2, 2, 8)]
+    kinds = {"read": (0, 12, (0, 1), grid_stride), "write": (1, 4, (0, 2), grid_stride),
+             "mix_12r_4w": (2, 16, (0, 1, 2, 3), grid_stride),
+             "mix_12r_4w_wave_tiles": (3, 16, (0, 3), wave_tiles)}
     flag_names = {0: "plain", 1: "nt_loads", 2: "nt_stores", 3: "nt_loads_stores"}
     out = {}
-    for kind, (mode, bpr, flag_set) in kinds.items():
+    for kind, (mode, bpr, flag_set, shapes) in kinds.items():
         for flags in flag_set:
             best = None
-            for unroll in (1, 2, 4):
-                for per_cu in (4, 8):
-                    grid = cus * per_cu
-                    run(mode, flags, unroll, grid)
-                    torch.cuda.synchronize()
-                    ev = [(hip.create(), hip.create()) for _ in range(reps)]
-                    for a, b in ev:
-                        hip.record(a, stream)
-                        run(mode, flags, unroll, grid)
-                        hip.record(b, stream)
-                    torch.cuda.synchronize()
-                    ms = sorted(hip.elapsed_ms(a, b) for a, b in ev)[reps // 2]
-                    gbps = bpr * 4 * n4 / (ms / 1e3) / 1e9
-                    if best is None or gbps > best["gbps"]:
-                        best = {"gbps": gbps, "ms": ms, "unroll": unroll, "grid": grid}
+            for unroll, per_cu, chunk in shapes:
+                grid = cus * per_cu
+                run(mode, flags, unroll, grid, chunk)
+                torch.cuda.synchronize()
+                ev = [(hip.create(), hip.create()) for _ in range(reps)]
+                for a, b in ev:
+                    hip.record(a, stream)
+                    run(mode, flags, unroll, grid, chunk)
+                    hip.record(b, stream)
+                torch.cuda.synchronize()
+                ms = sorted(hip.elapsed_ms(a, b) for a, b in ev)[reps // 2]
+                gbps = bpr * 4 * n4 / (ms / 1e3) / 1e9
+                if best is None or gbps > best["gbps"]:
+                    best = {"gbps": gbps, "ms": ms, "unroll": unroll, "grid": grid, "chunk": chunk}
             name = f"{kind}_{flag_names[flags]}"
             out[name] = best
             log(f"[bench] calibration {name}: {best['gbps']:.0f} GB/s "
-                f"(grid {best['grid']}, {best['unroll']} per thread)")
+                f"(grid {best['grid']}, unroll {best['unroll']}, chunk {best['chunk']})")
     best_mix = max(v["gbps"] for k, v in out.items() if k.startswith("mix"))
+    best_grid_stride = max(v["gbps"] for k, v in out.items()
+                           if k.startswith("mix") and "wave_tiles" not in k)
     return {"unit": "GB/s", "bytes_per_request": {"read": 12, "write": 4, "mix_12r_4w": 16},
             "n_requests": 4 * n4, "kinds": out, "best_mix_gbps": best_mix,
-            "best_mix_frac_of_peak": best_mix / PEAK_HBM_GBPS}
+            "best_mix_frac_of_peak": best_mix / PEAK_HBM_GBPS,
+            "best_grid_stride_mix_gbps": best_grid_stride}
 
 
 def bench_configs(hip, stream, steps, with_oracle):
@@ -377,36 +386,23 @@ def bench_admission(hip, stream, dt, tr, coeffs, ws, with_oracle):
                         out["delta"][:1], out["share"][:1], out["regime"][:1])
         torch.cuda.synchronize()
         lat_q.append(time.perf_counter() - t0)
-    # one scheduler step: attribution of a single 256-request batch
-    st = tracegen_single_batch(256)
-    sdt = llmv.DeviceTrace.from_host(st.offsets, st.p, st.c, st.tenant)
-    s_out = llmv.attribute(sdt, tr.shape, coeffs, st.n_tenants)
-    sws = llmv.workspace(st.n_batches, st.n_requests, st.n_tenants)
-    lat_s = []
-    for _ in range(50):
-        t0 = time.perf_counter()
-        llmv.llmv_attribute(sdt, tr.shape, coeffs, s_out["latency"], s_out["regime"],
-                            s_out["share"], st.n_tenants, s_out["tenant_sums"], sws)
-        torch.cuda.synchronize()
-        lat_s.append(time.perf_counter() - t0)
-    # the same two calls on the GPU's clock (HIP events around each call)
+    # the same query on the GPU's clock (HIP events around the call)
     gq = timed(lambda: llmv.llmv_admit(sums, phase, tr.n_batches, tr.shape, coeffs, *one,
                                        out["t_after"][:1], out["delta"][:1], out["share"][:1],
                                        out["regime"][:1]), reps=21)
-    gs = timed(lambda: llmv.llmv_attribute(sdt, tr.shape, coeffs, s_out["latency"], s_out["regime"],
-                                           s_out["share"], st.n_tenants, s_out["tenant_sums"],
-                                           sws), reps=21)
     res = {"metric": "admission queries/sec", "value": m / (ms_admit / 1e3), "unit": "queries/s",
            "n_candidates": m, "admit_ms": ms_admit, "n_batches": tr.n_batches,
            "batch_sums_ms": ms_sums,
            "batch_sums_gbps": (8 * tr.n_requests + 41 * tr.n_batches) / (ms_sums / 1e3) / 1e9,
            "single_query_us": float(np.median(lat_q)) * 1e6,
-           "single_step_256_us": float(np.median(lat_s)) * 1e6,
-           "single_query_gpu_us": gq * 1e3, "single_step_256_gpu_us": gs * 1e3}
+           "single_query_gpu_us": gq * 1e3,
+           "single_step": bench_steps(hip, stream, tr.shape, coeffs, timed)}
+    s256 = res["single_step"]["256"]
+    res["single_step_256_us"] = s256["host_sync_us"]
+    res["single_step_256_gpu_us"] = s256["gpu_clock_us"]
     log(f"[bench] admission: batch sums {ms_sums:.3f} ms, {m} queries in {ms_admit:.3f} ms "
-        f"({res['value']:.3e}/s); one query {res['single_query_us']:.1f} us, one 256-request "
-        f"step {res['single_step_256_us']:.1f} us (host, synchronous); on the GPU's clock "
-        f"{res['single_query_gpu_us']:.1f} and {res['single_step_256_gpu_us']:.1f} us")
+        f"({res['value']:.3e}/s); one query {res['single_query_us']:.1f} us host-synchronous, "
+        f"{res['single_query_gpu_us']:.1f} us on the GPU's clock")
     # the same 2^20 queries under the extended model, from llmv_batch_sums_ext's state
     sums5 = torch.empty((5, tr.n_batches), dtype=torch.int64, device=dev)
     llmv.llmv_batch_sums_ext(dt, sums5, phase, ws)
@@ -662,6 +658,79 @@ def tracegen_single_batch(n):
     c = rng.integers(128, 8193, n).tolist()
     t = rng.integers(0, 16, n).tolist()
     return tracegen.from_batches([([1] * n, c)], [t], 16)
+
+
+def bench_steps(hip, stream, shape, coeffs, timed, sizes=(1, 64, 256, 1024)):
+    """One scheduler step (one decode batch of n requests, 16 tenants):
+    llmv_attribute's step kernel host-synchronous (launch to completion, the
+    median of 50 calls) and on the GPU's clock (HIP events around the call),
+    and the library's host attributor on the same step (median of 200
+    calls); the GPU outputs checked against the host attributor's."""
+    import numpy as np
+    import torch
+    from paper_2608_08382_amd import llmv
+
+    res = {}
+    for n in sizes:
+        st = tracegen_single_batch(n)
+        sdt = llmv.DeviceTrace.from_host(st.offsets, st.p, st.c, st.tenant)
+        o = llmv.attribute(sdt, shape, coeffs, st.n_tenants, ws=torch.empty(0, device="cuda"))
+
+        def call():
+            llmv.llmv_attribute(sdt, shape, coeffs, o["latency"], o["regime"], o["share"],
+                                st.n_tenants, o["tenant_sums"], None)
+
+        call()
+        torch.cuda.synchronize()
+        lat = []
+        for _ in range(50):
+            t0 = time.perf_counter()
+            call()
+            torch.cuda.synchronize()
+            lat.append(time.perf_counter() - t0)
+        g = timed(call, reps=21)
+        h = llmv.llmv_attribute_host(st.offsets, st.p, st.c, st.tenant, shape, coeffs,
+                                     st.n_tenants)
+        # the C entry point called directly (arguments built once: the time
+        # is the attribution plus one ctypes call)
+        hl = host_step_times(llmv, st, shape, coeffs, 200)
+        same = all(np.array_equal(o[k].cpu().numpy(), h[k]) for k in ("latency", "regime", "share"))
+        assert same, f"step of {n}: GPU and host attributor differ"
+        res[str(n)] = {"host_sync_us": float(np.median(lat)) * 1e6, "gpu_clock_us": g * 1e3,
+                       "host_attributor_us": float(np.median(hl)) * 1e6,
+                       "gpu_equals_host_attributor": same}
+        log(f"[bench] step of {n} requests: {res[str(n)]['host_sync_us']:.1f} us "
+            f"host-synchronous, {res[str(n)]['gpu_clock_us']:.1f} us on the GPU's clock; host "
+            f"attributor {res[str(n)]['host_attributor_us']:.1f} us")
+    return res
+
+
+def host_step_times(llmv, st, shape, coeffs, reps):
+    """Seconds per llmv_attribute_host call on one step's host arrays."""
+    import ctypes
+    import numpy as np
+    off = np.ascontiguousarray(st.offsets, np.int64)
+    p = np.ascontiguousarray(st.p, np.int32)
+    c = np.ascontiguousarray(st.c, np.int32)
+    t = np.ascontiguousarray(st.tenant, np.int32)
+    lat = np.zeros(st.n_batches, np.float32)
+    reg = np.zeros(st.n_batches, np.uint8)
+    share = np.zeros(st.n_requests, np.float32)
+    ts = np.zeros(st.n_tenants, np.float64)
+    ptr = [ctypes.c_void_p(a.ctypes.data) for a in (off, p, c, t, lat, reg, share, ts)]
+    tr = llmv.llmv_trace(st.n_batches, st.n_requests, *ptr[:4])
+    sh = llmv.make_shape(shape)
+    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    lib = llmv.load()
+    args = (ctypes.byref(tr), ctypes.byref(sh) if sh is not None else None, co, ptr[4], ptr[5],
+            ptr[6], int(st.n_tenants), ptr[7])
+    out = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        rc = lib.llmv_attribute_host(*args)
+        out.append(time.perf_counter() - t0)
+        assert rc == 0
+    return out
 
 
 def main():

@@ -132,11 +132,32 @@ size_t llmv_sweep_workspace_size_ext(int64_t n_batches, int64_t n_requests, int3
  * Per batch, the model and the share constants are evaluated in fp64 from
  * exact integer sums; the constants are rounded to fp32 and each share is
  * evaluated in fp32 (a few ulp); tenant sums add the fp32 shares in fp64.
- * Every output is independent of the others being requested. */
+ * Every output is independent of the others being requested.  A trace of
+ * one scheduling step (at most 4096 requests and 1024 batches, and at most
+ * 4096 tenants when tenant sums are requested) runs as one workgroup in one
+ * launch and does not touch the workspace (ws may then be NULL). */
 int llmv_attribute(const llmv_trace *trace, const llmv_shape *shape,
                    const float coeffs[20], float *latency, uint8_t *regime,
                    float *share, int32_t n_tenants, double *tenant_sums,
                    void *ws, size_t ws_bytes, void *stream);
+
+/* Attribution of one scheduling step on the host, for a scheduler that
+ * attributes each step as it is formed and cannot afford a device round trip
+ * (Sec. 1: admission control and accounting inside the serving loop;
+ * Sec. 2.1, last paragraph: the model runs once per step).  The outputs of
+ * llmv_attribute, computed by the CPU from HOST arrays: every pointer in
+ * trace, and latency, regime, share and tenant_sums, are host pointers (each
+ * output optional, as in llmv_attribute).  Batch sums are exact integers,
+ * the model and the share constants fp64 and the shares fp32 with the same
+ * operations as the GPU kernels, so latency, regime and shares equal the
+ * GPU's bit for bit; tenant sums add the shares in fp64 in request order.
+ * Unlike the device entry points it checks the data first (LLMV_ERANGE for
+ * data outside the limits, nothing written).  Synchronous, single-threaded,
+ * no device use.  For traces of one step (a few thousand requests); large
+ * traces belong on the GPU. */
+int llmv_attribute_host(const llmv_trace *trace, const llmv_shape *shape,
+                        const float coeffs[20], float *latency, uint8_t *regime,
+                        float *share, int32_t n_tenants, double *tenant_sums);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):

@@ -7,7 +7,7 @@ import subprocess
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SOURCES = [os.path.join(PKG, "csrc", "api.hip"), os.path.join(PKG, "csrc", "fit.hip")]
-DEPS = SOURCES + [os.path.join(PKG, "csrc", h) for h in ("kernels.hpp", "groups.hpp", "fit.hpp", "host.hpp")] + [
+DEPS = SOURCES + [os.path.join(PKG, "csrc", h) for h in ("kernels.hpp", "groups.hpp", "fit.hpp", "host.hpp", "model.hpp", "step.hpp")] + [
     os.path.join(ROOT, "include", "llmv.h")]
 OUT = os.path.join(PKG, "libllmv.so")
 # bandwidth calibration kernels (measurement context for the benchmark; not
@@ -21,6 +21,10 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # fp64 atomic adds as hardware instructions, not CAS loops
     "-munsafe-fp-atomics",
+    # products rounded before their adds (no contraction into fused
+    # multiply-adds), on the device and the host alike; the shares' fused
+    # multiply-adds are written out as fmaf
+    "-ffp-contract=off",
     "-Wall",
 ]
 

@@ -12,6 +12,8 @@
 #include "groups.hpp"
 #include "kernels.hpp"
 #include "llmv.h"
+#include "model.hpp"
+#include "step.hpp"
 
 namespace llmv {
 // Scratch of llmv_attribute_noalloc, one copy per device (see llmv.h).
@@ -261,6 +263,24 @@ template <> struct TilePick<ExtModel> {
     return share ? k_tiles<MODE_EXT, HIST_GLOBAL, true> : k_tiles<MODE_EXT, HIST_GLOBAL, false>;
   }
 };
+
+// One scheduler step (at most kStepN requests, kStepB batches and, with
+// tenant sums, kStepT tenants) runs in k_step: one workgroup, one launch.
+bool step_fits(const llmv_trace* tr, bool want_tenant, int32_t T) {
+  return tr->n_requests <= kStepN && tr->n_batches <= kStepB && (!want_tenant || T <= kStepT);
+}
+
+int run_step(const Params& P, bool want_tenant, hipStream_t stream) {
+  const size_t dyn = want_tenant ? (size_t)P.n_tenants * sizeof(double) : 0;
+  if (g_ev_before) HIP_TRY(hipEventRecord(g_ev_before, stream), "hipEventRecord");
+  if (want_tenant)
+    hipLaunchKernelGGL(k_step<true>, dim3(1), dim3(kStepWG), dyn, stream, P);
+  else
+    hipLaunchKernelGGL(k_step<false>, dim3(1), dim3(kStepWG), 0, stream, P);
+  HIP_TRY(hipGetLastError(), "k_step launch");
+  if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
+  return LLMV_OK;
+}
 
 // Partition + tiles (+ tenant reduction) shared by attribute and features.
 // V: the kernel's second argument (the extended model, or nothing).
@@ -550,6 +570,47 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   return LLMV_OK;
 }
 
+// The batches of llmv_attribute_host (data checked, tenant sums cleared):
+// exact sums, Eq. 1 (model.hpp), shares and tenant sums in request order.
+#define LLMV_HOST_BATCHES(NAME, ATTR)                                                          \
+  ATTR void NAME(const int64_t* off, const int32_t* p, const int32_t* c, const int32_t* t,     \
+                 int64_t nB, const double* th, const double* S, float* latency,                \
+                 uint8_t* regime, float* share, double* tenant_sums) {                         \
+    for (int64_t b = 0; b < nB; ++b) {                                                         \
+      const int64_t lo = off[b], hi = off[b + 1], n = hi - lo;                                 \
+      if (n == 0) {                                                                            \
+        if (latency) latency[b] = 0.0f;                                                        \
+        if (regime) regime[b] = 255;                                                           \
+        continue;                                                                              \
+      }                                                                                        \
+      uint64_t Ps = 0, Cs = 0, Qs = 0;                                                         \
+      bool zero_context = false;                                                               \
+      for (int64_t i = lo; i < hi; ++i) {                                                      \
+        const uint64_t pi = (uint32_t)p[i], ci = (uint32_t)c[i];                               \
+        Ps += pi;                                                                              \
+        Cs += ci;                                                                              \
+        Qs += pi * pi;                                                                         \
+        zero_context |= ci == 0;                                                               \
+      }                                                                                        \
+      /* decode iff every request processes one token over a nonzero context */                \
+      const bool prefill = zero_context || Ps != (uint64_t)n;                                  \
+      double tB, k[4];                                                                         \
+      const int reg = eq1_batch(th, S, n, Ps, Cs, Qs, prefill, &tB, k);                        \
+      if (latency) latency[b] = (float)tB;                                                     \
+      if (regime) regime[b] = (uint8_t)reg;                                                    \
+      if (!share && !tenant_sums) continue;                                                    \
+      const float K[4] = {(float)k[0], (float)k[1], (float)k[2], (float)k[3]};                 \
+      for (int64_t i = lo; i < hi; ++i) {                                                      \
+        const float sh = share_of(K, p[i], c[i]);                                              \
+        if (share) share[i] = sh;                                                              \
+        if (tenant_sums) tenant_sums[t[i]] += (double)sh;                                      \
+      }                                                                                        \
+    }                                                                                          \
+  }
+LLMV_HOST_BATCHES(host_batches, )
+LLMV_HOST_BATCHES(host_batches_fma, __attribute__((target("fma"))))
+#undef LLMV_HOST_BATCHES
+
 }  // namespace
 
 extern "C" {
@@ -600,6 +661,8 @@ int llmv_attribute(const llmv_trace* trace, const llmv_shape* shape, const float
   if (rc) return rc;
   for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[i];
   if (!latency && !regime && !share && !tenant_sums) return LLMV_OK;  // nothing requested
+  if (step_fits(trace, tenant_sums != nullptr, n_tenants))
+    return run_step(P, tenant_sums != nullptr, (hipStream_t)stream);
   return run_tiles(MODE_ATTR, trace, P, NoVars{}, n_tenants, tenant_sums != nullptr,
                    share != nullptr, ws, ws_bytes, (hipStream_t)stream);
 }
@@ -613,6 +676,8 @@ int llmv_attribute_noalloc(const llmv_trace* trace, const llmv_shape* shape,
   if (rc) return rc;
   for (int i = 0; i < 20; ++i) P.th[i] = (double)coeffs[i];
   if (!latency && !regime && !share && !tenant_sums) return LLMV_OK;  // nothing requested
+  if (step_fits(trace, tenant_sums != nullptr, n_tenants))  // no scratch needed
+    return run_step(P, tenant_sums != nullptr, (hipStream_t)stream);
   const size_t need = layout(trace->n_requests, tenant_sums ? n_tenants : 0).total;
   if (need > LLMV_NOALLOC_SCRATCH_BYTES)
     return fail(LLMV_EINVAL,
@@ -777,6 +842,54 @@ int llmv_tenant_sums(const int32_t* tenant, const float* share, int64_t n, int32
                        share, n, n_tenants, (double*)nullptr, tenant_sums);
     HIP_TRY(hipGetLastError(), "k_tenant_hist launch");
   }
+  return LLMV_OK;
+}
+
+int llmv_attribute_host(const llmv_trace* trace, const llmv_shape* shape, const float coeffs[20],
+                        float* latency, uint8_t* regime, float* share, int32_t n_tenants,
+                        double* tenant_sums) {
+  const bool want_tenant = tenant_sums != nullptr;
+  if (!trace) return fail(LLMV_EINVAL, "trace is NULL");
+  const int64_t nB = trace->n_batches, N = trace->n_requests;
+  if (nB < 0 || N < 0)
+    return fail(LLMV_EINVAL, "negative sizes (n_batches=%lld, n_requests=%lld)", (long long)nB,
+                (long long)N);
+  if (!trace->offsets) return fail(LLMV_EINVAL, "trace offsets is NULL");
+  if (N > 0 && (!trace->p || !trace->c)) return fail(LLMV_EINVAL, "trace p or c is NULL");
+  if (want_tenant && (n_tenants <= 0 || n_tenants > LLMV_TENANTS_MAX))
+    return fail(LLMV_EINVAL, "n_tenants=%d outside [1, 2^24]", n_tenants);
+  if (want_tenant && N > 0 && !trace->tenant)
+    return fail(LLMV_EINVAL, "tenant sums requested but trace tenant is NULL");
+  if (!coeffs) return fail(LLMV_EINVAL, "coeffs is NULL");
+  double th[20], S[4];
+  for (int i = 0; i < 20; ++i) {
+    if (!std::isfinite(coeffs[i])) return fail(LLMV_EINVAL, "coeffs[%d] is not finite", i);
+    th[i] = (double)coeffs[i];
+  }
+  int rc = shape_constants(shape, S);
+  if (rc) return rc;
+  // host data: checked before any output is written (a tenant id out of
+  // range would write out of bounds)
+  const int64_t* off = trace->offsets;
+  const int32_t *p = trace->p, *c = trace->c, *t = trace->tenant;
+  if (off[0] != 0 || off[nB] != N) return fail(LLMV_ERANGE, "offsets[0] != 0 or offsets[nB] != N");
+  for (int64_t b = 0; b < nB; ++b)
+    if (off[b + 1] < off[b] || off[b + 1] - off[b] > LLMV_BATCH_MAX)
+      return fail(LLMV_ERANGE, "batch %lld: size outside [0, 2^22]", (long long)b);
+  for (int64_t i = 0; i < N; ++i) {
+    if (p[i] < 1 || p[i] > LLMV_P_MAX || c[i] < 0)
+      return fail(LLMV_ERANGE, "request %lld: p or c outside the limits", (long long)i);
+    if (want_tenant && (t[i] < 0 || t[i] >= n_tenants))
+      return fail(LLMV_ERANGE, "request %lld: tenant outside [0, n_tenants)", (long long)i);
+  }
+  if (want_tenant)
+    for (int32_t u = 0; u < n_tenants; ++u) tenant_sums[u] = 0.0;
+  // the shares' fused multiply-adds in hardware where the CPU has them (the
+  // library function otherwise; both round once)
+  if (__builtin_cpu_supports("fma"))
+    host_batches_fma(off, p, c, t, nB, th, S, latency, regime, share, tenant_sums);
+  else
+    host_batches(off, p, c, t, nB, th, S, latency, regime, share, tenant_sums);
   return LLMV_OK;
 }
 

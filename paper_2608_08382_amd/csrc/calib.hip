@@ -13,6 +13,10 @@
 //   mode 0: read 12 B per element (three int32 arrays)
 //   mode 1: write 4 B per element (one fp32 array)
 //   mode 2: read 12 B and write 4 B per element (the attribution mix)
+//   mode 3: the mix in wave tiles: each wave loads a tile of 256*G elements
+//           of each input (group g: lane l takes elements 256g + 4l .. + 3),
+//           then stores it; tiles are dealt to waves round-robin in chunks
+//           of `chunk` tiles (G = unroll: 2, 4 or 7)
 //   flags bit 0: non-temporal loads; bit 1: non-temporal stores
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -70,6 +74,51 @@ __global__ __launch_bounds__(256) void k_stream(const v4i* __restrict__ a, const
   if (MODE == 0 && acc == 0x7fffffff) sink[0] = acc;
 }
 
+// Wave tiles of 256*G elements, chunks of `chunk` tiles dealt round-robin
+// over the waves; all loads of a tile are issued before its stores.
+template <bool NTL, bool NTS, int G>
+__global__ __launch_bounds__(256) void k_wave_tiles(const v4i* __restrict__ a,
+                                                    const v4i* __restrict__ b,
+                                                    const v4i* __restrict__ t,
+                                                    v4f* __restrict__ s, int64_t n4, int chunk) {
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * 4, w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t tile4 = 64 * G;
+  const int64_t ntiles = (n4 + tile4 - 1) / tile4;
+  const int64_t nchunks = (ntiles + chunk - 1) / chunk;
+  for (int64_t ch = w; ch < nchunks; ch += waves) {
+    for (int64_t k = ch * chunk; k < ch * chunk + chunk && k < ntiles; ++k) {
+      v4i x[G], y[G], z[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int64_t i = k * tile4 + 64 * g + lane;
+        x[g] = y[g] = z[g] = (v4i){0, 0, 0, 0};
+        if (i < n4) {
+          x[g] = ld<NTL>(a + i);
+          y[g] = ld<NTL>(b + i);
+          z[g] = ld<NTL>(t + i);
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int64_t i = k * tile4 + 64 * g + lane;
+        const v4i v = x[g] + y[g] + z[g];
+        if (i < n4) st<NTS>(s + i, (v4f){(float)v.x, (float)v.y, (float)v.z, (float)v.w});
+      }
+    }
+  }
+}
+
+template <int G>
+void* pick_tiles(int flags) {
+  switch (flags & 3) {
+    case 0: return (void*)k_wave_tiles<false, false, G>;
+    case 1: return (void*)k_wave_tiles<true, false, G>;
+    case 2: return (void*)k_wave_tiles<false, true, G>;
+    default: return (void*)k_wave_tiles<true, true, G>;
+  }
+}
+
 template <int MODE, int U>
 void* pick(int flags) {
   switch (flags & 3) {
@@ -95,14 +144,25 @@ extern "C" {
 // Runs one calibration kernel over n4 16-byte elements per array (the
 // caller's device buffers, 16-byte aligned; a, b, t are read, s written).
 // grid: workgroups of 256 threads.  unroll: 1, 2 or 4 elements per thread
-// per iteration.  Returns 0, or -1 on a bad argument or launch error.
+// per iteration (modes 0-2).  Returns 0, or -1 on a bad argument or launch
+// error.
+// mode 3 (wave tiles): unroll is G (2, 4 or 7) and chunk the tiles per chunk.
 int llmv_calib_stream(int mode, int flags, int unroll, int grid, const void* a, const void* b,
-                      const void* t, void* s, int64_t n4, void* sink, void* stream) {
-  if (mode < 0 || mode > 2 || grid < 1 || n4 < 0 || !sink) return -1;
-  if (unroll != 1 && unroll != 2 && unroll != 4) return -1;
+                      const void* t, void* s, int64_t n4, void* sink, void* stream, int chunk) {
+  if (mode < 0 || mode > 3 || grid < 1 || n4 < 0 || !sink) return -1;
   if (mode != 1 && (!a || !b || !t)) return -1;
   if (mode != 0 && !s) return -1;
   hipStream_t st = (hipStream_t)stream;
+  if (mode == 3) {
+    if (chunk < 1) return -1;
+    void* k = unroll == 2 ? pick_tiles<2>(flags)
+              : (unroll == 4 ? pick_tiles<4>(flags) : (unroll == 7 ? pick_tiles<7>(flags) : nullptr));
+    if (!k) return -1;
+    void* args[] = {(void*)&a, (void*)&b, (void*)&t, (void*)&s, (void*)&n4, (void*)&chunk};
+    if (hipLaunchKernel(k, dim3(grid), dim3(256), args, 0, st) != hipSuccess) return -1;
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+  }
+  if (unroll != 1 && unroll != 2 && unroll != 4) return -1;
   void* k = mode == 0 ? pick_u<0>(flags, unroll)
             : (mode == 1 ? pick_u<1>(flags, unroll) : pick_u<2>(flags, unroll));
   if (!k) return -1;

@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "model.hpp"
+
 namespace llmv {
 
 constexpr int kWG = 256;                     // threads per workgroup
@@ -179,16 +181,6 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
 
 // ------------------------------------------------------------- the model
 
-// Eq. 1 with one coefficient set, terms added in order k = 0..4.
-__device__ __forceinline__ double eq1(const double* th, const double X[5]) {
-  double acc = th[0] * X[0];
-  acc = acc + th[1] * X[1];
-  acc = acc + th[2] * X[2];
-  acc = acc + th[3] * X[3];
-  acc = acc + th[4] * X[4];
-  return acc;
-}
-
 // Per-batch evaluation from exact integer sums.  Writes the batch outputs
 // and the per-request share constants k[0..3]:
 //   share_i = k0 + k1*p_i + k2*c_i + k3*p_i^2,
@@ -215,20 +207,10 @@ __device__ __forceinline__ void batch_model(const Params& P, int64_t bg, int64_t
     k[1] = (double)n;
     return;
   }
-  const int phase = prefill ? 0 : 1;
-  const double* thm = P.th + (phase * 2 + 0) * 5;
-  const double* thc = P.th + (phase * 2 + 1) * 5;
-  const double tm = eq1(thm, X);
-  const double tc = eq1(thc, X);
-  // Roofline max of the two segments; ties stay memory-bound.
-  const int seg = (tc > tm) ? 1 : 0;
-  if (P.latency) P.latency[bg] = (float)(seg ? tc : tm);
-  if (P.regime) P.regime[bg] = (uint8_t)(2 * phase + seg);
-  const double* th = seg ? thc : thm;
-  k[0] = th[0] * (P.S[0] / (double)n) + th[4] * (double)n;
-  k[1] = th[1] * P.S[1];
-  k[2] = th[2] * P.S[2];
-  k[3] = th[3] * P.S[3];
+  double t;
+  const int regime = eq1_batch(P.th, P.S, n, Psum, Csum, Qsum, prefill, &t, k);
+  if (P.latency) P.latency[bg] = (float)t;
+  if (P.regime) P.regime[bg] = (uint8_t)regime;
 }
 
 // Eq. 1 plus the two extra terms, added in order k = 0..6.
@@ -263,12 +245,6 @@ __device__ __forceinline__ void ext_model(const Params& P, const ExtModel& E, in
   k[2] = th[2] * P.S[2];
   k[3] = th[3] * P.S[3];
   *k4 = th[5] * E.S5;
-}
-
-// fp32 share of one request from fp32 batch constants (as request_out).
-__device__ __forceinline__ float share_of(const float* k, int32_t p, int32_t c) {
-  const float pf = (float)p;
-  return fmaf(k[3], pf * pf, fmaf(k[2], (float)c, fmaf(k[1], pf, k[0])));
 }
 
 // MODE_SUMS: the exact sums of a nonempty batch and its phase.

@@ -29,7 +29,7 @@ EXPORTS = ("llmv_shape_constants", "llmv_workspace_size", "llmv_sweep_workspace_
            "llmv_attribute_sweep_ext", "llmv_features", "llmv_tenant_sums", "llmv_validate",
            "llmv_batch_sums", "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit_workspace_size", "llmv_fit",
            "llmv_fit_metrics", "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
-           "llmv_attribute_ext", "llmv_attribute_noalloc",
+           "llmv_attribute_ext", "llmv_attribute_noalloc", "llmv_attribute_host",
            "llmv_last_error", "llmv_set_kernel_events")
 
 
@@ -85,6 +85,7 @@ def load(path: str = LIB_PATH):
             lib.llmv_shape_constants_ext.argtypes = [P, P]
             lib.llmv_attribute_ext.argtypes = [P, P, P, P, P, P, i32, P, P, sz, P]
             lib.llmv_attribute_noalloc.argtypes = [P, P, P, P, P, P, i32, P, P]
+            lib.llmv_attribute_host.argtypes = [P, P, P, P, P, P, i32, P]
             lib.llmv_fit_workspace_size.argtypes = [i64]
             lib.llmv_fit_workspace_size.restype = sz
             lib.llmv_fit.argtypes = [P, P, i64, P, P, P, i32, P, P, P, sz, P]
@@ -101,7 +102,7 @@ def load(path: str = LIB_PATH):
                       "llmv_batch_sums_ext", "llmv_admit", "llmv_admit_ext", "llmv_fit",
                       "llmv_fit_metrics",
                       "llmv_fit_ext", "llmv_fit_metrics_ext", "llmv_shape_constants_ext",
-                      "llmv_attribute_ext", "llmv_attribute_noalloc"):
+                      "llmv_attribute_ext", "llmv_attribute_noalloc", "llmv_attribute_host"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -203,6 +204,41 @@ def llmv_attribute_noalloc(trace: DeviceTrace, shape, coeffs, latency=None, regi
                                          _ptr(regime), _ptr(share), int(n_tenants),
                                          _ptr(tenant_sums), _stream(stream)),
            "llmv_attribute_noalloc")
+
+
+def llmv_attribute_host(offsets, p, c, tenant, shape, coeffs, n_tenants: int = 0,
+                        outputs=("latency", "regime", "share", "tenant_sums")):
+    """llmv_attribute_host on host (numpy) arrays: returns the requested
+    outputs as numpy arrays.  The arrays are passed to the library as they
+    are (contiguous, converted to int64 / int32 first)."""
+    import numpy as np
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    pp = np.ascontiguousarray(p, dtype=np.int32)
+    cc = np.ascontiguousarray(c, dtype=np.int32)
+    want_t = "tenant_sums" in outputs
+    tt = np.ascontiguousarray(tenant, dtype=np.int32) if (want_t and tenant is not None) else None
+    nB, N = len(off) - 1, len(pp)
+
+    def hp(a):
+        return None if a is None or a.size == 0 else ctypes.c_void_p(a.ctypes.data)
+
+    tr = llmv_trace(nB, N, hp(off), hp(pp), hp(cc), hp(tt))
+    out = {}
+    if "latency" in outputs:
+        out["latency"] = np.zeros(nB, np.float32)
+    if "regime" in outputs:
+        out["regime"] = np.zeros(nB, np.uint8)
+    if "share" in outputs:
+        out["share"] = np.zeros(N, np.float32)
+    if want_t:
+        out["tenant_sums"] = np.zeros(int(n_tenants), np.float64)
+    co = (ctypes.c_float * 20)(*[float(v) for v in coeffs])
+    sh = make_shape(shape)
+    _check(load().llmv_attribute_host(ctypes.byref(tr), _shape_ref(sh), co,
+                                      hp(out.get("latency")), hp(out.get("regime")),
+                                      hp(out.get("share")), int(n_tenants),
+                                      hp(out.get("tenant_sums"))), "llmv_attribute_host")
+    return out
 
 
 def llmv_attribute_sweep(trace: DeviceTrace, shapes, coeffs, n_tenants: int, out, ws=None,
