@@ -181,9 +181,9 @@ def bench_configs(hip, stream, steps, with_oracle):
     """The attribution step on the other single-GPU workloads: the tiny mixed
     trace (1k batches; launch-bound, L2-resident, no roofline claim), the
     decode-only trace (1M batches, Qwen2.5-14B) and the chunked-prefill trace
-    (1M batches, Qwen2.5-32B).  Each step between HIP events, the tile
-    kernel between the library's own events, and, with the oracle, every
-    output checked."""
+    (1M batches, Qwen2.5-32B).  Each step between HIP events (the median
+    step), the tile kernel between the library's own events, and, with the
+    oracle, every output checked."""
     import numpy as np
     import torch
     import tracegen
@@ -207,16 +207,18 @@ def bench_configs(hip, stream, steps, with_oracle):
         for _ in range(3):
             step()
         torch.cuda.synchronize()
+        # each step between its own HIP events (GPU clock; a pause of the
+        # host between two enqueues is not counted), the median reported
         evs = [(hip.create(), hip.create()) for _ in range(steps)]
-        start, stop = hip.create(), hip.create()
-        hip.record(start, stream)
+        sevs = [(hip.create(), hip.create()) for _ in range(steps)]
         for i in range(steps):
+            hip.record(sevs[i][0], stream)
             llmv.llmv_set_kernel_events(*evs[i])
             step()
+            hip.record(sevs[i][1], stream)
         llmv.llmv_set_kernel_events(None, None)
-        hip.record(stop, stream)
         torch.cuda.synchronize()
-        ms = hip.elapsed_ms(start, stop) / steps
+        ms = sorted(hip.elapsed_ms(a, b) for a, b in sevs)[steps // 2]
         k_ms = sum(hip.elapsed_ms(a, b) for a, b in evs) / steps
         nbytes = algorithmic_bytes(tr.n_requests, tr.n_batches)
         gbps = nbytes / (k_ms / 1e3) / 1e9
@@ -650,6 +652,69 @@ def bench_many_tenants(hip, stream, dt, tr, coeffs, bufs, with_oracle, n_tenants
     return res
 
 
+def bench_big_batches(hip, stream, dt, tr, coeffs, ws, with_oracle, steps=5):
+    """Batches larger than a wave tile, on the heavy-tailed trace's own
+    request arrays cut into other batches: uniform batches of 1792 requests
+    (one full tile), of 1793 (one request past it: every batch is held whole
+    by a k_long wave), of 3585 and 16384 (streamed by a k_long wave), of
+    131072 (spread over the grid in segments), and 124 batches of 4M
+    requests (segments).  ms per
+    llmv_attribute step (HIP events), and with the oracle every batch's
+    latency and regime and every tenant sum checked."""
+    import numpy as np
+    import torch
+    from paper_2608_08382_amd import llmv
+
+    dev = dt.p.device
+    res = {}
+    cases = {"uniform_1792": (1792, tr.n_requests), "uniform_1793": (1793, tr.n_requests),
+             "uniform_3585": (3585, tr.n_requests), "uniform_16384": (16384, tr.n_requests),
+             "uniform_131072": (131072, tr.n_requests),
+             "124_x_4M": (4_000_000, 124 * 4_000_000)}
+    for name, (size, n) in cases.items():
+        off = np.arange(0, n, size, dtype=np.int64)
+        off = np.append(off, n)
+        bt = llmv.DeviceTrace(torch.as_tensor(off, device=dev), dt.p[:n], dt.c[:n],
+                              dt.tenant[:n])
+        nb = len(off) - 1
+        lat = torch.empty(nb, dtype=torch.float32, device=dev)
+        reg = torch.empty(nb, dtype=torch.uint8, device=dev)
+        share = torch.empty(n, dtype=torch.float32, device=dev)
+        tsum = torch.empty(tr.n_tenants, dtype=torch.float64, device=dev)
+        bws = llmv.workspace(nb, n, tr.n_tenants)
+
+        def step():
+            llmv.llmv_attribute(bt, tr.shape, coeffs, lat, reg, share, tr.n_tenants, tsum, bws)
+
+        step()
+        torch.cuda.synchronize()
+        ev = [(hip.create(), hip.create()) for _ in range(steps)]
+        for a, b in ev:
+            hip.record(a, stream)
+            step()
+            hip.record(b, stream)
+        torch.cuda.synchronize()
+        ms = sorted(hip.elapsed_ms(a, b) for a, b in ev)[steps // 2]
+        r = {"batch_size": size, "n_batches": nb, "n_requests": n, "ms_per_step": ms,
+             "value": n / (ms / 1e3), "unit": "requests/s"}
+        log(f"[bench] big batches {name}: {ms:.3f} ms/step ({nb} batches of {size})")
+        if with_oracle:
+            import oracle
+            sys.path.insert(0, os.path.join(ROOT, "tests"))
+            import parity
+            ref = oracle.attribute(off, tr.p[:n], tr.c[:n], tr.tenant[:n], tr.shape, coeffs,
+                                   tr.n_tenants, ("T", "TM", "TC", "phase", "regime",
+                                                  "tenant_sums"))
+            r["parity"] = parity.compare(ref, off, lat.cpu().numpy(), reg.cpu().numpy(), None,
+                                         tsum.cpu().numpy())
+        res[name] = r
+        del bt, lat, reg, share, tsum, bws
+        torch.cuda.empty_cache()
+    res["ratio_1793_over_1792"] = res["uniform_1793"]["ms_per_step"] / \
+        res["uniform_1792"]["ms_per_step"]
+    return res
+
+
 def tracegen_single_batch(n):
     """One decode batch of n requests (context U[128, 8192]), 16 tenants."""
     import numpy as np
@@ -755,6 +820,8 @@ def main():
                     help="skip the admission-query measurement")
     ap.add_argument("--no-calibration", action="store_true",
                     help="skip the STREAM-style bandwidth calibration")
+    ap.add_argument("--no-big", action="store_true",
+                    help="skip the batches-larger-than-a-tile measurement")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the tiny, decode-only and chunked-prefill workloads")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -898,6 +965,11 @@ def main():
     if not args.no_configs:
         # the heavy-tailed trace stays resident; the others come and go
         result["configs"] = bench_configs(hip, stream, args.steps, not args.no_cpu_baseline)
+    if not args.no_big:
+        result["big_batches"] = bench_big_batches(hip, stream, dt, tr, coeffs, ws,
+                                                  not args.no_cpu_baseline)
+        result["big_batches"]["ratio_4M_over_step"] = \
+            result["big_batches"]["124_x_4M"]["ms_per_step"] / ms_per_step
     if not args.no_ext:
         result["extended_model"] = bench_ext(hip, stream, dt, tr, (lat, reg, share, tsum), ws,
                                              max(5, args.steps // 2), not args.no_cpu_baseline)

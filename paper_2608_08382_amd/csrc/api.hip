@@ -111,7 +111,7 @@ SweepKernel<NC> pick_sweep(int g) {
 }
 
 struct Layout {
-  size_t wg_first, claims, partials, counts, hot, flag, total;
+  size_t wg_first, claims, partials, counts, hot, flag, big_list, big_seg, long_list, total;
 };
 
 // Chunks for `workers` wave workers over n requests, for wave tiles of `cap`
@@ -162,8 +162,8 @@ Layout layout(int64_t n, int32_t T, int rows = 1) {
   L.wg_first = o;  // first batch of each chunk (chunk_map's n_chunks + 1 at most)
   o += align_up((size_t)(n / piece(kCapNarrow) + grid * kWaves * (1 + kDynPerWorker) + 1) *
                 sizeof(int64_t));
-  L.claims = o;
-  o += align_up(sizeof(unsigned long long));
+  L.claims = o;  // the launch's counters
+  o += align_up(kCounters * sizeof(unsigned long long));
   L.partials = o;  // [grid][rows][T]
   if (lds_hist(T)) o += align_up((size_t)grid * (size_t)rows * (size_t)T * sizeof(double));
   L.counts = o;  // what-if sweep: requests per tenant, and the hot tenants
@@ -172,6 +172,14 @@ Layout layout(int64_t n, int32_t T, int rows = 1) {
   o += align_up(kHot * sizeof(int32_t));
   L.flag = o;
   o += align_up(sizeof(int));
+  // batches of more than kListMin requests, listed with their segments
+  const size_t n_list = (size_t)(n / (kListMin + 1)) + 1;
+  L.big_list = o;
+  o += align_up(n_list * sizeof(BigEntry));
+  L.big_seg = o;  // each listed batch of k requests: at most k / kBigSeg + 2 segments
+  o += align_up(((size_t)(n / kBigSeg) + 2 * n_list) * sizeof(uint64_t));
+  L.long_list = o;  // batches larger than a wave tile (each more than kCapNarrow - 3 requests)
+  o += align_up((size_t)(n / (kCapNarrow - 3) + 1) * sizeof(int64_t));
   L.total = o;
   return L;
 }
@@ -264,6 +272,31 @@ template <> struct TilePick<ExtModel> {
   }
 };
 
+// The long-batch kernel matching a tile kernel.
+template <typename VT> struct LongPick;
+template <> struct LongPick<NoVars> {
+  typedef void (*K)(const Params, const NoVars, int64_t);
+  static K get(int mode, int hist, bool share) {
+    if (mode == MODE_FEAT) return k_long<MODE_FEAT, HIST_NONE, false>;
+    if (mode == MODE_SUMS) return k_long<MODE_SUMS, HIST_NONE, false>;
+    if (hist == HIST_NONE)
+      return share ? k_long<MODE_ATTR, HIST_NONE, true> : k_long<MODE_ATTR, HIST_NONE, false>;
+    if (hist == HIST_LDS)
+      return share ? k_long<MODE_ATTR, HIST_LDS, true> : k_long<MODE_ATTR, HIST_LDS, false>;
+    return share ? k_long<MODE_ATTR, HIST_GLOBAL, true> : k_long<MODE_ATTR, HIST_GLOBAL, false>;
+  }
+};
+template <> struct LongPick<ExtModel> {
+  typedef void (*K)(const Params, const ExtModel, int64_t);
+  static K get(int, int hist, bool share) {
+    if (hist == HIST_NONE)
+      return share ? k_long<MODE_EXT, HIST_NONE, true> : k_long<MODE_EXT, HIST_NONE, false>;
+    if (hist == HIST_LDS)
+      return share ? k_long<MODE_EXT, HIST_LDS, true> : k_long<MODE_EXT, HIST_LDS, false>;
+    return share ? k_long<MODE_EXT, HIST_GLOBAL, true> : k_long<MODE_EXT, HIST_GLOBAL, false>;
+  }
+};
+
 // One scheduler step (at most kStepN requests, kStepB batches and, with
 // tenant sums, kStepT tenants) runs in k_step: one workgroup, one launch.
 bool step_fits(const llmv_trace* tr, bool want_tenant, int32_t T) {
@@ -299,13 +332,23 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   const size_t dyn = hist == HIST_LDS ? (size_t)rep * (size_t)T * sizeof(double)
                      : (hist == HIST_GLOBAL ? kCacheLds : 0);
   const auto kern = TilePick<VT>::get(mode, hist, want_share);
+  const auto klong = LongPick<VT>::get(mode, hist, want_share);
   P.hist_rep = rep;
+  char* base = (char*)ws;
+  // batches larger than a wave tile, listed for k_long
+  P.long_list = (int64_t*)(base + L.long_list);
+  P.long_count = (unsigned long long*)(base + L.claims) + kLongCounter;
+  P.big_list = nullptr;
+  P.big_seg = nullptr;
 
   const int64_t cap = tile_cap(mode, hist);
+  // a batch larger than a tile needs more than cap - 4 requests
+  const bool longs = tr->n_requests > cap - 4;
   if (tr->n_requests <= small_n(cap) && hist != HIST_GLOBAL) {
     // A small trace (one scheduler step, say) in one launch: one workgroup,
     // its waves split the batches by count (no chunk table), and the
-    // workgroup's tenant histogram is the result (no reduction).
+    // workgroup's tenant histogram is the result (no reduction); k_long
+    // follows with one workgroup if a batch can be larger than a tile.
     P.split_by_count = 1;
     P.n_chunks = kWaves;
     P.n_static = kWaves;
@@ -316,11 +359,14 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
     hipLaunchKernelGGL(kern, dim3(1), dim3(kWG), dyn, stream, P, V);
     HIP_TRY(hipGetLastError(), "k_tiles launch");
     if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
+    if (longs) {
+      hipLaunchKernelGGL(klong, dim3(1), dim3(kWG), dyn, stream, P, V, (int64_t)1);
+      HIP_TRY(hipGetLastError(), "k_long launch");
+    }
     return LLMV_OK;
   }
 
   const int64_t grid = grid_for(tr->n_requests, cus, blocks_per_cu(kern, dyn));
-  char* base = (char*)ws;
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   const int n_chunks = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
@@ -332,6 +378,11 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   P.n_chunks = cm.n_chunks;
   P.n_static = cm.n_static;
   P.partials = hist == HIST_LDS ? (double*)(base + L.partials) : nullptr;
+  // Eq. 1 attribution: batches of more than kListMin requests are listed
+  // for the segment kernels
+  const bool listed = mode == MODE_ATTR && tr->n_requests > kListMin;
+  P.big_list = listed ? (BigEntry*)(base + L.big_list) : nullptr;
+  P.big_seg = listed ? (uint64_t*)(base + L.big_seg) : nullptr;
 
   rc = partition(tr, cm, wg_first, P.claims, stream);
   if (rc) return rc;
@@ -345,6 +396,18 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, stream, P, V);
   HIP_TRY(hipGetLastError(), "k_tiles launch");
   if (g_ev_after) HIP_TRY(hipEventRecord(g_ev_after, stream), "hipEventRecord");
+
+  if (listed) {
+    // exact sums of the listed batches' segments
+    hipLaunchKernelGGL(k_big_sums, dim3(kBigGrid), dim3(kBigWG), 0, stream, P);
+    HIP_TRY(hipGetLastError(), "k_big_sums launch");
+  }
+  if (longs) {
+    // the long batches, then the listed batches' per-request outputs
+    const int64_t lgrid = grid_for(tr->n_requests, cus, blocks_per_cu(klong, dyn));
+    hipLaunchKernelGGL(klong, dim3((unsigned)lgrid), dim3(kWG), dyn, stream, P, V, grid);
+    HIP_TRY(hipGetLastError(), "k_long launch");
+  }
 
   if (hist == HIST_LDS) {
     hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)n_chunks), dim3(64 * kReduceWaves), 0, stream,

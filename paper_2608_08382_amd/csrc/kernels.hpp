@@ -18,7 +18,10 @@
 //    and its share written once.  Batch totals are lane-local run sums added
 //    into per-batch LDS accumulators; batch membership comes from an LDS
 //    bitmask of batch starts and popcounts.  A batch larger than a tile is
-//    handled by the wave in two passes.
+//    listed: for k_long, whose waves walk such batches one each (held whole
+//    in registers when it spans two tiles), or, under Eq. 1 attribution with
+//    more than kListMin requests, with its segments for k_big_sums and the
+//    segment part of k_long, which spread it over the whole grid.
 //  * Tenant sums accumulate in an fp64 LDS histogram per workgroup, flushed
 //    once to a [grid][n_tenants] partial array that k_tenant_reduce folds in
 //    a fixed order.
@@ -71,6 +74,16 @@ struct ChunkMap {
   }
 };
 
+// Counters of a launch (claims[]): the chunk claims of the tile kernel in
+// kClaimGroups groups (wave worker w claims the dynamic chunks n_static +
+// (w mod kClaimGroups) + k*kClaimGroups, k = 0, 1, ..., from counter w mod
+// kClaimGroups, so that claims spread over several addresses), the listed
+// batches with their segments, and the long batches.
+constexpr int kClaimGroups = 8;
+constexpr int kSegCounter = kClaimGroups;
+constexpr int kLongCounter = kClaimGroups + 1;
+constexpr int kCounters = kClaimGroups + 2;
+
 // MODE_ATTR: latency, regime, share, tenant sums of one (shape, theta).
 // MODE_FEAT: the feature rows.  MODE_EXT: the outputs of MODE_ATTR under the
 // extended model (Eq. 1 plus a cross term a5*S5*sum p*c and a per-request
@@ -100,6 +113,13 @@ __host__ __device__ constexpr int64_t tile_cap(int mode, int hist) {
   return 64 * (wide_tile(mode, hist) ? kVecWide : kVecNarrow);
 }
 
+// A batch listed for the segment kernels: its index and exact sums (sum p,
+// sum c, sum p^2, count of c == 0), accumulated by k_big_sums.
+struct BigEntry {
+  int64_t b;
+  unsigned long long s[4];
+};
+
 struct Params {
   const int64_t* off;
   const int32_t* p;
@@ -107,7 +127,7 @@ struct Params {
   const int32_t* tenant;
   int64_t nB, N;
   const int64_t* wg_first;  // [n_chunks+1] first batch of each chunk
-  unsigned long long* claims;  // chunk claim counter
+  unsigned long long* claims;  // the launch's counters (kCounters)
   uint64_t claim_base;      // counter value when this launch starts
   int64_t n_chunks;
   int64_t n_static;         // chunks taken statically, round-robin (>= the wave workers)
@@ -123,6 +143,17 @@ struct Params {
   int64_t* bsums;           // [4][nB] (|B|, sum p, sum c, sum p^2) (MODE_FEAT), with
                             // sum p*c as a fifth row (MODE_SUMS), or null
   uint8_t* bphase;          // [nB] phase, 255 for an empty batch (MODE_FEAT) or null
+  // MODE_ATTR, multi-workgroup launches: a batch of more than kListMin
+  // requests is not walked by the wave that meets it but listed, with its
+  // segments of kBigSeg requests, for k_big_sums and k_long (null: such a
+  // batch goes to the long list).  Both counts are in claims[kSegCounter]
+  // (cleared by k_partition).
+  struct BigEntry* big_list;  // listed batches and their exact sums
+  uint64_t* big_seg;          // segments: (list index << 32) | segment within the batch
+  // The other batches larger than a wave tile, listed by the wave that meets
+  // them for k_long (count at *long_count = claims[kLongCounter]).
+  int64_t* long_list;
+  unsigned long long* long_count;
   int32_t n_tenants;
   int32_t hist_rep;         // MODE_ATTR, HIST_LDS: histogram replicas (1, 2 or 4)
   double S[4];              // shape constants
@@ -381,7 +412,8 @@ __device__ __forceinline__ float request_out(const Params& P, const float* k, co
 // ------------------------------------------------------------ partition
 
 // wg_first[w] = first batch whose start offset is >= the start of chunk w
-// (w < n_chunks), wg_first[n_chunks] = nB; clears the claim counter.
+// (w < n_chunks), wg_first[n_chunks] = nB; clears the launch's counters
+// (claims[0 .. kCounters-1]).
 __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, const ChunkMap cm,
                             int64_t* __restrict__ wg_first, unsigned long long* claims) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -393,7 +425,7 @@ __global__ void k_partition(const int64_t* __restrict__ off, int64_t nB, const C
   }
   if (gid == 0) {
     wg_first[cm.n_chunks] = nB;
-    *claims = 0ull;
+    for (int i = 0; i < kCounters; ++i) claims[i] = 0ull;
   }
 }
 
@@ -439,7 +471,7 @@ struct TileShape {
 
 // Within one wave tile the sum of c and the count of c == 0 share a word:
 // a tile holds fewer than 2^16 requests, each c < 2^31, so sum c < 2^47
-// stays below the count's bits.  (big_batch keeps them apart: a batch
+// stays below the count's bits.  (long_batch keeps them apart: a batch
 // larger than a tile may reach 2^22 requests and sum c up to 2^53.)
 constexpr uint64_t kZeroUnit = 1ull << 48;      // count of c == 0, above the c sum
 constexpr uint64_t kCMask = kZeroUnit - 1;
@@ -478,6 +510,13 @@ __device__ __forceinline__ int64_t uni(int64_t v) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
   const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
   return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ float uni_f32(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+}
+__device__ __forceinline__ double uni_f64(double v) {
+  return __builtin_bit_cast(double, (uint64_t)uni((int64_t)__builtin_bit_cast(uint64_t, v)));
 }
 
 __device__ __forceinline__ uint64_t wave_sum(uint64_t x) {
@@ -536,6 +575,7 @@ __device__ __forceinline__ void store_round(const Params& P, float* stage, int64
   wave_lds_sync();
 #pragma unroll
   for (int g = 0; g < kVec / 4; ++g) {
+    if (256 * g >= L - s0) break;          // no slot of the round left (wave-uniform)
     const int32_t e = 256 * g + 4 * lane;  // slot within the round
     const int32_t x = s0 + e;              // slot within the tile
     const float* src = &stage[(e / kVec) * kStagePitch + (e % kVec)];
@@ -550,28 +590,82 @@ __device__ __forceinline__ void store_round(const Params& P, float* stage, int64
   wave_lds_sync();
 }
 
-// One batch too large for a wave tile: two passes over its requests by the
-// whole wave (the second pass mostly hits in L2).
+// Buffer resource over n int32 elements from base (both wave-uniform,
+// n < 2^29): a load of an element at or past n returns 0 and reads no
+// memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t elem_rsrc(const int32_t* base, int64_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(base), (short)0, (int)(n * 4),
+                                           0x00020000);
+}
+constexpr int kNT = 2;  // cache policy of a buffer access: streamed (non-temporal)
+template <int AUX = 0>
+__device__ __forceinline__ v4i load4(__amdgpu_buffer_rsrc_t r, int32_t elem) {
+  return (v4i)__builtin_amdgcn_raw_buffer_load_b128(r, 4 * elem, 0, AUX);
+}
+
+// Slots x .. x+VEC-1 (x = VEC * lane) of one round of a long batch: p, c
+// (and tenant) through buffers over the round's m slots, so that slots past
+// the batch read as 0 without a memory access.
+template <int VEC, bool TENANT>
+__device__ __forceinline__ void load_round(const Params& P, int64_t o, int64_t m, int32_t x,
+                                           int32_t* pv, int32_t* cv, int32_t* tv) {
+  const auto bp = elem_rsrc(P.p + o, m), bc = elem_rsrc(P.c + o, m);
+#pragma unroll
+  for (int g = 0; g < VEC / 4; ++g) {
+    const v4i a = load4(bp, x + 4 * g), d = load4(bc, x + 4 * g);
+    pv[4 * g] = a.x; pv[4 * g + 1] = a.y; pv[4 * g + 2] = a.z; pv[4 * g + 3] = a.w;
+    cv[4 * g] = d.x; cv[4 * g + 1] = d.y; cv[4 * g + 2] = d.z; cv[4 * g + 3] = d.w;
+  }
+  if (TENANT) {
+    const auto bt = elem_rsrc(P.tenant + o, m);
+#pragma unroll
+    for (int g = 0; g < VEC / 4; ++g) {
+      const v4i t = load4(bt, x + 4 * g);
+      tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
+    }
+  }
+}
+
+// One batch too large for a wave tile (k_long), walked by one wave in
+// rounds of kRoundSlots slots from ra (its first request rounded down to 4).
+// A batch of two rounds is held whole in registers: its requests are read
+// once, as in a tile.  A longer one keeps its first round in registers and
+// streams the others twice: for the exact sums, then for the per-request
+// outputs.  wk, wk4: the wave's LDS words for the batch constants.
 template <int MODE, int HIST, bool SHARE>
-__device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
-                          WaveLds<kVecOf<MODE, HIST>>& W, double* wk4, float* stage, int64_t bg,
-                          int64_t rs, int64_t re, double* s_hist) {
+__device__ __forceinline__ void long_batch(const Params& P, const typename VarsOf<MODE>::type& V, double* wk,
+                           double* wk4, float* stage, int64_t bg, int64_t rs, int64_t re,
+                           double* s_hist) {
   constexpr int VEC = kVecOf<MODE, HIST>;
   LLMV_TILE_CONSTANTS(VEC);
+  constexpr bool OUT = MODE != MODE_SUMS;  // per-request outputs
+  constexpr bool TEN = OUT && HIST != HIST_NONE;
+  constexpr bool STAGE = kAttrMode<MODE> && SHARE;
   const int lane = threadIdx.x & 63;
-  const int64_t ra = rs & ~(int64_t)3;
-  // Sums over up to 2^22 requests: sum c reaches 2^53, so the tile path's
-  // packed (sum c, zero count) word does not apply; a zero context is
-  // recorded as a flag of its own.
+  const int64_t ra = uni(rs & ~(int64_t)3);
+  const int32_t xf = uni((int32_t)(rs - ra));  // first slot of the batch
+  const int32_t L = uni((int32_t)(re - ra));   // slots up to its end (> kRoundSlots)
+  const int32_t nr = (L + kRoundSlots - 1) / kRoundSlots;  // rounds, at least 2
+  const int32_t x0 = lane * kVec;
+  // slots of round r: [r*kRoundSlots, min((r+1)*kRoundSlots, L)), from request o(r)
+  auto o_of = [&](int32_t r) { return ra + (int64_t)r * kRoundSlots; };
+  auto m_of = [&](int32_t r) { return (int64_t)min(kRoundSlots, L - r * kRoundSlots); };
+
+  // Sums over up to 2^22 requests: sum c reaches 2^53, so the tile's packed
+  // (sum c, zero count) word does not apply; a zero context is a flag.
   uint64_t sp = 0, sc = 0, sq = 0, sr = 0;
   bool zc = false;  // this lane saw a request with c == 0
-  int32_t pv[kVec], cv[kVec], tv[kVec];
-  for (int64_t base = ra; base < re; base += kRoundSlots) {
-    const int64_t x = base + lane * kVec;
-    load_slots<VEC, false>(P, x, pv, cv, tv);
+  // this lane's slots of round r that hold requests of the batch, as a bit mask
+  auto vmask = [&](int32_t r) {
+    const int32_t s = r * kRoundSlots + x0;
+    const int32_t a = max(xf - s, 0), z = min(L - s, kVec);
+    return z > a ? ((1u << (z - a)) - 1u) << a : 0u;
+  };
+  auto add = [&](const int32_t* pv, const int32_t* cv, int32_t r) {
+    const uint32_t v = vmask(r);
 #pragma unroll
     for (int q = 0; q < kVec; ++q) {
-      if (x + q >= rs && x + q < re) {
+      if ((v >> q) & 1u) {
         const uint32_t p = (uint32_t)pv[q], c = (uint32_t)cv[q];
         sp += p;
         sc += c;
@@ -580,48 +674,163 @@ __device__ void big_batch(const Params& P, const typename VarsOf<MODE>::type& V,
         if constexpr (kCrossSum<MODE>) sr += (uint64_t)p * c;
       }
     }
-  }
-  sp = wave_sum(sp);
-  sc = wave_sum(sc);
-  sq = wave_sum(sq);
-  if constexpr (kCrossSum<MODE>) sr = wave_sum(sr);
-  const int64_t n = re - rs;
-  // decode iff every request processes one token over a nonzero context
-  const bool prefill = (sp != (uint64_t)n) || (__ballot(zc) != 0);
-  if constexpr (MODE == MODE_SUMS) {
-    if (lane == 0) sums_out(P, bg, n, sp, sc, sq, sr, prefill);
-    return;
-  }
-  if (lane == 0) {
-    if constexpr (MODE == MODE_EXT)
-      ext_model(P, V, bg, n, sp, sc, sq, sr, prefill, W.k[0], wk4);
-    else
-      batch_model<MODE>(P, bg, n, sp, sc, sq, prefill, W.k[0]);
-  }
-  wave_lds_sync();
-  const double kd[4] = {W.k[0][0], W.k[0][1], W.k[0][2], W.k[0][3]};
-  const float k[5] = {(float)kd[0], (float)kd[1], (float)kd[2], (float)kd[3],
-                      MODE == MODE_EXT ? (float)wk4[0] : 0.0f};
-  for (int64_t base = ra; base < re; base += kRoundSlots) {
-    const int64_t x = base + lane * kVec;
-    load_slots<VEC, HIST != HIST_NONE>(P, x, pv, cv, tv);
+  };
+  // the batch model on lane 0; every lane gets the share constants
+  double kd[4] = {0.0, 0.0, 0.0, 0.0};
+  float k[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  auto model = [&]() {
+    sp = wave_sum(sp);
+    sc = wave_sum(sc);
+    sq = wave_sum(sq);
+    if constexpr (kCrossSum<MODE>) sr = wave_sum(sr);
+    const int64_t n = re - rs;
+    // decode iff every request processes one token over a nonzero context
+    const bool prefill = (sp != (uint64_t)n) || (__ballot(zc) != 0);
+    if (lane == 0) {
+      if constexpr (MODE == MODE_SUMS)
+        sums_out(P, bg, n, sp, sc, sq, sr, prefill);
+      else if constexpr (MODE == MODE_EXT)
+        ext_model(P, V, bg, n, sp, sc, sq, sr, prefill, wk, wk4);
+      else
+        batch_model<MODE>(P, bg, n, sp, sc, sq, prefill, wk);
+    }
+    if constexpr (OUT) {
+      // the constants are wave-uniform: held in scalar registers
+      wave_lds_sync();
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        kd[q] = uni_f64(wk[q]);
+        k[q] = uni_f32((float)kd[q]);
+      }
+      if constexpr (MODE == MODE_EXT) k[4] = uni_f32((float)wk4[0]);
+    }
+  };
+  auto out = [&](const int32_t* pv, const int32_t* cv, const int32_t* tv, int32_t r) {
+    const int32_t s = r * kRoundSlots + x0;
+    const uint32_t v = vmask(r);
+    const int32_t m = (int32_t)m_of(r);
 #pragma unroll
     for (int g = 0; g < kVec / 4; ++g) {
+      if (4 * g >= m) break;  // no lane holds a slot of this group (wave-uniform)
       float sv[4];
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq) {
         const int q = 4 * g + qq;
         sv[qq] = 0.0f;
-        if (x + q >= rs && x + q < re)
-          sv[qq] = request_out<MODE, HIST, SHARE>(P, k, kd, pv[q], cv[q], s_hist, tv[q], x + q);
+        if ((v >> q) & 1u)
+          sv[qq] = request_out<MODE, HIST, SHARE>(P, k, kd, pv[q], cv[q], s_hist, tv[q], ra + s + q);
       }
-      if (kAttrMode<MODE> && SHARE)
-        *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
+      if (STAGE) *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
     }
-    if (kAttrMode<MODE> && SHARE)
-      store_round<VEC>(P, stage, ra, (int32_t)(base - ra), (int32_t)(rs - ra), (int32_t)(re - ra));
+    if (STAGE) store_round<VEC>(P, stage, ra, r * kRoundSlots, xf, L);
+  };
+
+  int32_t p0[kVec], c0[kVec], t0[kVec];
+  load_round<VEC, TEN>(P, o_of(0), m_of(0), x0, p0, c0, t0);
+  if (nr == 2) {
+    int32_t p1[kVec], c1[kVec], t1[kVec];
+    load_round<VEC, TEN>(P, o_of(1), m_of(1), x0, p1, c1, t1);
+    add(p0, c0, 0);
+    add(p1, c1, 1);
+    model();
+    if constexpr (OUT) {
+      out(p0, c0, t0, 0);
+      out(p1, c1, t1, 1);
+    }
+  } else {
+    {
+      int32_t pa[kVec], ca[kVec], ta[kVec];
+      load_round<VEC, false>(P, o_of(1), m_of(1), x0, pa, ca, ta);
+      add(p0, c0, 0);
+      add(pa, ca, 1);
+    }
+#pragma unroll 1
+    for (int32_t r = 2; r < nr; ++r) {
+      int32_t pa[kVec], ca[kVec], ta[kVec];
+      load_round<VEC, false>(P, o_of(r), m_of(r), x0, pa, ca, ta);
+      add(pa, ca, r);
+    }
+    model();
+    if constexpr (OUT) {
+      out(p0, c0, t0, 0);
+#pragma unroll 1
+      for (int32_t r = 1; r < nr; ++r) {
+        int32_t pa[kVec], ca[kVec], ta[kVec];
+        load_round<VEC, TEN>(P, o_of(r), m_of(r), x0, pa, ca, ta);
+        out(pa, ca, ta, r);
+      }
+    }
   }
   wave_lds_sync();
+}
+
+// ------------------------------------------------------ long batches, listed
+
+constexpr int kBigWG = kWG;                             // threads per segment workgroup
+constexpr int kBigPer = 32;                             // requests per thread per pass
+constexpr int64_t kBigSub = (int64_t)kBigWG * kBigPer;  // requests per workgroup pass
+constexpr int64_t kBigSeg = 4 * kBigSub;                // requests per segment
+constexpr int kBigGrid = 512;                           // k_big_sums workgroups
+#ifndef LLMV_LIST_MIN
+#define LLMV_LIST_MIN (64 * 64 * kVecWide)
+#endif
+// Eq. 1 attribution spreads the batches of more than kListMin requests (64
+// wide tiles) over the grid in segments; shorter ones are walked by one
+// k_long wave each.
+constexpr int64_t kListMin = LLMV_LIST_MIN;
+static_assert(kListMin >= 64 * kVecWide, "a listed batch is larger than any wave tile");
+
+// The batches listed for the segment kernels and their segments share one
+// counter (claims[kSegCounter]): the batch count above bit kSegBits, the
+// segment count below.
+constexpr int kSegBits = 40;
+constexpr uint64_t kSegMask = (1ull << kSegBits) - 1;
+
+// Lists the batches b .. b+adv-1, each larger than a wave tile (lane j < adv
+// holds offsets[b+j] in wv, lane j+1 the batch's end).  Under Eq. 1
+// attribution with the segment lists set (SEG), those of more than kListMin
+// requests go to big_list with their segments (segment j of a batch holds
+// its requests in [ra + j*kBigSeg, ra + (j+1)*kBigSeg), ra = its first
+// request rounded down to 4; the entry's sums start at zero), with one
+// atomic for the run.  The others are appended to the wave's LDS buffer
+// lbuf (n_long entries, at most kLongBuf), flushed to the long list by
+// flush() when the run would not fit.
+constexpr int kLongBuf = 4 * kTileBatches;  // int64 entries in a wave's share-constant area
+template <bool SEG, typename F>
+__device__ __forceinline__ void list_run(const Params& P, int64_t b, int64_t wv, int32_t adv,
+                                         int64_t* lbuf, int32_t& n_long, F&& flush) {
+  const int lane = threadIdx.x & 63;
+  const int64_t rs = wv, re = __shfl(wv, min(lane + 1, 63), 64);
+  const bool in = lane < adv;
+  const bool big = SEG && in && P.big_list != nullptr && re - rs > kListMin;
+  const bool lng = in && !big;
+  const uint64_t below = (1ull << lane) - 1ull;
+  const uint64_t ml = __ballot(lng);
+  if (ml) {
+    const int32_t cnt = __builtin_popcountll(ml);
+    if (n_long + cnt > kLongBuf) flush();
+    if (lng) lbuf[n_long + __builtin_popcountll(ml & below)] = b + lane;
+    n_long += cnt;
+  }
+  if constexpr (SEG) {
+    const uint64_t mb = __ballot(big);
+    if (mb) {
+      const uint32_t q = big ? (uint32_t)((re - (rs & ~(int64_t)3) + kBigSeg - 1) / kBigSeg) : 0u;
+      const uint32_t qs = wave_incl_scan_u32(q);
+      const uint64_t Q = (uint32_t)__builtin_amdgcn_readlane((int)qs, 63);
+      unsigned long long at = 0;
+      if (lane == 0)
+        at = atomicAdd(P.claims + kSegCounter,
+                       ((unsigned long long)__builtin_popcountll(mb) << kSegBits) | Q);
+      at = readlane_u64(at, 0);
+      if (big) {
+        const uint64_t k = (at >> kSegBits) + __builtin_popcountll(mb & below);
+        P.big_list[k] = BigEntry{b + lane, {0ull, 0ull, 0ull, 0ull}};
+        const uint64_t first = (at & kSegMask) + qs - q;
+        for (uint32_t j = 0; j < q; ++j) P.big_seg[first + j] = (k << 32) | j;
+      }
+    }
+  }
 }
 
 // V: the extended model (MODE_EXT), an empty struct otherwise.  The LDS
@@ -656,6 +865,8 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
   if (HIST == HIST_LDS)
     for (int u = tid; u < n_hist; u += kWG) s_hist[u] = 0.0;
   if (HIST == HIST_GLOBAL) cache_init(s_hist);
+  // one workgroup, no k_partition: the count of listed batches starts here
+  if (P.split_by_count && tid == 0) atomicExch(P.long_count, 0ull);
   // this lane's replica of the histogram
   double* s_hist_lane = s_hist;
   if (HIST == HIST_LDS) s_hist_lane = s_hist + (lane & (P.hist_rep - 1)) * P.n_tenants;
@@ -676,16 +887,33 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
   auto window = [&](int64_t x0, int64_t x1) {
     return (x0 < x1 && lane <= min((int64_t)kTileBatches, x1 - x0)) ? P.off[x0 + lane] : (int64_t)0;
   };
-  // claim k of this launch names chunk n_static + k; past the last chunk, stop
+  // claim k of this worker's group cg names chunk n_static + cg + k*kClaimGroups;
+  // past the last chunk, stop
+  const int cg = (int)(((int64_t)blockIdx.x * kWaves + (tid >> 6)) % kClaimGroups);
   auto claimed_chunk = [&](unsigned long long cl) {
     const uint64_t k = readlane_u64((uint64_t)cl, 0) - P.claim_base;
-    return (dyn && k < (uint64_t)(P.n_chunks - P.n_static)) ? P.n_static + (int64_t)k : P.n_chunks;
+    if (!dyn || k >= (uint64_t)(P.n_chunks - P.n_static)) return P.n_chunks;
+    const uint64_t c = (uint64_t)P.n_static + (uint64_t)cg + k * (uint64_t)kClaimGroups;
+    return c < (uint64_t)P.n_chunks ? (int64_t)c : P.n_chunks;
   };
   auto claim_next = [&](int64_t ch) {
     unsigned long long cl = ~0ull;
     if (dyn && ch < P.n_chunks && ch + workers >= P.n_static && lane == 0)
-      cl = atomicAdd(P.claims, 1ull);
+      cl = atomicAdd(P.claims + cg, 1ull);
     return cl;
+  };
+  // batches larger than a tile, buffered in the wave's share-constant area
+  // (free between tiles) and flushed to the long list with one atomic
+  int64_t* lbuf = (int64_t*)&W.k[0][0];
+  int32_t n_long = 0;
+  auto flush_long = [&]() {
+    unsigned long long at = 0;
+    if (lane == 0) at = atomicAdd(P.long_count, (unsigned long long)n_long);
+    at = readlane_u64(at, 0);
+    wave_lds_sync();
+    for (int32_t i = lane; i < n_long; i += 64) P.long_list[at + i] = lbuf[i];
+    wave_lds_sync();
+    n_long = 0;
   };
   int64_t chunk = (int64_t)blockIdx.x * kWaves + (tid >> 6);
   int64_t cb0 = 0, cb1 = 0, cwv = 0;  // the chunk's batch range and first window
@@ -717,7 +945,14 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
       const int64_t rel = wv - ra;
       const uint64_t fits = __ballot(lane >= 1 && lane <= lim && rel <= kTile);
       const int32_t count = uni((int32_t)__builtin_popcountll(fits));  // a prefix of lanes
-      const int32_t adv = count > 0 ? count : 1;  // batches consumed by this step
+      // batches consumed by this step: the tile's, or (count == 0) the run of
+      // batches from b each larger than a tile (lane j < lim: batch b+j)
+      int32_t adv = count;
+      if (count == 0) {
+        const int64_t end = __shfl(wv, min(lane + 1, 63), 64);
+        const uint64_t alone = __ballot(lane < lim && end - (wv & ~(int64_t)3) > kTile);
+        adv = uni((int32_t)__builtin_ctzll(~alone));  // at least 1: batch b is one
+      }
       const int64_t e = b + adv;
       const int64_t r1 = uni(readlane_i64(wv, adv));
 
@@ -731,8 +966,12 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
       }
 
       if (count == 0) {
-        big_batch<MODE, HIST, SHARE>(P, V, W, W_k4, stage, b, r0, r1, s_hist_lane);
+        // batches b .. e-1, each larger than a tile: listed for k_long, or
+        // (Eq. 1 attribution, more than kListMin requests) with their
+        // segments for k_big_sums and k_long
+        list_run<MODE == MODE_ATTR>(P, b, wv, adv, lbuf, n_long, flush_long);
       } else {
+        if (n_long) flush_long();  // the tile needs the share-constant area
         const int32_t lo = (int32_t)min(rel, (int64_t)kTile + 1);  // batch start, rel. to ra
         const int32_t lo_next = __shfl_down(lo, 1, 64);
         const int32_t L = (int32_t)(r1 - ra);
@@ -899,6 +1138,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
     cwv = nwin;
     claim = claim_next(chunk);
   }
+  if (n_long) flush_long();
 
   if (HIST == HIST_LDS) {
     // fold the replicas in a fixed order
@@ -1003,6 +1243,200 @@ __global__ __launch_bounds__(kWG) void k_admit(const int64_t* __restrict__ sums,
 __global__ void k_zero_u64(unsigned long long* __restrict__ x, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) x[i] = 0ull;
+}
+
+// ------------------------------------------------------ listed batches
+
+// Exact sums of the listed batches: workgroup w takes segments w, w +
+// gridDim.x, ..., sums its requests of each in passes of kBigSub, and adds
+// the totals into the batch's entry with four 64-bit atomics (integer sums:
+// the order of the adds does not change them).
+__global__ __launch_bounds__(kBigWG) void k_big_sums(const Params P) {
+  __shared__ unsigned long long s_red[kBigWG / 64][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t n_seg = *(volatile unsigned long long*)(P.claims + kSegCounter) & kSegMask;
+  for (uint64_t g = blockIdx.x; g < n_seg; g += gridDim.x) {
+    const uint64_t e = P.big_seg[g];
+    BigEntry* E = P.big_list + (e >> 32);
+    const int64_t b = E->b;
+    const int64_t rs = P.off[b], re = P.off[b + 1];
+    const int64_t lo = (rs & ~(int64_t)3) + (int64_t)(uint32_t)e * kBigSeg;
+    const int64_t hi = min(lo + kBigSeg, re);
+    uint64_t sp = 0, sc = 0, sq = 0, nz = 0;
+    for (int64_t base = lo; base < hi; base += kBigSub) {
+      const int64_t m = min(kBigSub, hi - base);
+      const auto bp = elem_rsrc(P.p + base, m), bc = elem_rsrc(P.c + base, m);
+      v4i pv[kBigPer / 4], cv[kBigPer / 4];
+#pragma unroll
+      for (int u = 0; u < kBigPer / 4; ++u) {
+        pv[u] = load4<kNT>(bp, 4 * (tid + kBigWG * u));
+        cv[u] = load4<kNT>(bc, 4 * (tid + kBigWG * u));
+      }
+#pragma unroll
+      for (int u = 0; u < kBigPer / 4; ++u) {
+        const int64_t i0 = base + 4 * (tid + kBigWG * u);
+        const int32_t pa[4] = {pv[u].x, pv[u].y, pv[u].z, pv[u].w};
+        const int32_t ca[4] = {cv[u].x, cv[u].y, cv[u].z, cv[u].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (i0 + j >= rs && i0 + j < hi) {
+            const uint32_t p = (uint32_t)pa[j], c = (uint32_t)ca[j];
+            sp += p;
+            sc += c;
+            sq += (uint64_t)p * p;
+            nz += c == 0 ? 1u : 0u;
+          }
+        }
+      }
+    }
+    sp = wave_sum(sp);
+    sc = wave_sum(sc);
+    sq = wave_sum(sq);
+    nz = wave_sum(nz);
+    if (lane == 0) {
+      s_red[wave][0] = sp;
+      s_red[wave][1] = sc;
+      s_red[wave][2] = sq;
+      s_red[wave][3] = nz;
+    }
+    __syncthreads();
+    if (tid < 4) {
+      unsigned long long v = 0;
+      for (int w = 0; w < kBigWG / 64; ++w) v += s_red[w][tid];
+      if (v) atomicAdd(&E->s[tid], v);
+    }
+    __syncthreads();  // s_red is rewritten for the next segment
+  }
+}
+
+// The batches larger than a wave tile.  Each wave of a workgroup takes
+// entries of the long list in turn (long_batch); then, under Eq. 1
+// attribution, workgroup w takes segments w, w + gridDim.x, ... of the
+// batches listed for k_big_sums: thread 0 evaluates the batch model from the
+// entry's sums (the workgroup of segment 0 writes the latency and regime),
+// and the segment's shares are written and added to the tenant histogram.
+// HIST_LDS: at the end the workgroup adds its histogram into row (w mod
+// rows) of the tile kernel's partials (written before this launch);
+// HIST_GLOBAL: its tenant cache is flushed into the output.
+// Two workgroups per compute unit: a batch of two tiles held whole fits in
+// 256 VGPRs.
+template <int MODE, int HIST, bool SHARE>
+__global__ __launch_bounds__(kWG, 2) void k_long(const Params P, const typename VarsOf<MODE>::type V,
+                                              int64_t rows) {
+  constexpr int VEC = kVecOf<MODE, HIST>;
+  LLMV_TILE_CONSTANTS(VEC);
+  constexpr bool STAGE = kAttrMode<MODE> && SHARE;
+  constexpr bool TEN = HIST != HIST_NONE;
+  extern __shared__ double s_hist[];  // HIST_LDS: [hist_rep][n_tenants]; HIST_GLOBAL: the cache
+  __shared__ double s_k[kWaves][4];
+  __shared__ double s_k4[kWaves];
+  __shared__ float s_stage[STAGE ? kWaves * 64 * kStagePitch : 1];
+  __shared__ float s_K[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t n_long = *(volatile unsigned long long*)P.long_count;
+  uint64_t n_seg = 0;
+  if (MODE == MODE_ATTR && P.big_list)
+    n_seg = *(volatile unsigned long long*)(P.claims + kSegCounter) & kSegMask;
+  if ((uint64_t)blockIdx.x * kWaves >= n_long && blockIdx.x >= n_seg) return;  // nothing here
+  const int32_t T = P.n_tenants;
+  if (HIST == HIST_LDS)
+    for (int u = tid; u < P.hist_rep * T; u += kWG) s_hist[u] = 0.0;
+  if (HIST == HIST_GLOBAL) cache_init(s_hist);
+  double* s_hist_lane = s_hist;
+  if (HIST == HIST_LDS) s_hist_lane = s_hist + (lane & (P.hist_rep - 1)) * T;
+  __syncthreads();
+
+  float* stage = s_stage + (STAGE ? wave * 64 * kStagePitch : 0);
+  for (uint64_t k = (uint64_t)blockIdx.x * kWaves + wave; k < n_long;
+       k += (uint64_t)gridDim.x * kWaves) {
+    const int64_t b = uni(P.long_list[k]);
+    const int64_t rs = uni(P.off[b]), re = uni(P.off[b + 1]);
+    long_batch<MODE, HIST, SHARE>(P, V, s_k[wave], &s_k4[wave], stage, b, rs, re, s_hist_lane);
+  }
+
+  if constexpr (MODE == MODE_ATTR) {
+    for (uint64_t g = blockIdx.x; g < n_seg; g += gridDim.x) {
+      __syncthreads();  // s_K is free (every wave is past its last use)
+      const uint64_t e = P.big_seg[g];
+      const BigEntry* E = P.big_list + (e >> 32);
+      const int64_t b = E->b;
+      const int64_t rs = P.off[b], re = P.off[b + 1];
+      const int64_t lo = (rs & ~(int64_t)3) + (int64_t)(uint32_t)e * kBigSeg;
+      const int64_t hi = min(lo + kBigSeg, re);
+      if (tid == 0) {
+        const int64_t n = re - rs;
+        const uint64_t Ps = E->s[0], Cs = E->s[1], Qs = E->s[2], Zs = E->s[3];
+        // decode iff every request processes one token over a nonzero context
+        const bool prefill = (Ps != (uint64_t)n) || (Zs != 0);
+        double kd[4];
+        if ((uint32_t)e == 0) {
+          batch_model<MODE_ATTR>(P, b, n, Ps, Cs, Qs, prefill, kd);
+        } else {
+          double t;
+          eq1_batch(P.th, P.S, n, Ps, Cs, Qs, prefill, &t, kd);
+        }
+        for (int q = 0; q < 4; ++q) s_K[q] = (float)kd[q];
+      }
+      __syncthreads();
+      if (!SHARE && !TEN) continue;
+      const float K[4] = {s_K[0], s_K[1], s_K[2], s_K[3]};
+      for (int64_t base = lo; base < hi; base += kBigSub) {
+        const int64_t m = min(kBigSub, hi - base);
+        const auto bp = elem_rsrc(P.p + base, m), bc = elem_rsrc(P.c + base, m);
+        const auto bt = elem_rsrc(TEN ? P.tenant + base : P.p + base, m);
+        v4i pv[kBigPer / 4], cv[kBigPer / 4], tv[kBigPer / 4];
+#pragma unroll
+        for (int u = 0; u < kBigPer / 4; ++u) {
+          pv[u] = load4<kNT>(bp, 4 * (tid + kBigWG * u));
+          cv[u] = load4<kNT>(bc, 4 * (tid + kBigWG * u));
+          if (TEN) tv[u] = load4<kNT>(bt, 4 * (tid + kBigWG * u));
+        }
+#pragma unroll
+        for (int u = 0; u < kBigPer / 4; ++u) {
+          const int64_t i0 = base + 4 * (tid + kBigWG * u);
+          const int32_t pa[4] = {pv[u].x, pv[u].y, pv[u].z, pv[u].w};
+          const int32_t ca[4] = {cv[u].x, cv[u].y, cv[u].z, cv[u].w};
+          const int32_t ta[4] = {TEN ? tv[u].x : 0, TEN ? tv[u].y : 0, TEN ? tv[u].z : 0,
+                                 TEN ? tv[u].w : 0};
+          float sv[4];
+          uint32_t valid = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            sv[j] = 0.0f;
+            if (i0 + j >= rs && i0 + j < hi) {
+              valid |= 1u << j;
+              sv[j] = share_of(K, pa[j], ca[j]);
+              if (HIST == HIST_LDS) atomicAdd(s_hist_lane + ta[j], (double)sv[j]);
+              if (HIST == HIST_GLOBAL) cache_add(s_hist, ta[j], (double)sv[j], P.tenant_sums);
+            }
+          }
+          if (SHARE) {
+            if (valid == 0xFu) {
+              __builtin_nontemporal_store((v4f){sv[0], sv[1], sv[2], sv[3]}, (v4f*)(P.share + i0));
+            } else {
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                if ((valid >> j) & 1u) P.share[i0 + j] = sv[j];
+            }
+          }
+        }
+      }
+    }
+  }
+
+  if (HIST == HIST_LDS) {
+    // the replicas folded, the nonzero entries added with fp64 atomics
+    __syncthreads();
+    double* row = P.partials + (int64_t)(blockIdx.x % rows) * T;
+    for (int u = tid; u < T; u += kWG) {
+      double acc = s_hist[u];
+      for (int r = 1; r < P.hist_rep; ++r) acc += s_hist[r * T + u];
+      if (acc != 0.0) unsafeAtomicAdd(row + u, acc);
+    }
+  } else if (HIST == HIST_GLOBAL) {
+    __syncthreads();
+    cache_flush(s_hist, P.tenant_sums);
+  }
 }
 
 // ------------------------------------------------------ tenant reductions

@@ -180,3 +180,99 @@ def test_big_batch_sweep(L, ext):
                        ("tenant_sums",))["tenant_sums"]
             e = parity.rel_err(out[s, v], ref)
             assert e.max() <= parity.RTOL, (ext, s, v, e.max())
+
+
+def long_trace(case, n_tenants):
+    """Batches larger than a wave tile between ordinary ones: p, c of decode
+    batches (p = 1, c > 0) and prefill batches (c = 0), random tenants."""
+    rng = np.random.default_rng(sum(map(ord, case)) + n_tenants)
+    if case == "many-just-over":      # two tiles each: held whole by a k_long wave
+        sizes = rng.choice([1790, 1791, 1792, 1793, 1794, 1795, 1796, 1537, 2000, 3], 700)
+    elif case == "mixed-sizes":       # two tiles, several tiles, listed with segments
+        sizes = np.concatenate([rng.integers(1, 300, 300), rng.integers(1793, 40000, 60)])
+        rng.shuffle(sizes)
+    elif case == "huge-and-small":    # segments over the whole grid
+        sizes = np.array([5, 3_000_000, 1, 0, 17, 1_000_001, 2] + list(rng.integers(0, 200, 100)))
+    elif case == "listed-runs":       # runs of listed batches next to runs of k_long ones
+        sizes = np.concatenate([rng.integers(114_689, 200_000, 12), rng.integers(1793, 114_688, 12),
+                                rng.integers(0, 100, 40), [114_688, 114_689, 114_690]])
+        sizes = np.concatenate([sizes[:20], np.sort(sizes[20:])])
+    elif case == "small-trace":       # one workgroup for the tiles, then k_long
+        sizes = np.array([3, 5000, 7, 2500, 1, 0, 1793, 2])
+    else:
+        raise KeyError(case)
+    sizes = np.asarray(sizes, np.int64)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    p = np.ones(N, np.int32)
+    c = rng.integers(1, 1 << 17, N).astype(np.int32)
+    for b in np.nonzero(rng.random(len(sizes)) < 0.4)[0]:
+        p[off[b]:off[b + 1]] = rng.integers(1, 3000, sizes[b])
+        c[off[b]:off[b + 1]] = 0
+    t = rng.integers(0, n_tenants, N).astype(np.int32)
+    return tracegen.Trace(off, p, c, t, n_tenants, None)
+
+
+@pytest.mark.parametrize("case", ["many-just-over", "mixed-sizes", "huge-and-small", "listed-runs",
+                                  "small-trace"])
+@pytest.mark.parametrize("n_tenants", [7, 5000])
+def test_long_batches(L, case, n_tenants):
+    """Eq. 1 attribution of batches larger than a wave tile: listed by the
+    tile kernel for k_long (one wave each, held whole over two tiles,
+    streamed beyond) or, above 64 wide tiles (114,688 requests), with their
+    segments for the whole grid; more of them than the grid has waves, and
+    more in a row than a wave buffers; the LDS histogram (7 tenants) and the
+    tenant cache (5000); every output against the oracle, and output
+    subsets agreeing with the full call."""
+    import torch
+    tr = long_trace(case, n_tenants)
+    off, p, c, t = tr.offsets, tr.p, tr.c, tr.tenant
+    say(f"[big] long {case} T={n_tenants}: nB={tr.n_batches} N={tr.n_requests}")
+    dt = L.DeviceTrace.from_host(off, p, c, t)
+    shape = tracegen.SHAPES["llama3.1-8b"]
+    co = tracegen.config_coeffs("heavy-tailed")
+    out = L.attribute(dt, shape, co, n_tenants)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.attribute(off, p, c, t, shape, co, n_tenants)
+    st = parity.compare(ref, off, g["latency"], g["regime"], g["share"], g["tenant_sums"])
+    say(f"[big] {st}")
+    for outs in (("latency", "regime"), ("share",), ("tenant_sums",)):
+        part = L.attribute(dt, shape, co, n_tenants, outs)
+        torch.cuda.synchronize()
+        for k in outs:
+            if k == "tenant_sums":
+                np.testing.assert_allclose(part[k].cpu().numpy(), g[k], rtol=1e-12)
+            else:
+                assert np.array_equal(part[k].cpu().numpy(), g[k]), (outs, k)
+
+
+@pytest.mark.parametrize("case", ["many-just-over", "mixed-sizes", "small-trace"])
+def test_long_batches_other_modes(L, case):
+    """The feature rows, the exact batch sums and the extended model over
+    batches larger than a wave tile (k_long's waves for every size)."""
+    import torch
+    tr = long_trace(case, 11)
+    off, p, c, t = tr.offsets, tr.p, tr.c, tr.tenant
+    say(f"[big] long modes {case}: nB={tr.n_batches} N={tr.n_requests}")
+    dt = L.DeviceTrace.from_host(off, p, c, t)
+    shape = tracegen.SHAPES["qwen2.5-14b"]
+    xr, xb = L.features(dt, shape)
+    torch.cuda.synchronize()
+    rr, rb = oracle.features(off, p, c, shape)
+    assert parity.rel_err(xr.cpu().numpy(), rr).max() <= parity.RTOL
+    assert parity.rel_err(xb.cpu().numpy(), rb).max() <= 1e-12
+    for ext in (False, True):
+        sums, phase = L.batch_sums(dt, ext=ext)
+        torch.cuda.synchronize()
+        want_s, want_p = (oracle.batch_sums_ext if ext else oracle.batch_sums)(off, p, c)[:2]
+        assert np.array_equal(sums.cpu().numpy(), want_s), ext
+        assert np.array_equal(phase.cpu().numpy(), want_p), ext
+    co = tracegen.ext_coeffs(105)
+    out = L.attribute_ext(dt, shape, co, 11,
+                          ws=L.workspace(tr.n_batches, tr.n_requests, 11))
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.attribute_ext(off, p, c, t, shape, co, 11)
+    st = parity.compare(ref, off, g["latency"], g["regime"], g["share"], g["tenant_sums"])
+    say(f"[big] ext {case}: {st}")

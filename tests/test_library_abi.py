@@ -260,14 +260,19 @@ def test_sweep_workspace_size(llmv):
     """The sweep's workspace: the common one (with a tenant histogram per
     setting of a pass) plus 20 bytes per request for the (batch, tenant)
     groups, 40 bytes per batch for their offsets, the exact batch sums and
-    the count of zero-context requests."""
+    the count of zero-context requests.  The common part grows with the
+    requests by its chunk table and the lists of batches larger than a wave
+    tile (8 bytes per 1,533 requests; 40 per 14,337 and their segments, 8
+    per 8,192 plus 16 per listed batch)."""
     lib = llmv.load()
     nB, N, T = 10_000, 1 << 24, 1024  # N large enough for the largest grid
     base = lib.llmv_sweep_workspace_size(nB, N, T)
     assert base % 256 == 0
     assert base >= lib.llmv_workspace_size(nB, N, T) + 20 * N
-    dn = lib.llmv_sweep_workspace_size(nB, N + (1 << 20), T) - base
-    assert 20 << 20 <= dn <= (20 << 20) + 3 * 8 * ((1 << 20) // 2048) + 8 * 256
+    d = 1 << 20
+    dn = lib.llmv_sweep_workspace_size(nB, N + d, T) - base
+    lists = 8 * (d // 1533 + 1) + 56 * (d // 14337 + 1) + 8 * (d // 8192 + 1)
+    assert 20 << 20 <= dn <= (20 << 20) + 3 * 8 * (d // 2048) + lists + 8 * 256
     db = lib.llmv_sweep_workspace_size(nB + (1 << 16), N, T) - base
     assert 40 << 16 <= db <= (40 << 16) + 3 * 256
     assert lib.llmv_sweep_workspace_size(0, 0, 1) > 0
