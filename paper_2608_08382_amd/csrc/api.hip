@@ -60,9 +60,9 @@ int64_t grid_max_for(int64_t n) {
 
 // Resident workgroups per compute unit for a kernel and its dynamic LDS.
 template <typename K>
-int blocks_per_cu(K kernel, size_t dyn) {
+int blocks_per_cu(K kernel, size_t dyn, int block = kWG) {
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, kWG, dyn) != hipSuccess || nb < 1)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, block, dyn) != hipSuccess || nb < 1)
     nb = 1;
   return nb;
 }
@@ -190,9 +190,11 @@ Layout layout(int64_t n, int32_t T, int rows = 1) {
 // the sweep tiles read past the last group); under the extended model a
 // fourth batch sum and the groups' sums of p*c.
 struct GroupLayout {
-  size_t first, scnt, soff, gofs, bsum, tsum, gw, gf, gr, total;
+  size_t first, scnt, soff, gofs, bsum, tsum, gw, gf, gr, part2, total;
 };
-GroupLayout group_layout(size_t o, int64_t nB, int64_t N, bool ext) {
+// part2: a second set of pass partials ([grid][rows][T], as the Layout's),
+// which a pass writes while the next pass folds the other.
+GroupLayout group_layout(size_t o, int64_t nB, int64_t N, bool ext, int32_t T = 0, int rows = 1) {
   GroupLayout G{};
   const int64_t nS = (N + kSlice - 1) / kSlice;
   const int64_t nt = (nS + kScanTile - 1) / kScanTile;
@@ -214,6 +216,8 @@ GroupLayout group_layout(size_t o, int64_t nB, int64_t N, bool ext) {
   o += align_up((size_t)(N + kGT) * sizeof(v4f));
   G.gr = o;
   if (ext) o += align_up((size_t)(N + kGT) * sizeof(float));
+  G.part2 = o;
+  if (lds_hist(T)) o += align_up((size_t)grid_max_for(N) * (size_t)rows * (size_t)T * sizeof(double));
   G.total = o;
   return G;
 }
@@ -507,7 +511,7 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   // out); each pass keeps G tenant histograms in LDS.
   const int G = sweep_group(n_tenants);
   const Layout L = layout(N, n_tenants, G);
-  const GroupLayout GL = group_layout(L.total, nB, N, EXT);
+  const GroupLayout GL = group_layout(L.total, nB, N, EXT, n_tenants, G);
   rc = check_ws(ws, ws_bytes, GL.total);
   if (rc) return rc;
   char* base = (char*)ws;
@@ -522,7 +526,7 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   }
   const size_t dyn = (size_t)G * (size_t)(n_tenants + kHotSlots) * sizeof(double);
   const SweepKernel<NC> kern = pick_sweep<NC>(G);
-  const int64_t grid = grid_for(N, cus, blocks_per_cu(kern, dyn));
+  const int64_t grid = grid_for(N, cus, blocks_per_cu(kern, dyn, kSweepWG));
   unsigned long long* claims = (unsigned long long*)(base + L.claims);
 
   // the most frequent tenants get replicated histogram entries
@@ -588,7 +592,7 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   // the passes: the chunks of k_tiles over the batches; every launch takes
   // exactly n_chunks claims (one per chunk it runs, the static ones
   // included), so launch i starts at claim i * n_chunks
-  const ChunkMap cm = chunk_map(N, grid * kWaves, false, kCapNarrow);  // one static chunk per wave
+  const ChunkMap cm = chunk_map(N, grid * kSweepWaves, false, kCapNarrow);  // one static chunk per wave
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   rc = partition(trace, cm, wg_first, claims, st);
   if (rc) return rc;
@@ -606,7 +610,15 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
   Q.partials = (double*)(base + L.partials);
   Q.n_tenants = n_tenants;
   Q.hot = hot;
+  // pass i writes partials bufs[i % 2] and folds pass i - 1's from the
+  // other buffer (when its sums fit the fold's mapping); the last pass's, or
+  // every pass's otherwise, go to k_tenant_reduce
+  double* bufs[2] = {(double*)(base + L.partials), (double*)(base + GL.part2)};
+  const bool fold = grid <= (int64_t)kFoldGroups * kFoldRows &&
+                    (int64_t)G * n_tenants <= (int64_t)kFoldPer * grid;
   int64_t launch = 0;
+  int64_t pv0 = 0;  // the previous pass's first setting
+  int32_t pn = 0;   // and its settings
   for (int64_t v0 = 0; v0 < n_var; v0 += G, ++launch) {
     VarTableOf<NC> V{};
     V.n = (int32_t)(n_var - v0 < G ? n_var - v0 : G);
@@ -622,13 +634,23 @@ int sweep_run(const llmv_trace* trace, const llmv_shape* shapes, int32_t n_shape
       }
     }
     Q.claim_base = (uint64_t)launch * (uint64_t)cm.n_chunks;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kWG), dyn, st, Q, V);
+    Q.partials = fold ? bufs[launch & 1] : bufs[0];
+    Q.prev = fold && launch > 0 ? bufs[(launch - 1) & 1] : nullptr;
+    Q.prev_out = out + pv0 * n_tenants;
+    Q.prev_n = pn;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kSweepWG), dyn, st, Q, V);
     HIP_TRY(hipGetLastError(), "k_sweep_groups launch");
-    const int n_hist = V.n * n_tenants;
-    hipLaunchKernelGGL(k_tenant_reduce, dim3((unsigned)((n_hist + kTenantChunk - 1) / kTenantChunk)),
-                       dim3(64 * kReduceWaves), 0, st, (const double*)Q.partials, (int)grid, n_hist,
-                       out + v0 * n_tenants);
-    HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+    const bool last = v0 + G >= n_var;
+    if (!fold || last) {
+      const int n_hist = V.n * n_tenants;
+      hipLaunchKernelGGL(k_tenant_reduce,
+                         dim3((unsigned)((n_hist + kTenantChunk - 1) / kTenantChunk)),
+                         dim3(64 * kReduceWaves), 0, st, (const double*)Q.partials, (int)grid,
+                         n_hist, out + v0 * n_tenants);
+      HIP_TRY(hipGetLastError(), "k_tenant_reduce launch");
+    }
+    pv0 = v0;
+    pn = V.n;
   }
   return LLMV_OK;
 }
@@ -703,8 +725,9 @@ static size_t sweep_ws(int64_t n_batches, int64_t n_requests, int32_t n_tenants,
   const int64_t nB = n_batches > 0 ? n_batches : 0;
   const int64_t n = n_requests > 0 ? n_requests : 0;
   const int32_t T = n_tenants > 0 ? n_tenants : 0;
-  const Layout L = layout(n, T, lds_hist(T) ? sweep_group(T) : 1);
-  return group_layout(L.total, nB, n, ext).total;
+  const int rows = lds_hist(T) ? sweep_group(T) : 1;
+  const Layout L = layout(n, T, rows);
+  return group_layout(L.total, nB, n, ext, T, rows).total;
 }
 
 size_t llmv_sweep_workspace_size(int64_t n_batches, int64_t n_requests, int32_t n_tenants) {

@@ -411,21 +411,44 @@ struct GroupSweep {
   double* partials;                 // [grid][V.n][n_tenants]
   int32_t n_tenants;
   const int32_t* hot;               // [kHot]
+  // the previous pass's partials ([gridDim.x][prev_n][n_tenants], the other
+  // buffer), folded into its output rows by this pass (null: none)
+  const double* prev;
+  double* prev_out;
+  int32_t prev_n;
 };
+
+// Fold of the previous pass inside a pass: workgroup w owns entries
+// [w*kFoldPer, (w+1)*kFoldPer) of the prev_n*n_tenants sums; thread t holds
+// entry t % kFoldPer and rows t/kFoldPer + kFoldGroups*k, k < kFoldRows, loaded
+// at the start of the pass and added after its own work (rows in a fixed
+// order).  Used when prev_n*n_tenants <= kFoldPer*gridDim.x and gridDim.x <=
+// kFoldGroups*kFoldRows.
+constexpr int kFoldPer = 32;
+constexpr int kFoldGroups = 16;  // kSweepWG / kFoldPer
+constexpr int kFoldRows = 16;
+
+// Threads per sweep workgroup: eight waves share one set of NV tenant
+// histograms (one workgroup per compute unit), so a pass writes half as many
+// partial rows as with four-wave workgroups.
+constexpr int kSweepWG = 512;
+constexpr int kSweepWaves = kSweepWG / 64;
+static_assert(kSweepWG == 16 * 32, "the fold's thread mapping");
 
 // NV: histogram rows, i.e. settings per pass, >= V.n; NC: 5 (Eq. 1) or 7
 // (the extended model).  Work: the chunks of k_tiles (one static chunk per
 // wave, then claimed ones).  LDS per workgroup: NV * (n_tenants + kHotSlots)
 // doubles (dynamic) plus the per-wave tables.
 template <int NV, int NC>
-__global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const VarTableOf<NC> V) {
+__global__ __launch_bounds__(kSweepWG) void k_sweep_groups(const GroupSweep P, const VarTableOf<NC> V) {
   constexpr bool EXT = NC == 7;
   constexpr int kGB = kGBof<NC>;
   constexpr int KC = EXT ? 4 : 3;                    // batch-independent constants
   extern __shared__ double s_hist[];                 // [NV][n_tenants + kHotSlots]
-  __shared__ v4f s_kt[kWaves][NV][kGB];              // per wave: (k0, k1, k2, k3)
-  __shared__ float s_kt5[kWaves][EXT ? NV : 1][EXT ? kGB : 1];  // per wave: k5
+  __shared__ v4f s_kt[kSweepWaves][NV][kGB];              // per wave: (k0, k1, k2, k3)
+  __shared__ float s_kt5[kSweepWaves][EXT ? NV : 1][EXT ? kGB : 1];  // per wave: k5
   __shared__ float s_K[NV * 4 * KC];                 // [setting][regime][k1..k3 (, k5)]
+  __shared__ double s_fold[kSweepWG];                // the fold's row groups
   const int tid = threadIdx.x, lane = tid & 63;
   // [setting][batch of the tile]: lanes of one read that hold different
   // batches fall in different banks
@@ -435,13 +458,24 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
   int32_t hot[kHot];
 #pragma unroll
   for (int h = 0; h < kHot; ++h) hot[h] = uni(P.hot[h]);
-  for (int i = tid; i < NV * 4 * KC; i += kWG)
+  for (int i = tid; i < NV * 4 * KC; i += kSweepWG)
     s_K[i] = V.K[i / (4 * KC)][(i / KC) % 4][i % KC];
-  for (int u = tid; u < NV * TS; u += kWG) s_hist[u] = 0.0;
+  // the previous pass's partials of this workgroup's entries, loaded now and
+  // folded after this pass's own work
+  const int64_t fe = (int64_t)blockIdx.x * kFoldPer + tid % kFoldPer;
+  const int frg = tid / kFoldPer;
+  const int64_t fE = (int64_t)P.prev_n * T;
+  double fr[kFoldRows];
+#pragma unroll
+  for (int k = 0; k < kFoldRows; ++k) {
+    const int row = frg + kFoldGroups * k;
+    fr[k] = (P.prev && fe < fE && row < (int)gridDim.x) ? P.prev[(int64_t)row * fE + fe] : 0.0;
+  }
+  for (int u = tid; u < NV * TS; u += kSweepWG) s_hist[u] = 0.0;
   __syncthreads();
 
-  const int64_t workers = (int64_t)gridDim.x * kWaves;
-  int64_t chunk = (int64_t)blockIdx.x * kWaves + (tid >> 6);
+  const int64_t workers = (int64_t)gridDim.x * kSweepWaves;
+  int64_t chunk = (int64_t)blockIdx.x * kSweepWaves + (tid >> 6);
   while (chunk < P.n_chunks) {
     // claim the next chunk now: the value is first read once this one is done
     unsigned long long claim = ~0ull;
@@ -556,7 +590,7 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
   // fold the hot tenants' replicas (fixed order), then flush n_tenants
   // entries per setting
   __syncthreads();
-  for (int i = tid; i < V.n * kHot; i += kWG) {
+  for (int i = tid; i < V.n * kHot; i += kSweepWG) {
     const int g = i / kHot, h = i % kHot;
     if (hot[h] >= 0) {
       double acc = s_hist[g * TS + hot[h]];
@@ -566,7 +600,21 @@ __global__ __launch_bounds__(kWG) void k_sweep_groups(const GroupSweep P, const 
   }
   __syncthreads();
   double* dst = P.partials + (int64_t)blockIdx.x * V.n * T;
-  for (int i = tid; i < V.n * T; i += kWG) dst[i] = s_hist[(i / T) * TS + i % T];
+  for (int i = tid; i < V.n * T; i += kSweepWG) dst[i] = s_hist[(i / T) * TS + i % T];
+
+  // the fold: each thread's rows in order, then the row groups in order
+  if (P.prev) {
+    double acc = fr[0];
+#pragma unroll
+    for (int k = 1; k < kFoldRows; ++k) acc += fr[k];
+    s_fold[frg * kFoldPer + tid % kFoldPer] = acc;
+    __syncthreads();
+    if (frg == 0 && fe < fE) {
+      double t = s_fold[tid];
+      for (int g = 1; g < kFoldGroups; ++g) t += s_fold[g * kFoldPer + tid];
+      P.prev_out[fe] = t;
+    }
+  }
 }
 
 }  // namespace llmv
