@@ -754,6 +754,7 @@ def bench_steps(hip, stream, shape, coeffs, timed, sizes=(1, 64, 256, 1024)):
             torch.cuda.synchronize()
             lat.append(time.perf_counter() - t0)
         g = timed(call, reps=21)
+        per_step = graph_step_time(hip, stream, call, o)
         h = llmv.llmv_attribute_host(st.offsets, st.p, st.c, st.tenant, shape, coeffs,
                                      st.n_tenants)
         # the C entry point called directly (arguments built once: the time
@@ -762,12 +763,49 @@ def bench_steps(hip, stream, shape, coeffs, timed, sizes=(1, 64, 256, 1024)):
         same = all(np.array_equal(o[k].cpu().numpy(), h[k]) for k in ("latency", "regime", "share"))
         assert same, f"step of {n}: GPU and host attributor differ"
         res[str(n)] = {"host_sync_us": float(np.median(lat)) * 1e6, "gpu_clock_us": g * 1e3,
+                       "gpu_clock_us_back_to_back": per_step,
                        "host_attributor_us": float(np.median(hl)) * 1e6,
                        "gpu_equals_host_attributor": same}
         log(f"[bench] step of {n} requests: {res[str(n)]['host_sync_us']:.1f} us "
-            f"host-synchronous, {res[str(n)]['gpu_clock_us']:.1f} us on the GPU's clock; host "
-            f"attributor {res[str(n)]['host_attributor_us']:.1f} us")
+            f"host-synchronous, {res[str(n)]['gpu_clock_us']:.1f} us on the GPU's clock "
+            f"({per_step:.1f} us per step back to back); host attributor "
+            f"{res[str(n)]['host_attributor_us']:.1f} us")
     return res
+
+
+def graph_step_time(hip, stream, call, outs, n_calls=100, replays=5):
+    """GPU time per step when steps are issued back to back: n_calls calls
+    captured in one HIP graph, each replay between HIP events (median);
+    between replays an eager call and a synchronisation, and after each
+    replay every output checked against the eager call's."""
+    import numpy as np
+    import torch
+    call()
+    torch.cuda.synchronize()
+    ref = {k: v.cpu().numpy().copy() for k, v in outs.items()}
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(n_calls):
+            call()
+    torch.cuda.synchronize()
+    per = []
+    for _ in range(replays):
+        call()
+        torch.cuda.synchronize()
+        a, b = hip.create(), hip.create()
+        hip.record(a, stream)
+        graph.replay()
+        hip.record(b, stream)
+        torch.cuda.synchronize()
+        per.append(hip.elapsed_ms(a, b) * 1e3 / n_calls)
+        for k, v in outs.items():
+            got = v.cpu().numpy()
+            if k == "tenant_sums":
+                assert np.allclose(got, ref[k], rtol=1e-12, atol=0.0), "graph replay: " + k
+            else:
+                assert np.array_equal(got, ref[k]), "graph replay: " + k
+    del graph
+    return float(np.median(per))
 
 
 def host_step_times(llmv, st, shape, coeffs, reps):
