@@ -47,10 +47,10 @@ constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histo
 constexpr int kMaxGrid = 1024;                   // persistent workgroups, upper bound (256 CUs x 4)
 constexpr int kTenantChunk = 16;                 // tenants per k_tenant_reduce block
 #ifndef LLMV_STATIC_EIGHTHS
-#define LLMV_STATIC_EIGHTHS 6
+#define LLMV_STATIC_EIGHTHS 7
 #endif
 #ifndef LLMV_DYN_PER_WORKER
-#define LLMV_DYN_PER_WORKER 8
+#define LLMV_DYN_PER_WORKER 4
 #endif
 constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;  // requests in static chunks, in eighths
 constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave worker, at most
