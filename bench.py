@@ -19,6 +19,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "k_tiles_heavy-tailed_counters.json")
+SWEEP_COUNTERS = os.path.join(ROOT, "profiles", "k_sweep_groups_whatif_counters.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_08382_amd", "csrc", f)
                   for f in ("kernels.hpp", "api.hip")]
 
@@ -289,6 +290,17 @@ def bench_sweep(hip, stream, with_oracle):
     res = {"metric": "attributed request-variants/sec", "value": tr.n_requests * variants / (ms / 1e3),
            "unit": "request-variants/s", "ms": ms, "variants": variants,
            "n_requests": tr.n_requests, "n_batches": tr.n_batches, "n_tenants": tr.n_tenants}
+    # the pass kernel's limiting resource, from the committed rocprofv3 counters
+    try:
+        prof = json.load(open(SWEEP_COUNTERS))
+        res["bound"] = {"resource": "lds", "kernel": prof["kernel"],
+                        "frac": prof["lds_busy_frac"],
+                        "frac_definition": "SQ_LDS_IDX_ACTIVE / SQ_BUSY_CU_CYCLES per pass (LDS busy "
+                                           "with the fp64 histogram atomics while the CUs are busy)",
+                        "valu_busy_frac": prof["valu_busy_frac"], "pass_us": prof["pass_us"],
+                        "source": os.path.relpath(SWEEP_COUNTERS, ROOT)}
+    except (OSError, ValueError, KeyError):
+        res["bound"] = None
     log(f"[bench] what-if sweep: {variants} variants in {ms:.2f} ms, "
         f"{res['value']:.3e} request-variants/s")
     if with_oracle:
