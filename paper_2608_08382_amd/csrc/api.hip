@@ -116,14 +116,15 @@ struct Layout {
 
 // Chunks for `workers` wave workers over n requests, for wave tiles of `cap`
 // slots.  When a worker's share is at least min_dyn_share(cap) requests:
-// kStaticEighths/8 of the requests in static chunks, the rest in up to
-// kDynPerWorker claimed chunks per worker of at least min_chunk(cap)
-// requests.  The static part is one chunk per worker, or with `pieces`
-// chunks of piece(cap) requests dealt round-robin (neighbouring
+// eighths/8 of the requests in static chunks, the rest in up to
+// dyn_per_worker (at most kDynPerWorker) claimed chunks per worker of at
+// least min_chunk(cap) requests.  The static part is one chunk per worker,
+// or with `pieces` chunks of piece(cap) requests dealt round-robin (neighbouring
 // waves then stream neighbouring memory).  Otherwise one static chunk per
 // worker and no claims (a claim is a device-wide atomic on one counter;
 // thousands of them cost more than a short launch can win back).
-ChunkMap chunk_map(int64_t n, int64_t workers, bool pieces, int64_t cap) {
+ChunkMap chunk_map(int64_t n, int64_t workers, bool pieces, int64_t cap,
+                   int eighths = kStaticEighths, int dyn_per_worker = kDynPerWorker) {
   const int64_t kPiece = piece(cap), kMinChunk = min_chunk(cap);
   ChunkMap m{};
   m.n_static = workers;
@@ -135,16 +136,16 @@ ChunkMap chunk_map(int64_t n, int64_t workers, bool pieces, int64_t cap) {
     m.n_chunks = workers;
     return m;
   }
-  const int64_t n_static = n / 8 * kStaticEighths / kPiece;
+  const int64_t n_static = n / 8 * eighths / kPiece;
   if (pieces && n_static >= workers) {
     m.n_static = n_static;
     m.s1 = kPiece;
   } else {
-    m.s1 = n / 8 * kStaticEighths / workers;
+    m.s1 = n / 8 * eighths / workers;
   }
   m.F = m.s1 * m.n_static;
   const int64_t rest = n - m.F;
-  int64_t dyn = (int64_t)kDynPerWorker * workers;
+  int64_t dyn = (int64_t)min(dyn_per_worker, kDynPerWorker) * workers;
   if (dyn > rest / kMinChunk) dyn = rest / kMinChunk;
   if (dyn < 1) dyn = 1;
   m.s2 = (rest + dyn - 1) / dyn;
@@ -374,7 +375,14 @@ int run_tiles(int mode, const llmv_trace* tr, Params& P, const VT& V, int32_t T,
   int64_t* wg_first = (int64_t*)(base + L.wg_first);
   const int n_chunks = want_tenant ? (T + kTenantChunk - 1) / kTenantChunk : 0;
 
-  const ChunkMap cm = chunk_map(tr->n_requests, grid * kWaves, true, cap);
+  // When the mean batch is larger than a tile, most requests lie in batches
+  // that the tile kernel only lists for k_long: a chunk then takes a few
+  // microseconds, and chunk setups and claims (device-scope atomics) cost
+  // more than the balance they buy.  One static chunk per wave over all but
+  // the remainder, at most 2 claimed chunks per wave.
+  const bool long_mean = tr->n_requests > tr->n_batches * (int64_t)cap;
+  const ChunkMap cm = long_mean ? chunk_map(tr->n_requests, grid * kWaves, false, cap, 8, 2)
+                                : chunk_map(tr->n_requests, grid * kWaves, true, cap);
   P.wg_first = wg_first;
   P.split_by_count = 0;
   P.claims = (unsigned long long*)(base + L.claims);
