@@ -100,12 +100,13 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 enum { HIST_NONE = 0, HIST_LDS = 1, HIST_GLOBAL = 2 };
 
 // Lane slots of a tile kernel instance: the wide tile where it is faster
-// (Eq. 1 attribution without the tenant cache: 28 slots, about 2% on the
-// heavy-tailed trace; the feature rows and batch sums, about 1%); the narrow
-// one for the extended model and the tenant cache, where the wide tile's
-// registers (up to 255 VGPRs) cost more than its longer tiles gain.
+// (attribution under Eq. 1 or the extended model without the tenant cache:
+// 28 slots, about 2% on the heavy-tailed trace; the feature rows and batch
+// sums, about 1%); the narrow one for the tenant cache, where the wide
+// tile's registers (up to 255 VGPRs) cost more than its longer tiles gain.
 __host__ __device__ constexpr bool wide_tile(int mode, int hist) {
-  return (mode == MODE_ATTR && hist != HIST_GLOBAL) || mode == MODE_FEAT || mode == MODE_SUMS;
+  return (hist != HIST_GLOBAL && (mode == MODE_ATTR || mode == MODE_EXT)) ||
+         mode == MODE_FEAT || mode == MODE_SUMS;
 }
 template <int MODE, int HIST>
 constexpr int kVecOf = wide_tile(MODE, HIST) ? kVecWide : kVecNarrow;

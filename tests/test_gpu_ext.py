@@ -155,7 +155,7 @@ def test_empty_batches(L, pattern):
     check(L, tr, None, tracegen.ext_coeffs(43), tr.n_tenants, pattern)
 
 
-@pytest.mark.parametrize("N", [1, 12287, 12289])
+@pytest.mark.parametrize("N", [1, 12289, 14335, 14336, 14337])
 def test_single_launch_boundary(L, N):
     rng = np.random.default_rng(N + 5)
     sizes = []
