@@ -276,3 +276,26 @@ def test_long_batches_other_modes(L, case):
     ref = oracle.attribute_ext(off, p, c, t, shape, co, 11)
     st = parity.compare(ref, off, g["latency"], g["regime"], g["share"], g["tenant_sums"])
     say(f"[big] ext {case}: {st}")
+
+
+def test_long_mean_full_size(L):
+    """Batches of 1793 requests (one more than a wave tile) over the
+    decode-only trace's 128M requests: the mean batch is larger than a tile,
+    so the tile kernel's work is one static chunk per wave plus claimed
+    chunks (a wave's share passes 32 tiles), listing every batch for k_long.
+    Every latency, regime, share and tenant sum against the oracle."""
+    import torch
+    tr = tracegen.config_trace("decode-only")
+    n = tr.n_requests
+    assert n > 2048 * 32 * 1792
+    off = np.append(np.arange(0, n, 1793, dtype=np.int64), n)
+    say(f"[big] long mean: nB={len(off) - 1} N={n}")
+    dt = L.DeviceTrace.from_host(off, tr.p, tr.c, tr.tenant)
+    shape = tracegen.SHAPES["qwen2.5-14b"]
+    co = tracegen.config_coeffs("decode-only")
+    out = L.attribute(dt, shape, co, tr.n_tenants)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.attribute(off, tr.p, tr.c, tr.tenant, shape, co, tr.n_tenants)
+    st = parity.compare(ref, off, g["latency"], g["regime"], g["share"], g["tenant_sums"])
+    say(f"[big] long mean: {st}")
