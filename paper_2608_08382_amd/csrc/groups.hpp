@@ -444,6 +444,10 @@ __global__ __launch_bounds__(kSweepWG) void k_sweep_groups(const GroupSweep P, c
   constexpr bool EXT = NC == 7;
   constexpr int kGB = kGBof<NC>;
   constexpr int KC = EXT ? 4 : 3;                    // batch-independent constants
+#ifndef LLMV_SWEEP_PRE
+#define LLMV_SWEEP_PRE 1
+#endif
+  constexpr bool PRE = LLMV_SWEEP_PRE && !(EXT && NV == 4);  // registers: no spills
   extern __shared__ double s_hist[];                 // [NV][n_tenants + kHotSlots]
   __shared__ v4f s_kt[kSweepWaves][NV][kGB];              // per wave: (k0, k1, k2, k3)
   __shared__ float s_kt5[kSweepWaves][EXT ? NV : 1][EXT ? kGB : 1];  // per wave: k5
@@ -550,6 +554,31 @@ __global__ __launch_bounds__(kSweepWG) void k_sweep_groups(const GroupSweep P, c
         uint32_t kcur = 0xffffffffu;
         v4f K[NV];
         float K5[EXT ? NV : 1];
+        // PRE: the constants of the batch of the lane's first slot and of
+        // the batch after it are read before the first atomic: a read
+        // between the atomics waits for every atomic before it (LDS
+        // operations of a wave complete in order)
+        v4f KB[PRE ? NV : 1];
+        float KB5[PRE && EXT ? NV : 1];
+        uint32_t kbi = 0xffffffffu;
+        if constexpr (PRE) {
+          uint32_t l0 = ((wv[0] >> kGrpTenantBits) - (uint32_t)b) & kGrpBatchMask;
+          l0 = min(l0, (uint32_t)count - 1u);  // slots before the tile's first group: any batch
+          kcur = l0;
+#pragma unroll
+          for (int g = 0; g < NV; ++g) {
+            K[g] = kt[g][l0];
+            if (EXT) K5[g] = kt5[g][l0];
+          }
+          if (l0 + 1u < (uint32_t)count) {
+            kbi = l0 + 1u;
+#pragma unroll
+            for (int g = 0; g < NV; ++g) {
+              KB[g] = kt[g][kbi];
+              if (EXT) KB5[g] = kt5[g][kbi];
+            }
+          }
+        }
 #pragma unroll
         for (int q = 0; q < kGV; ++q) {
           if (x + q >= g0 && x + q < g1) {
@@ -562,10 +591,18 @@ __global__ __launch_bounds__(kSweepWG) void k_sweep_groups(const GroupSweep P, c
               if (t == hot[h]) e = T + h * kHotRep + (lane & (kHotRep - 1));
             if (lb != kcur) {
               kcur = lb;
+              if (PRE && lb == kbi) {
 #pragma unroll
-              for (int g = 0; g < NV; ++g) {
-                K[g] = kt[g][lb];
-                if (EXT) K5[g] = kt5[g][lb];
+                for (int g = 0; g < NV; ++g) {
+                  K[g] = KB[g];
+                  if (EXT) K5[g] = KB5[g];
+                }
+              } else {
+#pragma unroll
+                for (int g = 0; g < NV; ++g) {
+                  K[g] = kt[g][lb];
+                  if (EXT) K5[g] = kt5[g][lb];
+                }
               }
             }
             const v4f f = fv[q];
