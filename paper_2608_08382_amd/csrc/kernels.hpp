@@ -55,7 +55,10 @@ constexpr int kTenantChunk = 16;                 // tenants per k_tenant_reduce 
 constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;  // requests in static chunks, in eighths
 constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave worker, at most
 // For wave tiles of `cap` request slots:
-constexpr int64_t min_chunk(int64_t cap) { return 4 * cap; }       // requests per claimed chunk, at least
+#ifndef LLMV_MIN_CHUNK_TILES
+#define LLMV_MIN_CHUNK_TILES 2
+#endif
+constexpr int64_t min_chunk(int64_t cap) { return LLMV_MIN_CHUNK_TILES * cap; }  // requests per claimed chunk, at least
 constexpr int64_t min_dyn_share(int64_t cap) { return 32 * cap; }  // per worker, for claimed chunks
 constexpr int64_t piece(int64_t cap) { return 16 * cap; }          // requests per static piece
 
