@@ -60,7 +60,10 @@ constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave 
 #endif
 constexpr int64_t min_chunk(int64_t cap) { return LLMV_MIN_CHUNK_TILES * cap; }  // requests per claimed chunk, at least
 constexpr int64_t min_dyn_share(int64_t cap) { return 32 * cap; }  // per worker, for claimed chunks
-constexpr int64_t piece(int64_t cap) { return 16 * cap; }          // requests per static piece
+#ifndef LLMV_PIECE_TILES
+#define LLMV_PIECE_TILES 8
+#endif
+constexpr int64_t piece(int64_t cap) { return LLMV_PIECE_TILES * cap; }  // requests per static piece
 
 // Chunks of the tile kernel's work.  Chunk w < n_static (static) starts at
 // request w*s1; chunk n_static + j (claimed) starts at request F + j*s2,
