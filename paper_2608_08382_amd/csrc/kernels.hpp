@@ -46,24 +46,25 @@ constexpr int kCapNarrow = 64 * kVecNarrow;  // request slots per narrow wave ti
 constexpr int kHistLdsMax = 4096;                // tenants held in an LDS histogram
 constexpr int kMaxGrid = 1024;                   // persistent workgroups, upper bound (256 CUs x 4)
 constexpr int kTenantChunk = 16;                 // tenants per k_tenant_reduce block
+// Work split of the tile kernel (build-time settings, for measurement)
 #ifndef LLMV_STATIC_EIGHTHS
-#define LLMV_STATIC_EIGHTHS 7
+#define LLMV_STATIC_EIGHTHS 7  // requests in static chunks, in eighths
 #endif
 #ifndef LLMV_DYN_PER_WORKER
-#define LLMV_DYN_PER_WORKER 4
+#define LLMV_DYN_PER_WORKER 4  // claimed chunks per wave worker, at most
 #endif
-constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;  // requests in static chunks, in eighths
-constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;   // claimed chunks per wave worker, at most
-// For wave tiles of `cap` request slots:
 #ifndef LLMV_MIN_CHUNK_TILES
-#define LLMV_MIN_CHUNK_TILES 2
+#define LLMV_MIN_CHUNK_TILES 2  // tiles per claimed chunk, at least
 #endif
+#ifndef LLMV_PIECE_TILES
+#define LLMV_PIECE_TILES 8  // tiles per static piece
+#endif
+constexpr int kStaticEighths = LLMV_STATIC_EIGHTHS;
+constexpr int kDynPerWorker = LLMV_DYN_PER_WORKER;
+// For wave tiles of `cap` request slots:
 constexpr int64_t min_chunk(int64_t cap) { return LLMV_MIN_CHUNK_TILES * cap; }  // requests per claimed chunk, at least
 constexpr int64_t min_dyn_share(int64_t cap) { return 32 * cap; }  // per worker, for claimed chunks
-#ifndef LLMV_PIECE_TILES
-#define LLMV_PIECE_TILES 8
-#endif
-constexpr int64_t piece(int64_t cap) { return LLMV_PIECE_TILES * cap; }  // requests per static piece
+constexpr int64_t piece(int64_t cap) { return LLMV_PIECE_TILES * cap; }       // requests per static piece
 
 // Chunks of the tile kernel's work.  Chunk w < n_static (static) starts at
 // request w*s1; chunk n_static + j (claimed) starts at request F + j*s2,
