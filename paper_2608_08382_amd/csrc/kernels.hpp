@@ -574,25 +574,40 @@ __device__ __forceinline__ void load_slots(const Params& P, int64_t x, int32_t* 
 // Writes one round of shares staged lane-major in the wave's LDS stage
 // (lane l: slots s0 + kVec*l .. s0 + kVec*l + kVec-1, pitch kStagePitch) so
 // that every global store instruction writes 1 KB of consecutive shares.
-// Only slots in [xf, L) are written.
-template <int VEC>
+// Only slots in [xf, L) are written.  BATCH: every group's stage read is
+// issued before the first store, so that the reads wait once (a wave's LDS
+// operations complete in order, behind the round's tenant-sum atomics)
+// instead of once per store; it holds the round's shares in 28 more
+// registers, which the tile kernel affords and k_long (at its register
+// limit) does not.
+template <int VEC, bool BATCH>
 __device__ __forceinline__ void store_round(const Params& P, float* stage, int64_t ra, int32_t s0,
                                             int32_t xf, int32_t L) {
   LLMV_TILE_CONSTANTS(VEC);
   const int lane = threadIdx.x & 63;
   wave_lds_sync();
+  // the round's shares of this lane's store groups: read all at once (BATCH)
+  // or each before its store
+  v4f val[BATCH ? kVec / 4 : 1];
+  if constexpr (BATCH) {
+#pragma unroll
+    for (int g = 0; g < kVec / 4; ++g) {
+      const int32_t e = 256 * g + 4 * lane;
+      val[g] = *(const v4f*)&stage[(e / kVec) * kStagePitch + (e % kVec)];
+    }
+  }
 #pragma unroll
   for (int g = 0; g < kVec / 4; ++g) {
     if (256 * g >= L - s0) break;          // no slot of the round left (wave-uniform)
     const int32_t e = 256 * g + 4 * lane;  // slot within the round
     const int32_t x = s0 + e;              // slot within the tile
-    const float* src = &stage[(e / kVec) * kStagePitch + (e % kVec)];
+    const v4f v = BATCH ? val[BATCH ? g : 0] : *(const v4f*)&stage[(e / kVec) * kStagePitch + (e % kVec)];
     if (x >= xf && x + 4 <= L) {
-      __builtin_nontemporal_store(*(const v4f*)src, (v4f*)(P.share + ra + x));  // not re-read
+      __builtin_nontemporal_store(v, (v4f*)(P.share + ra + x));  // not re-read
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (x + q >= xf && x + q < L) P.share[ra + x + q] = src[q];
+        if (x + q >= xf && x + q < L) P.share[ra + x + q] = v[q];
     }
   }
   wave_lds_sync();
@@ -730,7 +745,7 @@ __device__ __forceinline__ void long_batch(const Params& P, const typename VarsO
       }
       if (STAGE) *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
     }
-    if (STAGE) store_round<VEC>(P, stage, ra, r * kRoundSlots, xf, L);
+    if (STAGE) store_round<VEC, false>(P, stage, ra, r * kRoundSlots, xf, L);
   };
 
   int32_t p0[kVec], c0[kVec], t0[kVec];
@@ -1141,7 +1156,7 @@ __global__ __launch_bounds__(kWG) void k_tiles(const Params P,
               if (kAttrMode<MODE> && SHARE)
                 *(v4f*)&stage[lane * kStagePitch + 4 * g] = (v4f){sv[0], sv[1], sv[2], sv[3]};
             }
-            if (kAttrMode<MODE> && SHARE) store_round<VEC>(P, stage, ra, r * kRoundSlots, xf, L);
+            if (kAttrMode<MODE> && SHARE) store_round<VEC, true>(P, stage, ra, r * kRoundSlots, xf, L);
           }
         }
         wave_lds_sync();
