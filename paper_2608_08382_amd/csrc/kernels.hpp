@@ -527,9 +527,11 @@ __device__ __forceinline__ double uni_f64(double v) {
   return __builtin_bit_cast(double, (uint64_t)uni((int64_t)__builtin_bit_cast(uint64_t, v)));
 }
 
+// The sum over the 64 lanes (integer, modulo 2^64), wave-uniform.  DPP
+// steps (no LDS): a shuffle would go through the LDS and wait behind the
+// wave's LDS atomics.
 __device__ __forceinline__ uint64_t wave_sum(uint64_t x) {
-  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
-  return x;
+  return readlane_u64(wave_incl_scan(x), 63);
 }
 
 __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
