@@ -526,6 +526,34 @@ def test_sweep_tenant_counts(L, case):
             assert e.max() <= parity.RTOL, (case, s_, v, e.max())
 
 
+@pytest.mark.parametrize("ext", [False, True])
+def test_sweep_tiny_batches(L, ext):
+    """Batches of 0 to 3 requests (1 to 3 groups each), so that a lane's
+    run of groups spans many batches: the pass kernel reads the constants of
+    a lane's first two batches ahead and every later batch inside its loop.
+    Every setting's tenant sums against the oracle."""
+    import torch
+    rng = np.random.default_rng(404 + ext)
+    sizes = rng.integers(0, 4, 6000)
+    tr = random_fill(rng, sizes, n_tenants=37)
+    shapes = [tracegen.SHAPES["llama3.1-8b"]]
+    dt = L.DeviceTrace.from_host(tr.offsets, tr.p, tr.c, tr.tenant)
+    if ext:
+        co = np.stack([tracegen.ext_coeffs(700 + j) for j in range(9)])
+        out = L.attribute_sweep(dt, shapes, co, tr.n_tenants, ext=True)
+    else:
+        co = tracegen.sweep_coeffs(tracegen.base_coeffs(78), 9)
+        out = L.attribute_sweep(dt, shapes, co, tr.n_tenants)
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    for v in range(9):
+        f = oracle.attribute_ext if ext else oracle.attribute
+        ref = f(tr.offsets, tr.p, tr.c, tr.tenant, shapes[0], co[v], tr.n_tenants,
+                ("tenant_sums",))["tenant_sums"]
+        e = parity.rel_err(out[0, v], ref)
+        assert e.max() <= parity.RTOL, (ext, v, e.max())
+
+
 def test_sweep_unit_shape_and_hand_coeffs(L):
     tt = HAND["tenant_trace"]
     by = {e["name"]: e for e in HAND["unit_shape_examples"]}
