@@ -631,13 +631,16 @@ __device__ __forceinline__ v4i load4(__amdgpu_buffer_rsrc_t r, int32_t elem) {
 // Slots x .. x+VEC-1 (x = VEC * lane) of one round of a long batch: p, c
 // (and tenant) through buffers over the round's m slots, so that slots past
 // the batch read as 0 without a memory access.
-template <int VEC, bool TENANT>
+// NG: the groups of 4 slots loaded (the rest are zero), all of them unless a
+// round is known to hold at most 4*NG slots.
+template <int VEC, bool TENANT, int NG = VEC / 4>
 __device__ __forceinline__ void load_round(const Params& P, int64_t o, int64_t m, int32_t x,
                                            int32_t* pv, int32_t* cv, int32_t* tv) {
   const auto bp = elem_rsrc(P.p + o, m), bc = elem_rsrc(P.c + o, m);
 #pragma unroll
   for (int g = 0; g < VEC / 4; ++g) {
-    const v4i a = load4(bp, x + 4 * g), d = load4(bc, x + 4 * g);
+    const v4i z = {0, 0, 0, 0};
+    const v4i a = g < NG ? load4(bp, x + 4 * g) : z, d = g < NG ? load4(bc, x + 4 * g) : z;
     pv[4 * g] = a.x; pv[4 * g + 1] = a.y; pv[4 * g + 2] = a.z; pv[4 * g + 3] = a.w;
     cv[4 * g] = d.x; cv[4 * g + 1] = d.y; cv[4 * g + 2] = d.z; cv[4 * g + 3] = d.w;
   }
@@ -645,7 +648,7 @@ __device__ __forceinline__ void load_round(const Params& P, int64_t o, int64_t m
     const auto bt = elem_rsrc(P.tenant + o, m);
 #pragma unroll
     for (int g = 0; g < VEC / 4; ++g) {
-      const v4i t = load4(bt, x + 4 * g);
+      const v4i t = g < NG ? load4(bt, x + 4 * g) : (v4i){0, 0, 0, 0};
       tv[4 * g] = t.x; tv[4 * g + 1] = t.y; tv[4 * g + 2] = t.z; tv[4 * g + 3] = t.w;
     }
   }
@@ -754,7 +757,13 @@ __device__ __forceinline__ void long_batch(const Params& P, const typename VarsO
   load_round<VEC, TEN>(P, o_of(0), m_of(0), x0, p0, c0, t0);
   if (nr == 2) {
     int32_t p1[kVec], c1[kVec], t1[kVec];
-    load_round<VEC, TEN>(P, o_of(1), m_of(1), x0, p1, c1, t1);
+    // a second round of at most 4 slots (a batch just over a tile) sits in
+    // lane 0's first group: one load per array instead of VEC/4 (not with
+    // the tenant cache, where the second path would spill)
+    if (HIST != HIST_GLOBAL && m_of(1) <= 4)
+      load_round<VEC, TEN, 1>(P, o_of(1), m_of(1), x0, p1, c1, t1);
+    else
+      load_round<VEC, TEN>(P, o_of(1), m_of(1), x0, p1, c1, t1);
     add(p0, c0, 0);
     add(p1, c1, 1);
     model();
